@@ -1,0 +1,505 @@
+"""Benchmark of the Pixelated Butterfly hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole hot path over one batch of synthetic input
+that is already resident in HBM:
+  linear workloads   forward (T_lr = X V^T, Y = X (M o W)^T + T_lr U^T),
+                     backward-data (S = dY U, dX = dY (M o W) + S V) and
+                     backward-weight (dW on the mask, dU, dV);
+  mlp_pair           both layers with the GELU epilogues, forward + backward;
+  attention          block-sparse attention forward + backward.
+Prints ONE JSON line.  `value` is nonzero-block TFLOP/s of the step (only the
+kept b x b blocks' FLOPs of the three block-sparse products, or of the six
+attention block products), the metric of the workload table.  The same line
+carries the fraction of the bf16 MFMA peak, the speedup over the dense layer
+of the same shape run with the library's own dense MFMA GEMM, per-call times
+measured with HIP events on the compute stream, a roofline entry for the
+dominant call, and the CPU oracle timed on a bounded sample of the workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+METRIC = "nonzero-block TFLOP/s fwd+bwd and % bf16 MFMA peak; speedup vs dense GEMM"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (no sparsity)
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+RIDGE_BF16 = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="mlp_fc1_768x3072", choices=sorted(synth.WORKLOADS))
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--calls-only", default="", help="comma list of calls to loop (profiling aid)")
+    return p.parse_args()
+
+
+class Timer:
+    """HIP events on the compute stream between the calls of a step."""
+
+    def __init__(self, torch, names):
+        self.torch = torch
+        self.names = names
+        self.ev = []
+
+    def step_events(self):
+        e = [self.torch.cuda.Event(enable_timing=True) for _ in range(len(self.names) + 1)]
+        self.ev.append(e)
+        return e
+
+    def per_call_ms(self):
+        out = {n: 0.0 for n in self.names}
+        for e in self.ev:
+            for i, n in enumerate(self.names):
+                out[n] += e[i].elapsed_time(e[i + 1])
+        return {n: v / max(1, len(self.ev)) for n, v in out.items()}
+
+
+def dev_bf16(torch, raw):
+    return torch.from_numpy(raw.view(np.int16).copy()).cuda().view(torch.bfloat16)
+
+
+def dev_any(torch, raw):
+    if raw.dtype == np.uint16:
+        return dev_bf16(torch, raw)
+    return torch.from_numpy(raw).cuda()
+
+
+# ---------------------------------------------------------------------------
+# Linear layer workloads
+# ---------------------------------------------------------------------------
+class Linear:
+    calls = ["fwd", "bwd_data", "bwd_weight"]
+
+    def __init__(self, torch, pf, wl, seed=0):
+        self.torch, self.pf, self.wl = torch, pf, wl
+        T, K, N, b, ms, r, dt = wl.T, wl.K, wl.N, wl.b, wl.max_stride, wl.r, wl.dtype
+        self.L = pf.pf_layout_create(N, K, b, ms)
+        pf.pf_layout_upload(self.L)
+        self.nnzb = pf.pf_layout_info_get(self.L)["nnzb"]
+        dr = lambda shape, std, stream: dev_any(torch, synth.draw(shape, std, seed, stream, dt)[1])
+        self.X = dr((T, K), wl.std_x, 1)
+        self.W = dr((self.nnzb, b, b), wl.std_w, 2)
+        self.U = dr((N, r), wl.std_uv, 3)
+        self.V = dr((r, K), wl.std_uv, 4)
+        self.dY = dr((T, N), wl.std_dy, 5)
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        e = lambda *s: torch.empty(*s, dtype=tdt, device="cuda")
+        self.Y, self.Tl, self.S, self.dX = e(T, N), e(T, r), e(T, r), e(T, K)
+        self.dW, self.dU, self.dV = torch.empty_like(self.W), e(N, r), e(r, K)
+        self.wsb = pf.pf_workspace_bytes(self.L, T, r, dt)
+        self.ws = torch.empty(max(self.wsb, 256), dtype=torch.uint8, device="cuda")
+        self.dtype = dt
+
+    def call(self, name):
+        pf, T, r, dt = self.pf, self.wl.T, self.wl.r, self.dtype
+        if name == "fwd":
+            pf.pf_linear_fwd(self.L, dt, T, r, self.X, self.W, self.U, self.V, self.Y, self.Tl)
+        elif name == "bwd_data":
+            pf.pf_linear_bwd_data(self.L, dt, T, r, self.dY, self.W, self.U, self.V, self.S, self.dX)
+        else:
+            pf.pf_linear_bwd_weight(self.L, dt, T, r, self.dY, self.X, self.Tl, self.S, self.dW,
+                                    self.dU, self.dV, self.ws, self.wsb)
+
+    def flops(self):
+        wl = self.wl
+        sparse = 3 * 2 * wl.T * self.nnzb * wl.b * wl.b
+        lowrank = 3 * 2 * wl.T * wl.r * (wl.K + wl.N)
+        dense = 3 * 2 * wl.T * wl.N * wl.K
+        return sparse, lowrank, dense
+
+    def call_work(self, name):
+        """(flops, algorithmic bytes) of one call: each operand read once,
+        each output written once."""
+        wl, e = self.wl, (2 if self.dtype == "bf16" else 4)
+        T, K, N, r, w = wl.T, wl.K, wl.N, wl.r, self.nnzb * wl.b * wl.b
+        fl = 2 * T * w + 2 * T * r * (K + N)
+        if name == "fwd":
+            by = T * K + w + N * r + r * K + T * N + T * r
+        elif name == "bwd_data":
+            by = T * N + w + N * r + r * K + T * K + T * r
+        else:
+            by = T * N + T * K + 2 * T * r + w + N * r + r * K
+        return fl, by * e
+
+    def dense_setup(self):
+        torch, wl = self.torch, self.wl
+        tdt = torch.bfloat16 if self.dtype == "bf16" else torch.float32
+        self.Wd = torch.randn(wl.N, wl.K, dtype=tdt, device="cuda") * 0.02
+        self.Yd = torch.empty(wl.T, wl.N, dtype=tdt, device="cuda")
+        self.dXd = torch.empty(wl.T, wl.K, dtype=tdt, device="cuda")
+        self.dWd = torch.empty(wl.N, wl.K, dtype=tdt, device="cuda")
+        self.dwsb = self.pf.pf_dense_workspace_bytes(self.dtype, self.pf.PF_OP_TN, wl.N, wl.K, wl.T)
+        self.dws = torch.empty(max(self.dwsb, 256), dtype=torch.uint8, device="cuda")
+
+    def dense_step(self):
+        pf, wl, dt = self.pf, self.wl, self.dtype
+        pf.pf_dense_gemm(dt, pf.PF_OP_NT, wl.T, wl.N, wl.K, self.X, self.Wd, self.Yd)
+        pf.pf_dense_gemm(dt, pf.PF_OP_NN, wl.T, wl.K, wl.N, self.dY, self.Wd, self.dXd)
+        pf.pf_dense_gemm(dt, pf.PF_OP_TN, wl.N, wl.K, wl.T, self.dY, self.X, self.dWd,
+                         self.dws, self.dwsb)
+
+    def torch_dense_step(self):
+        torch = self.torch
+        torch.matmul(self.X, self.Wd.t(), out=self.Yd)
+        torch.matmul(self.dY, self.Wd, out=self.dXd)
+        torch.matmul(self.dY.t(), self.X, out=self.dWd)
+
+    def cpu_baseline(self, budget_s=12.0):
+        """The fp64 oracle (dense masked) on the same workload shape for a
+        bounded number of tokens; rate in nonzero-block TFLOP/s."""
+        from oracle import linear as ol
+        from oracle import mask as om
+        wl = self.wl
+        M, (row_ptr, col_idx, *_x) = om.layout(wl.N, wl.K, wl.b, wl.max_stride)
+        Mel = om.element_mask(M, wl.b)
+        Ts = min(wl.T, 1024)
+        X = synth.draw((Ts, wl.K), wl.std_x, 0, 1, wl.dtype)[0]
+        W = synth.draw((int(M.sum()), wl.b, wl.b), wl.std_w, 0, 2, wl.dtype)[0]
+        U = synth.draw((wl.N, wl.r), wl.std_uv, 0, 3, wl.dtype)[0]
+        V = synth.draw((wl.r, wl.K), wl.std_uv, 0, 4, wl.dtype)[0]
+        dY = synth.draw((Ts, wl.N), wl.std_dy, 0, 5, wl.dtype)[0]
+        Wd = ol.unpack(W, row_ptr, col_idx, wl.N // wl.b, wl.K // wl.b, wl.b)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            ol.forward(X, Wd, U, V)
+            ol.backward(X, Wd, Mel, dY, U, V)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 1000:
+                break
+        fl = 3 * 2 * Ts * int(M.sum()) * wl.b * wl.b * reps
+        return fl / el / 1e12, f"oracle fwd+bwd (fp64, dense masked) on {Ts} of {wl.T} tokens x {reps} reps, {el:.1f} s"
+
+
+class MlpPair(Linear):
+    calls = ["fwd1", "fwd2", "bwd_data2", "bwd_weight2", "bwd_data1", "bwd_weight1"]
+
+    def __init__(self, torch, pf, wl, seed=0):
+        self.torch, self.pf, self.wl, self.dtype = torch, pf, wl, wl.dtype
+        T, K, N, b, ms, r = wl.T, wl.K, wl.N, wl.b, wl.max_stride, wl.r
+        self.L1 = pf.pf_layout_create(N, K, b, ms)
+        self.L2 = pf.pf_layout_create(K, N, b, ms)
+        pf.pf_layout_upload(self.L1)
+        pf.pf_layout_upload(self.L2)
+        self.nnzb1 = pf.pf_layout_info_get(self.L1)["nnzb"]
+        self.nnzb2 = pf.pf_layout_info_get(self.L2)["nnzb"]
+        dr = lambda shape, st, s: dev_bf16(torch, synth.draw(shape, st, seed, s, "bf16")[1])
+        self.X = dr((T, K), wl.std_x, 1)
+        self.W1, self.U1, self.V1 = dr((self.nnzb1, b, b), wl.std_w, 2), dr((N, r), wl.std_uv, 3), dr((r, K), wl.std_uv, 4)
+        self.W2, self.U2, self.V2 = dr((self.nnzb2, b, b), wl.std_w, 6), dr((K, r), wl.std_uv, 7), dr((r, N), wl.std_uv, 8)
+        self.dY = dr((T, K), wl.std_dy, 5)
+        e = lambda *s: torch.empty(*s, dtype=torch.bfloat16, device="cuda")
+        self.Hpre, self.H, self.T1, self.Y, self.T2 = e(T, N), e(T, N), e(T, r), e(T, K), e(T, r)
+        self.dHpre, self.S2, self.dX, self.S1 = e(T, N), e(T, r), e(T, K), e(T, r)
+        self.dW1, self.dU1, self.dV1 = torch.empty_like(self.W1), e(N, r), e(r, K)
+        self.dW2, self.dU2, self.dV2 = torch.empty_like(self.W2), e(K, r), e(r, N)
+        self.wsb = max(pf.pf_workspace_bytes(self.L1, T, r, "bf16"), pf.pf_workspace_bytes(self.L2, T, r, "bf16"))
+        self.ws = torch.empty(max(self.wsb, 256), dtype=torch.uint8, device="cuda")
+        self.nnzb = self.nnzb1
+
+    def call(self, name):
+        pf, T, r, dt = self.pf, self.wl.T, self.wl.r, "bf16"
+        if name == "fwd1":
+            pf.pf_linear_fwd(self.L1, dt, T, r, self.X, self.W1, self.U1, self.V1, self.H, self.T1,
+                             pf.PF_EPI_GELU, self.Hpre)
+        elif name == "fwd2":
+            pf.pf_linear_fwd(self.L2, dt, T, r, self.H, self.W2, self.U2, self.V2, self.Y, self.T2)
+        elif name == "bwd_data2":
+            pf.pf_linear_bwd_data(self.L2, dt, T, r, self.dY, self.W2, self.U2, self.V2, self.S2,
+                                  self.dHpre, pf.PF_EPI_GELU, self.Hpre)
+        elif name == "bwd_weight2":
+            pf.pf_linear_bwd_weight(self.L2, dt, T, r, self.dY, self.H, self.T2, self.S2, self.dW2,
+                                    self.dU2, self.dV2, self.ws, self.wsb)
+        elif name == "bwd_data1":
+            pf.pf_linear_bwd_data(self.L1, dt, T, r, self.dHpre, self.W1, self.U1, self.V1, self.S1, self.dX)
+        else:
+            pf.pf_linear_bwd_weight(self.L1, dt, T, r, self.dHpre, self.X, self.T1, self.S1, self.dW1,
+                                    self.dU1, self.dV1, self.ws, self.wsb)
+
+    def flops(self):
+        wl = self.wl
+        sparse = 3 * 2 * wl.T * (self.nnzb1 + self.nnzb2) * wl.b * wl.b
+        lowrank = 2 * 3 * 2 * wl.T * wl.r * (wl.K + wl.N)
+        dense = 2 * 3 * 2 * wl.T * wl.N * wl.K
+        return sparse, lowrank, dense
+
+    def call_work(self, name):
+        wl = self.wl
+        T, r = wl.T, wl.r
+        K, N, nz = (wl.K, wl.N, self.nnzb1) if name.endswith("1") else (wl.N, wl.K, self.nnzb2)
+        w = nz * wl.b * wl.b
+        fl = 2 * T * w + 2 * T * r * (K + N)
+        gelu = T * wl.N  # the extra pre-activation tensor
+        if name.startswith("fwd"):
+            by = T * K + w + N * r + r * K + T * N + T * r + (gelu if name == "fwd1" else 0)
+        elif name.startswith("bwd_data"):
+            by = T * N + w + N * r + r * K + T * K + T * r + (gelu if name == "bwd_data2" else 0)
+        else:
+            by = T * N + T * K + 2 * T * r + w + N * r + r * K
+        return fl, 2 * by
+
+    def dense_setup(self):
+        torch, wl = self.torch, self.wl
+        bf = dict(dtype=torch.bfloat16, device="cuda")
+        self.Wd1 = torch.randn(wl.N, wl.K, **bf) * 0.02
+        self.Wd2 = torch.randn(wl.K, wl.N, **bf) * 0.02
+        self.Hd, self.Yd = torch.empty(wl.T, wl.N, **bf), torch.empty(wl.T, wl.K, **bf)
+        self.dHd, self.dXd = torch.empty(wl.T, wl.N, **bf), torch.empty(wl.T, wl.K, **bf)
+        self.dW1d, self.dW2d = torch.empty(wl.N, wl.K, **bf), torch.empty(wl.K, wl.N, **bf)
+        self.dwsb = max(self.pf.pf_dense_workspace_bytes("bf16", self.pf.PF_OP_TN, wl.N, wl.K, wl.T),
+                        self.pf.pf_dense_workspace_bytes("bf16", self.pf.PF_OP_TN, wl.K, wl.N, wl.T))
+        self.dws = torch.empty(max(self.dwsb, 256), dtype=torch.uint8, device="cuda")
+
+    def dense_step(self):
+        pf, wl, d = self.pf, self.wl, "bf16"
+        T, K, N = wl.T, wl.K, wl.N
+        pf.pf_dense_gemm(d, pf.PF_OP_NT, T, N, K, self.X, self.Wd1, self.Hd)
+        pf.pf_dense_gemm(d, pf.PF_OP_NT, T, K, N, self.Hd, self.Wd2, self.Yd)
+        pf.pf_dense_gemm(d, pf.PF_OP_NN, T, N, K, self.dY, self.Wd2, self.dHd)
+        pf.pf_dense_gemm(d, pf.PF_OP_TN, K, N, T, self.dY, self.Hd, self.dW2d, self.dws, self.dwsb)
+        pf.pf_dense_gemm(d, pf.PF_OP_NN, T, K, N, self.dHd, self.Wd1, self.dXd)
+        pf.pf_dense_gemm(d, pf.PF_OP_TN, N, K, T, self.dHd, self.X, self.dW1d, self.dws, self.dwsb)
+
+    def torch_dense_step(self):
+        torch = self.torch
+        torch.matmul(self.X, self.Wd1.t(), out=self.Hd)
+        torch.matmul(self.Hd, self.Wd2.t(), out=self.Yd)
+        torch.matmul(self.dY, self.Wd2, out=self.dHd)
+        torch.matmul(self.dY.t(), self.Hd, out=self.dW2d)
+        torch.matmul(self.dHd, self.Wd1, out=self.dXd)
+        torch.matmul(self.dHd.t(), self.X, out=self.dW1d)
+
+    def cpu_baseline(self, budget_s=12.0):
+        from oracle import linear as ol
+        from oracle import mask as om
+        wl = self.wl
+        M1, (rp1, ci1, *_a) = om.layout(wl.N, wl.K, wl.b, wl.max_stride)
+        M2, (rp2, ci2, *_b) = om.layout(wl.K, wl.N, wl.b, wl.max_stride)
+        Ts = min(wl.T, 512)
+        g = lambda shape, st, s: synth.draw(shape, st, 0, s, "bf16")[0]
+        X, dY = g((Ts, wl.K), wl.std_x, 1), g((Ts, wl.K), wl.std_dy, 5)
+        W1 = ol.unpack(g((int(M1.sum()), wl.b, wl.b), wl.std_w, 2), rp1, ci1, wl.N // wl.b, wl.K // wl.b, wl.b)
+        W2 = ol.unpack(g((int(M2.sum()), wl.b, wl.b), wl.std_w, 6), rp2, ci2, wl.K // wl.b, wl.N // wl.b, wl.b)
+        U1, V1 = g((wl.N, wl.r), wl.std_uv, 3), g((wl.r, wl.K), wl.std_uv, 4)
+        U2, V2 = g((wl.K, wl.r), wl.std_uv, 7), g((wl.r, wl.N), wl.std_uv, 8)
+        E1, E2 = om.element_mask(M1, wl.b), om.element_mask(M2, wl.b)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            ol.mlp_pair_backward(X, W1, E1, U1, V1, W2, E2, U2, V2, dY)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 1000:
+                break
+        fl = 3 * 2 * Ts * (int(M1.sum()) + int(M2.sum())) * wl.b * wl.b * reps
+        return fl / el / 1e12, f"oracle 2-layer fwd+bwd (fp64, dense masked) on {Ts} of {wl.T} tokens x {reps} reps, {el:.1f} s"
+
+
+# ---------------------------------------------------------------------------
+# Attention workload
+# ---------------------------------------------------------------------------
+class Attention:
+    calls = ["attn_fwd", "attn_bwd"]
+
+    def __init__(self, torch, pf, wl, seed=0):
+        self.torch, self.pf, self.wl, self.dtype = torch, pf, wl, "bf16"
+        B, H, S, d = wl.B, wl.H, wl.S, wl.d
+        self.L = pf.pf_layout_create(S, S, wl.b, wl.max_stride)
+        pf.pf_layout_upload(self.L)
+        self.nnzb = pf.pf_layout_info_get(self.L)["nnzb"]
+        dr = lambda s: dev_bf16(torch, synth.draw((B, H, S, d), 1.0, seed, s, "bf16")[1])
+        self.Q, self.K, self.V, self.dO = dr(11), dr(12), dr(13), dr(14)
+        self.O = torch.empty_like(self.Q)
+        self.lse = torch.empty(B, H, S, dtype=torch.float32, device="cuda")
+        self.dQ, self.dK, self.dV = torch.empty_like(self.Q), torch.empty_like(self.Q), torch.empty_like(self.Q)
+        self.wsb = pf.pf_attn_workspace_bytes(B, H, S)
+        self.ws = torch.empty(self.wsb, dtype=torch.uint8, device="cuda")
+        self.scale = 1.0 / np.sqrt(d)
+
+    def call(self, name):
+        pf, wl = self.pf, self.wl
+        if name == "attn_fwd":
+            pf.pf_attn_fwd(self.L, wl.B, wl.H, wl.S, wl.d, self.scale, self.Q, self.K, self.V, self.O, self.lse)
+        else:
+            pf.pf_attn_bwd(self.L, wl.B, wl.H, wl.S, wl.d, self.scale, self.Q, self.K, self.V, self.O,
+                           self.lse, self.dO, self.dQ, self.dK, self.dV, self.ws, self.wsb)
+
+    def flops(self):
+        wl = self.wl
+        per = 2 * wl.b * wl.b * wl.d * self.nnzb * wl.B * wl.H
+        return 6 * per, 0, 6 * 2 * wl.S * wl.S * wl.d * wl.B * wl.H
+
+    def call_work(self, name):
+        wl = self.wl
+        per = 2 * wl.b * wl.b * wl.d * self.nnzb * wl.B * wl.H
+        t = wl.B * wl.H * wl.S * wl.d * 2
+        rows = wl.B * wl.H * wl.S * 4
+        if name == "attn_fwd":
+            return 2 * per, 4 * t + rows
+        return 4 * per, 7 * t + rows
+
+    def dense_setup(self):
+        torch, wl = self.torch, self.wl
+        nb = wl.S // wl.b  # every block kept: the dense attention of the same shape
+        self.Ld = self.pf.pf_layout_create_from_mask(nb, nb, wl.b, np.ones((nb, nb), bool))
+        self.pf.pf_layout_upload(self.Ld)
+
+    def dense_step(self):
+        pf, wl = self.pf, self.wl
+        pf.pf_attn_fwd(self.Ld, wl.B, wl.H, wl.S, wl.d, self.scale, self.Q, self.K, self.V, self.O, self.lse)
+        pf.pf_attn_bwd(self.Ld, wl.B, wl.H, wl.S, wl.d, self.scale, self.Q, self.K, self.V, self.O,
+                       self.lse, self.dO, self.dQ, self.dK, self.dV, self.ws, self.wsb)
+
+    def torch_dense_step(self):
+        pass
+
+    def cpu_baseline(self, budget_s=12.0):
+        from oracle import attention as oa
+        from oracle import mask as om
+        wl = self.wl
+        M, _ = om.layout(wl.S, wl.S, wl.b, wl.max_stride)
+        Mel = om.element_mask(M, wl.b)
+        g = lambda s: synth.draw((1, 1, wl.S, wl.d), 1.0, 0, s, "bf16")[0][0, 0]
+        Q, K, V, dO = g(11), g(12), g(13), g(14)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oa.backward_head(Q, K, V, Mel, 1.0 / np.sqrt(wl.d), dO)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 1000:
+                break
+        fl = 6 * 2 * wl.b * wl.b * wl.d * int(M.sum()) * reps
+        return fl / el / 1e12, f"oracle fwd+bwd (fp64, dense masked) on {reps} heads of {wl.B * wl.H}, {el:.1f} s"
+
+
+def blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"]
+        if n:
+            return int(max(n))
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def timed(torch, fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(steps):
+        fn()
+    e.record()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see the sharding design notes); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2112_00029_amd import pixelfly as pf
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = synth.WORKLOADS[args.workload]
+    R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention}[wl.kind](torch, pf, wl)
+
+    calls = [c for c in args.calls_only.split(",") if c] or R.calls
+    # warmup, then the timed region with events between calls
+    for _ in range(args.warmup):
+        for c in calls:
+            R.call(c)
+    torch.cuda.synchronize()
+    timer = Timer(torch, calls)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        ev = timer.step_events()
+        for i, c in enumerate(calls):
+            ev[i].record()
+            R.call(c)
+        ev[-1].record()
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    per_call = timer.per_call_ms()
+    if args.calls_only:
+        print(json.dumps({"calls_only": calls, "ms_per_step": ms, "per_call_ms": per_call}))
+        return
+
+    sparse, lowrank, dense_fl = R.flops()
+    value = sparse / (ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if R.dtype == "bf16" else PEAK_FP32_TFLOPS
+
+    dense_ms = torch_ms = None
+    if not args.no_dense:
+        R.dense_setup()
+        dense_ms = timed(torch, R.dense_step, max(5, args.steps // 4), 3)
+        if wl.kind != "attention":
+            torch_ms = timed(torch, R.torch_dense_step, max(5, args.steps // 4), 3)
+
+    # roofline for the dominant call
+    dom = max(per_call, key=per_call.get)
+    fl, by = R.call_work(dom)
+    t = per_call[dom] * 1e-3
+    ai = fl / by
+    if R.dtype == "bf16" and ai >= RIDGE_BF16:
+        roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = None
+    roof.update({"call": dom, "ms": per_call[dom], "algorithmic_bytes": by, "flops": fl,
+                 "flop_per_byte": ai})
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        v, sample = R.cpu_baseline()
+        cpu = {"value": v, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle", "sample": sample}
+
+    cfg = {"workload": wl.name}
+    if wl.kind == "attention":
+        cfg.update(B=wl.B, H=wl.H, S=wl.S, d=wl.d, b=wl.b, max_stride=wl.max_stride)
+    else:
+        cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=wl.max_stride, r=wl.r)
+    out = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": R.dtype, "data": "synthetic (seeded, shapes of the workload)",
+        "config": cfg,
+        "pct_peak": 100.0 * value / peak,
+        "useful_tflops_incl_lowrank": (sparse + lowrank) / (ms * 1e-3) / 1e12,
+        "dense_ms_per_step": dense_ms,
+        "speedup_vs_dense": (dense_ms / ms) if dense_ms else None,
+        "dense_tflops": (dense_fl / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
+        "torch_dense_ms_per_step": torch_ms,
+        "per_call_ms": per_call,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,261 @@
+/*
+ * pixelfly.h -- C ABI of libpixelfly.so, the MI355X (gfx950) hot path of
+ * Pixelated Butterfly: the flat block butterfly + low-rank linear layer
+ *
+ *     Y = X (M o W)^T + (X V^T) U^T                      (Section 3.3)
+ *
+ * run forward and backward, and block-sparse softmax attention on the same
+ * mask family (appendix on method details, attention).
+ *
+ * Conventions shared by every call
+ *   - Matrices are row-major.  X: T x K (tokens x in-features), Y: T x N,
+ *     U: N x r, V: r x K.  W is stored packed: the kept b x b blocks in
+ *     block-CSR order (block row ascending, then block column ascending),
+ *     element (q, c) of packed block p being W[i*b + q][j*b + c] for the
+ *     block (i, j) at CSR position p.
+ *   - Device pointers are plain device addresses (e.g. torch
+ *     tensor.data_ptr()); `stream` is a hipStream_t passed as void* (NULL is
+ *     the null stream).  The caller owns every device buffer it passes.
+ *   - dtype is uniform per call: PF_BF16 (bfloat16 storage, fp32
+ *     accumulation, round-to-nearest-even stores) or PF_FP32.
+ *   - Compute calls validate every argument on the host before enqueuing
+ *     anything; on error they return a negative pf_status, enqueue nothing
+ *     and leave outputs untouched (pf_last_error() gives the detail).  They
+ *     never allocate, never synchronise and return as soon as the kernels
+ *     are enqueued on `stream`.
+ *   - Calls that take a workspace need at least pf_workspace_bytes(...)
+ *     bytes of device memory, 256-byte aligned, whose contents on entry do
+ *     not matter.
+ *   - Split-token reductions (pf_linear_bwd_weight, pf_dense_gemm with
+ *     PF_OP_TN) use a static per-GPU array of completion counters inside
+ *     the library (zero at load, left zero by every call); such calls must
+ *     not run concurrently on different streams of one GPU.
+ *   - No C++ exception crosses this ABI.  Kernel launch failures map to
+ *     PF_ERR_HIP.
+ */
+#ifndef PIXELFLY_H
+#define PIXELFLY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PF_OK = 0,
+  PF_ERR_INVALID_ARG = -1, /* bad dimension, null or misaligned pointer ... */
+  PF_ERR_UNSUPPORTED = -2, /* valid but not implemented (e.g. b = 16)       */
+  PF_ERR_WORKSPACE = -3,   /* workspace smaller than pf_workspace_bytes     */
+  PF_ERR_HIP = -4,         /* a HIP runtime call or launch failed           */
+  PF_ERR_NOMEM = -5,       /* host or device allocation failed (setup only) */
+  PF_ERR_STATE = -6        /* layout not uploaded before a compute call     */
+} pf_status;
+
+typedef enum { PF_BF16 = 0, PF_FP32 = 1 } pf_dtype;
+
+typedef enum {
+  PF_EPI_NONE = 0,
+  /* forward: Y_pre = acc, Y = gelu(acc) (exact erf GELU);
+     backward-data: dX = acc * gelu'(aux) with aux = the forward's Y_pre. */
+  PF_EPI_GELU = 1
+} pf_epilogue;
+
+typedef enum { PF_OP_NT = 0, PF_OP_NN = 1, PF_OP_TN = 2 } pf_gemm_op;
+
+typedef struct pf_layout pf_layout; /* opaque; immutable after create */
+
+/* Host views of a layout's block-CSR (valid until pf_layout_destroy). */
+typedef struct {
+  int64_t n_out, n_in;     /* N, K in elements                          */
+  int32_t b;               /* block size                                */
+  int32_t max_stride;      /* as requested, in blocks                   */
+  int32_t eff_stride;      /* clamped to the next power of two >= s      */
+  int32_t s;               /* square side min(nb_out, nb_in) in blocks   */
+  int32_t nb_out, nb_in;   /* N / b, K / b                               */
+  int64_t nnzb;            /* kept blocks                                */
+  const int32_t *row_ptr;  /* [nb_out + 1]                               */
+  const int32_t *col_idx;  /* [nnzb], CSR order                          */
+  const int32_t *col_ptr;  /* [nb_in + 1]                                */
+  const int32_t *row_idx;  /* [nnzb], CSC order                          */
+  const int32_t *tperm;    /* [nnzb]: CSR position of the p-th CSC block */
+} pf_layout_info;
+
+/*
+ * Build the flat block butterfly mask of an n_out x n_in weight with block
+ * size b and maximum stride max_stride (in blocks) and its block-CSR.
+ * Definitions: block butterfly factor and factor matrix (Section 3.1), flat
+ * butterfly of maximum stride k = I + sum of factors B_2..B_k (Section 3.2),
+ * mask selection by block size and maximum stride (Section 3.3, step 2),
+ * rectangular "stretch" (appendix on method details).  In block units,
+ * with s = min(n_out/b, n_in/b): block (i, j) is kept iff
+ * x = (i mod s) XOR (j mod s) is 0 or a power of two below max_stride; the
+ * s x s square is the power-of-two pattern cropped to s (partners >= s are
+ * dropped) and is tiled along the longer dimension.
+ * Requires b >= 1 dividing n_out and n_in, max_stride a power of two >= 1.
+ * Host only (no device work).  *out receives a new layout (free with
+ * pf_layout_destroy).  Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_layout_create(int64_t n_out, int64_t n_in, int32_t b,
+                           int32_t max_stride, pf_layout **out);
+
+/*
+ * Layout from an explicit block mask instead of the butterfly rule: block
+ * (i, j) of the nb_out x nb_in grid is kept iff block_mask[i*nb_in + j] != 0
+ * (row-major, host memory, read during the call only).  Serves the dense
+ * comparator (all blocks kept) and other block patterns, e.g. the random
+ * block patterns of the paper's microbenchmark (appendix on
+ * microbenchmarking).  Every block row must keep at least one block.
+ * max_stride and eff_stride of the layout read 0.  Host only.
+ * Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_layout_create_from_mask(int32_t nb_out, int32_t nb_in, int32_t b,
+                                     const uint8_t *block_mask, pf_layout **out);
+
+/* Fill *out with host views of the layout.  Errors: INVALID_ARG. */
+pf_status pf_layout_info_get(const pf_layout *layout, pf_layout_info *out);
+
+/* Diagnostic: re-verify that the layout's kernel work lists (forward tiles,
+ * backward-data tiles, weight-gradient items) cover every kept block exactly
+ * once with the right packed index.  Host only.  Errors: INVALID_ARG with
+ * the first violation in pf_last_error(). */
+pf_status pf_layout_check(const pf_layout *layout);
+
+/* Diagnostic: work-list statistics, n >= 6 entries written to stats:
+ * [0] forward tile rows G, [1] forward tiles, [2] backward-data tile
+ * columns G, [3] backward-data tiles, [4] weight-gradient items,
+ * [5] kept blocks covered by those items.  Host only. */
+pf_status pf_layout_plan_get(const pf_layout *layout, int32_t *stats,
+                             int32_t n);
+
+/*
+ * Copy the layout's index arrays and kernel work lists to the current HIP
+ * device (one-time, synchronous on `stream`).  Must precede compute calls;
+ * the layout then serves that device only.  Errors: INVALID_ARG, HIP, NOMEM,
+ * UNSUPPORTED (b not in {32, 64, 128}).
+ */
+pf_status pf_layout_upload(pf_layout *layout, void *stream);
+
+/* Free host and device memory of the layout (NULL is a no-op).  The caller
+ * must make sure no enqueued work still uses it. */
+void pf_layout_destroy(pf_layout *layout);
+
+/* Workspace bytes needed by pf_linear_bwd_weight for T tokens and rank r
+ * (0 when none is needed).  Returns 0 on invalid arguments. */
+size_t pf_workspace_bytes(const pf_layout *layout, int64_t T, int32_t r,
+                          pf_dtype dtype);
+
+/*
+ * Forward (Section 3.3; low-rank applied as U (V^T x), appendix on
+ * efficient implementation):
+ *     T_lr = X V^T                     (T x r, saved for the backward)
+ *     Y    = X (M o W)^T + T_lr U^T    (T x N)
+ * X: T x K, Wblk: packed [nnzb][b][b], U: N x r, V: r x K, Y: T x N,
+ * T_lr: T x r.  r = 0 drops the low-rank term (U, V, T_lr may be NULL).
+ * r must be a multiple of b (rank block-aligned, Section 3.3 step 2).
+ * epi = PF_EPI_GELU writes Y_pre (T x N) = the pre-activation and
+ * Y = gelu(Y_pre); with PF_EPI_NONE Y_pre must be NULL.
+ * Tokens T >= 1 is arbitrary (ragged last tile handled).
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, HIP.
+ */
+pf_status pf_linear_fwd(const pf_layout *layout, pf_dtype dtype, int64_t T,
+                        int32_t r, const void *X, const void *Wblk,
+                        const void *U, const void *V, void *Y, void *T_lr,
+                        pf_epilogue epi, void *Y_pre, void *stream);
+
+/*
+ * Backward-data (gradient of the layer w.r.t. its input):
+ *     S  = dY U                         (T x r, saved for bwd_weight)
+ *     dX = dY (M o W) + S V             (T x K)
+ * dY: T x N.  With epi = PF_EPI_GELU, aux is a T x K tensor (the previous
+ * layer's Y_pre) and dX = (dY (M o W) + S V) * gelu'(aux).
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, HIP.
+ */
+pf_status pf_linear_bwd_data(const pf_layout *layout, pf_dtype dtype,
+                             int64_t T, int32_t r, const void *dY,
+                             const void *Wblk, const void *U, const void *V,
+                             void *S, void *dX, pf_epilogue epi,
+                             const void *aux, void *stream);
+
+/*
+ * Backward-weight, restricted to the mask (gradient Lemma and sparse
+ * training algorithm of the appendix on gradient computation):
+ *     dW = (dY^T X) o M   stored packed like Wblk: only kept blocks
+ *     dU = dY^T T_lr      (N x r)
+ *     dV = S^T X          (r x K)
+ * Reductions run over the T tokens; split-token partial sums are combined
+ * in a fixed order, so results are deterministic.
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, WORKSPACE, HIP.
+ */
+pf_status pf_linear_bwd_weight(const pf_layout *layout, pf_dtype dtype,
+                               int64_t T, int32_t r, const void *dY,
+                               const void *X, const void *T_lr, const void *S,
+                               void *dWblk, void *dU, void *dV,
+                               void *workspace, size_t ws_bytes, void *stream);
+
+/* dH_pre = dH * gelu'(H_pre), n elements (exact erf GELU).  Standalone form
+ * of the GELU epilogue.  Errors: INVALID_ARG, UNSUPPORTED, HIP. */
+pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH,
+                      const void *H_pre, void *dH_pre, void *stream);
+
+/*
+ * Block-sparse attention forward, bf16, one mask shared by all B*H heads:
+ *     S = Q K^T * scale on the kept b x b blocks only, softmax over each
+ *     row's kept entries, O = P V, lse = log(sum exp S) per row (fp32).
+ * Q, K, V, O: [B][H][Sq][d] bf16; lse: [B][H][Sq] fp32.  The layout must be
+ * square (n_out = n_in = Sq) with b = 64; d = 64.  Non-causal, no dropout.
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, HIP.
+ */
+pf_status pf_attn_fwd(const pf_layout *layout, int32_t B, int32_t H,
+                      int32_t Sq, int32_t d, float scale, const void *Q,
+                      const void *K, const void *V, void *O, float *lse,
+                      void *stream);
+
+/*
+ * Block-sparse attention backward for L = <dO, O>:
+ *     delta = rowsum(dO o O), P = exp(S - lse), dV = P^T dO,
+ *     dS = P o (dO V^T - delta), dQ = dS K * scale, dK = dS^T Q * scale.
+ * Same shapes as pf_attn_fwd; dQ, dK, dV bf16.  Needs a workspace of
+ * B*H*Sq floats (pf_attn_workspace_bytes).
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, WORKSPACE, HIP.
+ */
+pf_status pf_attn_bwd(const pf_layout *layout, int32_t B, int32_t H,
+                      int32_t Sq, int32_t d, float scale, const void *Q,
+                      const void *K, const void *V, const void *O,
+                      const float *lse, const void *dO, void *dQ, void *dK,
+                      void *dV, void *workspace, size_t ws_bytes,
+                      void *stream);
+
+/* Workspace bytes of pf_attn_bwd. */
+size_t pf_attn_workspace_bytes(int32_t B, int32_t H, int32_t Sq);
+
+/*
+ * Dense comparator GEMM built from the same MFMA tiles as the sparse
+ * kernels (the speedup baseline: an equally shaped dense layer):
+ *   PF_OP_NT: C[M][N] = A[M][K] . B[N][K]^T   (forward,  X W^T)
+ *   PF_OP_NN: C[M][N] = A[M][K] . B[K][N]     (backward-data, dY W)
+ *   PF_OP_TN: C[M][N] = A[K][M]^T . B[K][N]   (backward-weight, dY^T X)
+ * M, N multiples of 64; K a multiple of 64 (NT, NN) or >= 1 (TN, where K is
+ * the reduction over tokens).  For TN a workspace of
+ * pf_dense_workspace_bytes is needed.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.
+ */
+pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N,
+                        int64_t K, const void *A, const void *B, void *C,
+                        void *workspace, size_t ws_bytes, void *stream);
+
+size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M,
+                                int64_t N, int64_t K);
+
+/* Static text of a status code. */
+const char *pf_status_string(pf_status s);
+
+/* Detail of the calling thread's last error ("" if none). */
+const char *pf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PIXELFLY_H */

@@ -1,0 +1,431 @@
+// Block-sparse softmax attention for gfx950: 64 x 64 score blocks on the
+// flat block butterfly mask, head dim 64, bf16 I/O, fp32 softmax/accumulate.
+//
+// Workgroup = 4 waves over one 64-row block (of queries for the forward and
+// dQ, of keys for dK/dV); each wave owns 16 rows.  Everything is computed in
+// transposed form so that each lane owns ONE row (its softmax statistics are
+// per-lane scalars) and the probability tile feeds the next MFMA straight
+// from registers:
+//   forward : S^T = K_j Q_w^T (16x16x32 MFMA), online softmax per query,
+//             O^T += V_j^T P^T.
+//   dQ      : recompute S^T, P^T; dP^T = V_j dO_w^T; dS^T = P^T o (dP^T -
+//             delta); dQ^T += K_j^T dS^T.
+//   dK, dV  : S = Q_i K_w^T, P, dP = dO_i V_w^T, dS; dV^T += dO_i^T P,
+//             dK^T += Q_i^T dS.
+// The register tile of P (rows = 16 keys per MFMA output, 4 per lane) is
+// used as a K-operand with keys in the order {16c + 4*(l/16) + 0..3} for two
+// consecutive c; the matching operand is read from LDS with the transpose
+// read in that same key order, so the contraction pairs up correctly.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "pf_internal.h"
+
+namespace pf {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int D = 64;       // head dim
+constexpr int BQ = 64;      // block size
+constexpr int LDK = D + 8;  // LDS row stride (elements)
+constexpr int LDV = D + 16;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float bf2f_a(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ bf16_t f2bf_a(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+
+__device__ __forceinline__ int xcd_remap_a(int bid, int n) {
+  constexpr int X = 8;
+  int q = n / X, rem = n % X, x = bid % X, slot = bid / X;
+  return x * q + min(x, rem) + slot;
+}
+
+__device__ __forceinline__ s16x4 tr16a(const bf16_t *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4 *)(p));
+}
+
+// A-operand of a 16x16x32 MFMA, A[m][k] = tile[k][m] (tile stored [k][m],
+// m contiguous), with k in the permuted order {kb + 4*(l/16) + 0..3} then
+// {kb + 16 + 4*(l/16) + 0..3}; m = m0 + l % 16.
+__device__ __forceinline__ bf16x8 fragA_tr_perm(const bf16_t *tile, int ld, int kb, int m0, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const bf16_t *p = tile + (kb + g * 4 + (i >> 2)) * ld + m0 + (i & 3) * 4;
+  s16x4 lo = tr16a(p), hi = tr16a(p + 16 * ld);
+  s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Operand of a 16x16x32 MFMA from a [row][k] tile: row r0 + l % 16,
+// k = kb + (l/16)*8 + 0..7 (16-byte read).
+__device__ __forceinline__ bf16x8 frag_rows(const bf16_t *tile, int ld, int r0, int kb, int lane) {
+  return *(const bf16x8 *)(tile + (r0 + (lane & 15)) * ld + kb + (lane >> 4) * 8);
+}
+
+// Same from global memory.
+__device__ __forceinline__ bf16x8 frag_rows_g(const bf16_t *p, int r0, int kb, int lane) {
+  return *(const bf16x8 *)(p + (int64_t)(r0 + (lane & 15)) * D + kb + (lane >> 4) * 8);
+}
+
+// Pack a register tile (two 16-row MFMA outputs c0, c1) as the permuted
+// K-operand.
+__device__ __forceinline__ bf16x8 pack_perm(const f32x4 &c0, const f32x4 &c1) {
+  bf16x8 v;
+  v[0] = (__bf16)c0[0]; v[1] = (__bf16)c0[1]; v[2] = (__bf16)c0[2]; v[3] = (__bf16)c0[3];
+  v[4] = (__bf16)c1[0]; v[5] = (__bf16)c1[1]; v[6] = (__bf16)c1[2]; v[7] = (__bf16)c1[3];
+  return v;
+}
+
+#define MFMA16(a, b, c) __builtin_amdgcn_mfma_f32_16x16x32_bf16((a), (b), (c), 0, 0, 0)
+
+// Cooperative load of a 64 x 64 bf16 tile (row stride D in global) into
+// registers: 512 chunks of 16 bytes, two per thread.
+struct Tile64 {
+  u32x4 r0, r1;  // named fields: never addressed with a run-time index
+  __device__ __forceinline__ void load(const bf16_t *g, int tid) {
+    const int row = tid >> 3, c = (tid & 7) * 8;
+    r0 = *(const u32x4 *)(g + row * D + c);
+    r1 = *(const u32x4 *)(g + (row + 32) * D + c);
+  }
+  __device__ __forceinline__ void store(bf16_t *s, int ld, int tid) const {
+    const int row = tid >> 3, c = (tid & 7) * 8;
+    *(u32x4 *)(s + row * ld + c) = r0;
+    *(u32x4 *)(s + (row + 32) * ld + c) = r1;
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Forward
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BQ * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BQ * LDV];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
+  const int bh = bid / a.nbq, qb = bid % a.nbq;
+  const int64_t head = (int64_t)bh * a.S * D;
+  const bf16_t *Q = (const bf16_t *)a.Q + head;
+  const bf16_t *K = (const bf16_t *)a.K + head;
+  const bf16_t *V = (const bf16_t *)a.V + head;
+  const int q0 = qb * BQ + wave * 16;
+  const float c = a.scale * kLog2e;
+
+  bf16x8 qf[2];
+  qf[0] = frag_rows_g(Q, q0, 0, lane);
+  qf[1] = frag_rows_g(Q, q0, 32, lane);
+
+  const int p0 = a.row_ptr[qb], p1 = a.row_ptr[qb + 1];
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  Tile64 tk, tv;
+  tk.load(K + (int64_t)a.col_idx[p0] * BQ * D, tid);
+  tv.load(V + (int64_t)a.col_idx[p0] * BQ * D, tid);
+  tk.store(Ks[0], LDK, tid);
+  tv.store(Vs[0], LDV, tid);
+  __syncthreads();
+
+  for (int p = p0; p < p1; ++p) {
+    const int cur = (p - p0) & 1;
+    if (p + 1 < p1) {
+      tk.load(K + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
+      tv.load(V + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
+    }
+    // S^T[key][query] for 64 keys x this wave's 16 queries.
+    f32x4 s[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 0, lane), qf[0], s[mt]);
+      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 32, lane), qf[1], s[mt]);
+    }
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bmax = fmaxf(bmax, s[mt][j]);
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+    const float m_new = fmaxf(m_run, bmax * c);
+    const float alpha = exp2f(m_run - m_new);
+    float rs = 0.f;
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float e = exp2f(s[mt][j] * c - m_new);
+        s[mt][j] = e;
+        rs += e;
+      }
+    rs += __shfl_xor(rs, 16);
+    rs += __shfl_xor(rs, 32);
+    l_run = l_run * alpha + rs;
+    m_run = m_new;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[dt][j] *= alpha;
+    // O^T[dim][query] += V^T[dim][key] P^T[key][query]
+    const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      o[dt] = MFMA16(fragA_tr_perm(Vs[cur], LDV, 0, dt * 16, lane), pb0, o[dt]);
+      o[dt] = MFMA16(fragA_tr_perm(Vs[cur], LDV, 32, dt * 16, lane), pb1, o[dt]);
+    }
+    if (p + 1 < p1) {
+      tk.store(Ks[cur ^ 1], LDK, tid);
+      tv.store(Vs[cur ^ 1], LDV, tid);
+    }
+    __syncthreads();
+  }
+
+  const float inv = 1.f / l_run;
+  const int q = q0 + (lane & 15);
+  bf16_t *O = (bf16_t *)a.Oout + head + (int64_t)q * D;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    u32x2 w;
+    w[0] = (uint32_t)f2bf_a(o[dt][0] * inv) | ((uint32_t)f2bf_a(o[dt][1] * inv) << 16);
+    w[1] = (uint32_t)f2bf_a(o[dt][2] * inv) | ((uint32_t)f2bf_a(o[dt][3] * inv) << 16);
+    *(u32x2 *)(O + dt * 16 + (lane >> 4) * 4) = w;
+  }
+  if (lane < 16) a.lse[(int64_t)bh * a.S + q] = (m_run + __log2f(l_run)) * kLn2;
+}
+
+// ---------------------------------------------------------------------------
+// Backward, pass 1: delta and dQ (one workgroup per query block)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BQ * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BQ * LDK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
+  const int bh = bid / a.nbq, qb = bid % a.nbq;
+  const int64_t head = (int64_t)bh * a.S * D;
+  const bf16_t *Q = (const bf16_t *)a.Q + head;
+  const bf16_t *K = (const bf16_t *)a.K + head;
+  const bf16_t *V = (const bf16_t *)a.V + head;
+  const bf16_t *O = (const bf16_t *)a.O + head;
+  const bf16_t *dO = (const bf16_t *)a.dO + head;
+  const int q0 = qb * BQ + wave * 16;
+  const int q = q0 + (lane & 15);
+  const float c = a.scale * kLog2e;
+
+  bf16x8 qf[2], dof[2];
+  qf[0] = frag_rows_g(Q, q0, 0, lane);
+  qf[1] = frag_rows_g(Q, q0, 32, lane);
+  dof[0] = frag_rows_g(dO, q0, 0, lane);
+  dof[1] = frag_rows_g(dO, q0, 32, lane);
+
+  // delta = rowsum(dO o O): lane covers dims (l/16)*16 .. +15 of query q.
+  float delta = 0.f;
+  {
+    const bf16_t *po = O + (int64_t)q * D + (lane >> 4) * 16;
+    const bf16_t *pd = dO + (int64_t)q * D + (lane >> 4) * 16;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const u32x4 vo = *(const u32x4 *)(po + h * 8), vd = *(const u32x4 *)(pd + h * 8);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        delta += __uint_as_float(vo[e] << 16) * __uint_as_float(vd[e] << 16);
+        delta += __uint_as_float(vo[e] & 0xffff0000u) * __uint_as_float(vd[e] & 0xffff0000u);
+      }
+    }
+    delta += __shfl_xor(delta, 16);
+    delta += __shfl_xor(delta, 32);
+  }
+  if (lane < 16) a.delta[(int64_t)bh * a.S + q] = delta;
+  const float lse2 = a.lse_in[(int64_t)bh * a.S + q] * kLog2e;
+
+  const int p0 = a.row_ptr[qb], p1 = a.row_ptr[qb + 1];
+  f32x4 dq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  Tile64 tk, tv;
+  tk.load(K + (int64_t)a.col_idx[p0] * BQ * D, tid);
+  tv.load(V + (int64_t)a.col_idx[p0] * BQ * D, tid);
+  tk.store(Ks[0], LDK, tid);
+  tv.store(Vs[0], LDK, tid);
+  __syncthreads();
+
+  for (int p = p0; p < p1; ++p) {
+    const int cur = (p - p0) & 1;
+    if (p + 1 < p1) {
+      tk.load(K + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
+      tv.load(V + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
+    }
+    f32x4 s[4], dp[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 0, lane), qf[0], s[mt]);
+      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 32, lane), qf[1], s[mt]);
+      dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[mt] = MFMA16(frag_rows(Vs[cur], LDK, mt * 16, 0, lane), dof[0], dp[mt]);
+      dp[mt] = MFMA16(frag_rows(Vs[cur], LDK, mt * 16, 32, lane), dof[1], dp[mt]);
+    }
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float pr = exp2f(s[mt][j] * c - lse2);
+        s[mt][j] = pr * (dp[mt][j] - delta);  // dS^T
+      }
+    const bf16x8 d0 = pack_perm(s[0], s[1]), d1 = pack_perm(s[2], s[3]);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      dq[dt] = MFMA16(fragA_tr_perm(Ks[cur], LDK, 0, dt * 16, lane), d0, dq[dt]);
+      dq[dt] = MFMA16(fragA_tr_perm(Ks[cur], LDK, 32, dt * 16, lane), d1, dq[dt]);
+    }
+    if (p + 1 < p1) {
+      tk.store(Ks[cur ^ 1], LDK, tid);
+      tv.store(Vs[cur ^ 1], LDK, tid);
+    }
+    __syncthreads();
+  }
+
+  bf16_t *dQ = (bf16_t *)a.dQ + head + (int64_t)q * D;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    u32x2 w;
+    w[0] = (uint32_t)f2bf_a(dq[dt][0] * a.scale) | ((uint32_t)f2bf_a(dq[dt][1] * a.scale) << 16);
+    w[1] = (uint32_t)f2bf_a(dq[dt][2] * a.scale) | ((uint32_t)f2bf_a(dq[dt][3] * a.scale) << 16);
+    *(u32x2 *)(dQ + dt * 16 + (lane >> 4) * 4) = w;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward, pass 2: dK and dV (one workgroup per key block)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[2][BQ * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[2][BQ * LDK];
+  __shared__ float ls[2][BQ], ds[2][BQ];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
+  const int bh = bid / a.nbq, kb = bid % a.nbq;
+  const int64_t head = (int64_t)bh * a.S * D;
+  const bf16_t *Q = (const bf16_t *)a.Q + head;
+  const bf16_t *K = (const bf16_t *)a.K + head;
+  const bf16_t *V = (const bf16_t *)a.V + head;
+  const bf16_t *dO = (const bf16_t *)a.dO + head;
+  const float *lse = a.lse_in + (int64_t)bh * a.S;
+  const float *dl = a.delta + (int64_t)bh * a.S;
+  const int k0 = kb * BQ + wave * 16;
+  const float c = a.scale * kLog2e;
+
+  bf16x8 kf[2], vf[2];
+  kf[0] = frag_rows_g(K, k0, 0, lane);
+  kf[1] = frag_rows_g(K, k0, 32, lane);
+  vf[0] = frag_rows_g(V, k0, 0, lane);
+  vf[1] = frag_rows_g(V, k0, 32, lane);
+
+  const int p0 = a.col_ptr[kb], p1 = a.col_ptr[kb + 1];
+  f32x4 dk[4], dv[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    dk[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    dv[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  if (p0 < p1) {  // a key block no query attends keeps zero gradients
+
+  Tile64 tq, td;
+  float rl = 0.f, rd = 0.f;
+  auto gload = [&](int p) {
+    const int64_t qrow = (int64_t)a.row_idx[p] * BQ;
+    tq.load(Q + qrow * D, tid);
+    td.load(dO + qrow * D, tid);
+    if (tid < BQ) { rl = lse[qrow + tid] * kLog2e; rd = dl[qrow + tid]; }
+  };
+  auto sstore = [&](int buf) {
+    tq.store(Qs[buf], LDK, tid);
+    td.store(dOs[buf], LDK, tid);
+    if (tid < BQ) { ls[buf][tid] = rl; ds[buf][tid] = rd; }
+  };
+  gload(p0);
+  sstore(0);
+  __syncthreads();
+
+  for (int p = p0; p < p1; ++p) {
+    const int cur = (p - p0) & 1;
+    if (p + 1 < p1) gload(p + 1);
+    // S[query][key], dP[query][key] for 64 queries x this wave's 16 keys.
+    f32x4 s[4], dp[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      s[mt] = MFMA16(frag_rows(Qs[cur], LDK, mt * 16, 0, lane), kf[0], s[mt]);
+      s[mt] = MFMA16(frag_rows(Qs[cur], LDK, mt * 16, 32, lane), kf[1], s[mt]);
+      dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dp[mt] = MFMA16(frag_rows(dOs[cur], LDK, mt * 16, 0, lane), vf[0], dp[mt]);
+      dp[mt] = MFMA16(frag_rows(dOs[cur], LDK, mt * 16, 32, lane), vf[1], dp[mt]);
+    }
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int qi = mt * 16 + (lane >> 4) * 4 + j;
+        const float pr = exp2f(s[mt][j] * c - ls[cur][qi]);
+        s[mt][j] = pr;
+        dp[mt][j] = pr * (dp[mt][j] - ds[cur][qi]);  // dS
+      }
+    const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
+    const bf16x8 sb0 = pack_perm(dp[0], dp[1]), sb1 = pack_perm(dp[2], dp[3]);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      dv[dt] = MFMA16(fragA_tr_perm(dOs[cur], LDK, 0, dt * 16, lane), pb0, dv[dt]);
+      dv[dt] = MFMA16(fragA_tr_perm(dOs[cur], LDK, 32, dt * 16, lane), pb1, dv[dt]);
+      dk[dt] = MFMA16(fragA_tr_perm(Qs[cur], LDK, 0, dt * 16, lane), sb0, dk[dt]);
+      dk[dt] = MFMA16(fragA_tr_perm(Qs[cur], LDK, 32, dt * 16, lane), sb1, dk[dt]);
+    }
+    if (p + 1 < p1) sstore(cur ^ 1);
+    __syncthreads();
+  }
+  }
+
+  const int key = k0 + (lane & 15);
+  bf16_t *dK = (bf16_t *)a.dK + head + (int64_t)key * D;
+  bf16_t *dV = (bf16_t *)a.dV + head + (int64_t)key * D;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) {
+    u32x2 w;
+    w[0] = (uint32_t)f2bf_a(dk[dt][0] * a.scale) | ((uint32_t)f2bf_a(dk[dt][1] * a.scale) << 16);
+    w[1] = (uint32_t)f2bf_a(dk[dt][2] * a.scale) | ((uint32_t)f2bf_a(dk[dt][3] * a.scale) << 16);
+    *(u32x2 *)(dK + dt * 16 + (lane >> 4) * 4) = w;
+    w[0] = (uint32_t)f2bf_a(dv[dt][0]) | ((uint32_t)f2bf_a(dv[dt][1]) << 16);
+    w[1] = (uint32_t)f2bf_a(dv[dt][2]) | ((uint32_t)f2bf_a(dv[dt][3]) << 16);
+    *(u32x2 *)(dV + dt * 16 + (lane >> 4) * 4) = w;
+  }
+}
+
+hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s) {
+  const int64_t grid = (int64_t)a.BH * a.nbq;
+  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_fwd_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_bwd(const AttnArgs &a, hipStream_t s) {
+  const int64_t grid = (int64_t)a.BH * a.nbq;
+  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(attn_bwd_dq_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_bwd_dkv_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace pf

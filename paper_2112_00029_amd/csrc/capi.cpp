@@ -1,0 +1,537 @@
+// C ABI of libpixelfly.so: argument validation (all before any enqueue) and
+// dispatch to the HIP kernels.  See include/pixelfly.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "layout.h"
+#include "pf_internal.h"
+#include "pixelfly.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+pf_status fail(pf_status s, const std::string &msg) {
+  g_err = msg;
+  return s;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+
+pf_status need_ptr(const void *p, const char *name) {
+  if (!p) return fail(PF_ERR_INVALID_ARG, std::string(name) + " is NULL");
+  if (!aligned16(p))
+    return fail(PF_ERR_INVALID_ARG, std::string(name) + " is not 16-byte aligned");
+  return PF_OK;
+}
+
+bool kernel_block(int32_t b) { return b == 32 || b == 64 || b == 128; }
+
+pf_status check_layout_arg(const pf_layout *L) {
+  if (!L) return fail(PF_ERR_INVALID_ARG, "layout is NULL");
+  if (!kernel_block(L->b))
+    return fail(PF_ERR_UNSUPPORTED, "kernels support b in {32, 64, 128}");
+  return PF_OK;
+}
+
+// Called after all argument checks: the layout must live on this device.
+pf_status check_state(const pf_layout *L) {
+  if (L->device < 0 || !L->dev_mem)
+    return fail(PF_ERR_STATE, "layout not uploaded (call pf_layout_upload)");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != L->device)
+    return fail(PF_ERR_STATE, "layout was uploaded to another device");
+  return PF_OK;
+}
+
+pf_status check_dtype_r(pf_dtype dt, int64_t T, int32_t r, int32_t b) {
+  if (dt != PF_BF16 && dt != PF_FP32) return fail(PF_ERR_INVALID_ARG, "bad dtype");
+  if (T < 1) return fail(PF_ERR_INVALID_ARG, "T must be >= 1");
+  if (T > ((int64_t)1 << 31) / 2) return fail(PF_ERR_INVALID_ARG, "T too large");
+  if (r < 0 || r % b) return fail(PF_ERR_INVALID_ARG, "r must be a non-negative multiple of b");
+  return PF_OK;
+}
+
+pf_status hip_status(hipError_t e, const char *what) {
+  if (e == hipSuccess) return PF_OK;
+  return fail(PF_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Largest power of two <= min(gmax, n).
+int pow2_group(int gmax, int n) {
+  int g = 1;
+  while (g * 2 <= gmax && g * 2 <= n) g *= 2;
+  return g;
+}
+
+// Dense-mode NT launch: C[T x nblk*b] = A[T x nsteps*b] . B^T (B [n][k]) or
+// A . B (B [k][n]).
+pf_status dense_nt(int dtype, int blk, bool b_kn, int64_t M, const void *A, int64_t lda,
+                   const void *B, int64_t ldb, int nsteps, int nblk, void *C, int64_t ldc,
+                   hipStream_t s, const char *what) {
+  pf::NTArgs a{};
+  a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
+  a.dense = 1; a.dense_nsteps = nsteps; a.dense_nblk = nblk;
+  a.C = C; a.ldc = ldc; a.M = M;
+  int G = pow2_group(pf::max_group(blk), nblk);
+  a.ntiles = (nblk + G - 1) / G;
+  return hip_status(pf::launch_nt(dtype, blk, G, b_kn, a, s), what);
+}
+
+// Split-token plan of the TN kernel.
+struct TNPlan {
+  int nsplit;
+  int64_t chunk;
+  size_t ws;
+};
+
+TNPlan tn_plan(int items, int64_t T) {
+  TNPlan p{1, ((T + 31) / 32) * 32, 0};
+  const int target = 2 * 256;
+  if (items < target && items <= pf::kMaxCounters) {
+    int64_t want = (target + items - 1) / items;
+    int64_t maxs = std::max<int64_t>(1, T / 256);
+    int64_t ns = std::min<int64_t>(want, maxs);
+    if (ns > 1) {
+      int64_t chunk = ((T + ns - 1) / ns + 31) / 32 * 32;
+      ns = (T + chunk - 1) / chunk;
+      if (ns > 1) {
+        p.nsplit = (int)ns;
+        p.chunk = chunk;
+        p.ws = (size_t)items * ns * 128 * 128 * sizeof(float);
+      }
+    }
+  }
+  return p;
+}
+
+void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
+                     const void *X, const void *T_lr, const void *S, void *dU, void *dV) {
+  a.n_dense = 0;
+  if (r > 0) {
+    a.dr[0] = pf::TNDense{dY, L->n_out, T_lr, r, dU, r, L->nb_out, r / L->b};
+    a.dr[1] = pf::TNDense{S, r, X, L->n_in, dV, L->n_in, r / L->b, L->nb_in};
+    a.n_dense = 2;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *pf_status_string(pf_status s) {
+  switch (s) {
+    case PF_OK: return "ok";
+    case PF_ERR_INVALID_ARG: return "invalid argument";
+    case PF_ERR_UNSUPPORTED: return "unsupported";
+    case PF_ERR_WORKSPACE: return "workspace too small";
+    case PF_ERR_HIP: return "HIP error";
+    case PF_ERR_NOMEM: return "out of memory";
+    case PF_ERR_STATE: return "layout not ready";
+  }
+  return "unknown status";
+}
+
+const char *pf_last_error(void) { return g_err.c_str(); }
+
+pf_status pf_layout_create(int64_t n_out, int64_t n_in, int32_t b, int32_t max_stride,
+                           pf_layout **out) {
+  if (!out) return fail(PF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  pf_layout *L = new (std::nothrow) pf_layout();
+  if (!L) return fail(PF_ERR_NOMEM, "host allocation failed");
+  std::string e;
+  try {
+    e = pf::build_layout(*L, n_out, n_in, b, max_stride);
+  } catch (const std::bad_alloc &) {
+    delete L;
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  } catch (...) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, "layout build failed");
+  }
+  if (!e.empty()) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, e);
+  }
+  *out = L;
+  return PF_OK;
+}
+
+pf_status pf_layout_create_from_mask(int32_t nb_out, int32_t nb_in, int32_t b,
+                                     const uint8_t *block_mask, pf_layout **out) {
+  if (!out) return fail(PF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  pf_layout *L = new (std::nothrow) pf_layout();
+  if (!L) return fail(PF_ERR_NOMEM, "host allocation failed");
+  std::string e;
+  try {
+    e = pf::build_layout_from_mask(*L, nb_out, nb_in, b, block_mask);
+  } catch (const std::bad_alloc &) {
+    delete L;
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  } catch (...) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, "layout build failed");
+  }
+  if (!e.empty()) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, e);
+  }
+  *out = L;
+  return PF_OK;
+}
+
+pf_status pf_layout_info_get(const pf_layout *L, pf_layout_info *o) {
+  if (!L || !o) return fail(PF_ERR_INVALID_ARG, "NULL argument");
+  o->n_out = L->n_out;
+  o->n_in = L->n_in;
+  o->b = L->b;
+  o->max_stride = L->max_stride;
+  o->eff_stride = L->eff_stride;
+  o->s = L->s;
+  o->nb_out = L->nb_out;
+  o->nb_in = L->nb_in;
+  o->nnzb = L->nnzb;
+  o->row_ptr = L->row_ptr.data();
+  o->col_idx = L->col_idx.data();
+  o->col_ptr = L->col_ptr.data();
+  o->row_idx = L->row_idx.data();
+  o->tperm = L->tperm.data();
+  return PF_OK;
+}
+
+pf_status pf_layout_check(const pf_layout *L) {
+  if (!L) return fail(PF_ERR_INVALID_ARG, "layout is NULL");
+  std::string e = pf::check_layout(*L);
+  if (!e.empty()) return fail(PF_ERR_INVALID_ARG, e);
+  return PF_OK;
+}
+
+pf_status pf_layout_plan_get(const pf_layout *L, int32_t *stats, int32_t n) {
+  if (!L || !stats || n < 6) return fail(PF_ERR_INVALID_ARG, "bad arguments");
+  stats[0] = L->G_fwd;
+  stats[1] = (int32_t)L->fwd_tiles.size();
+  stats[2] = L->G_bwd;
+  stats[3] = (int32_t)L->bwd_tiles.size();
+  stats[4] = (int32_t)L->tn_items.size();
+  int kept = 0;
+  for (auto &it : L->tn_items)
+    for (int q = 0; q < pf::kTNMax * pf::kTNMax; ++q) kept += it.out_blk[q] >= 0;
+  stats[5] = kept;
+  return PF_OK;
+}
+
+pf_status pf_layout_upload(pf_layout *L, void *stream) {
+  if (!L) return fail(PF_ERR_INVALID_ARG, "layout is NULL");
+  if (!kernel_block(L->b))
+    return fail(PF_ERR_UNSUPPORTED, "kernels support b in {32, 64, 128}");
+  if (L->dev_mem) return PF_OK;
+  int dev = -1;
+  pf_status st = hip_status(hipGetDevice(&dev), "hipGetDevice");
+  if (st != PF_OK) return st;
+  auto bytes = [](size_t n, size_t sz) { return (n * sz + 255) / 256 * 256; };
+  size_t off[11], total = 0;
+  size_t sizes[11] = {
+      bytes(L->fwd_tiles.size(), sizeof(pf::NTTile)), bytes(L->bwd_tiles.size(), sizeof(pf::NTTile)),
+      bytes(L->kcols_fwd.size(), 4), bytes(L->blks_fwd.size(), 4),
+      bytes(L->kcols_bwd.size(), 4), bytes(L->blks_bwd.size(), 4),
+      bytes(L->tn_items.size(), sizeof(pf::TNItem)), bytes(L->row_ptr.size(), 4),
+      bytes(L->col_idx.size(), 4), bytes(L->col_ptr.size(), 4), bytes(L->row_idx.size(), 4)};
+  const void *src[11] = {L->fwd_tiles.data(), L->bwd_tiles.data(), L->kcols_fwd.data(),
+                         L->blks_fwd.data(),  L->kcols_bwd.data(), L->blks_bwd.data(),
+                         L->tn_items.data(),  L->row_ptr.data(),   L->col_idx.data(),
+                         L->col_ptr.data(),   L->row_idx.data()};
+  size_t nbytes[11] = {L->fwd_tiles.size() * sizeof(pf::NTTile), L->bwd_tiles.size() * sizeof(pf::NTTile),
+                       L->kcols_fwd.size() * 4, L->blks_fwd.size() * 4, L->kcols_bwd.size() * 4,
+                       L->blks_bwd.size() * 4, L->tn_items.size() * sizeof(pf::TNItem),
+                       L->row_ptr.size() * 4, L->col_idx.size() * 4, L->col_ptr.size() * 4,
+                       L->row_idx.size() * 4};
+  for (int i = 0; i < 11; ++i) {
+    off[i] = total;
+    total += sizes[i];
+  }
+  void *mem = nullptr;
+  if (hipMalloc(&mem, total) != hipSuccess) return fail(PF_ERR_NOMEM, "hipMalloc for layout failed");
+  hipStream_t s = (hipStream_t)stream;
+  for (int i = 0; i < 11; ++i)
+    if (nbytes[i]) {
+      hipError_t e = hipMemcpyAsync((char *)mem + off[i], src[i], nbytes[i], hipMemcpyHostToDevice, s);
+      if (e != hipSuccess) {
+        (void)hipFree(mem);
+        return hip_status(e, "layout upload");
+      }
+    }
+  hipError_t e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return hip_status(e, "layout upload sync");
+  }
+  char *m = (char *)mem;
+  L->d_fwd_tiles = (const pf::NTTile *)(m + off[0]);
+  L->d_bwd_tiles = (const pf::NTTile *)(m + off[1]);
+  L->d_kcols_fwd = (const int32_t *)(m + off[2]);
+  L->d_blks_fwd = (const int32_t *)(m + off[3]);
+  L->d_kcols_bwd = (const int32_t *)(m + off[4]);
+  L->d_blks_bwd = (const int32_t *)(m + off[5]);
+  L->d_tn_items = (const pf::TNItem *)(m + off[6]);
+  L->d_row_ptr = (const int32_t *)(m + off[7]);
+  L->d_col_idx = (const int32_t *)(m + off[8]);
+  L->d_col_ptr = (const int32_t *)(m + off[9]);
+  L->d_row_idx = (const int32_t *)(m + off[10]);
+  L->dev_mem = mem;
+  L->device = dev;
+  return PF_OK;
+}
+
+void pf_layout_destroy(pf_layout *L) {
+  if (!L) return;
+  if (L->dev_mem) {
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (cur != L->device) (void)hipSetDevice(L->device);
+    (void)hipFree(L->dev_mem);
+    if (cur >= 0 && cur != L->device) (void)hipSetDevice(cur);
+  }
+  delete L;
+}
+
+size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dtype) {
+  if (!L || T < 1 || r < 0 || !kernel_block(L->b) || r % L->b) return 0;
+  if (dtype != PF_BF16 && dtype != PF_FP32) return 0;
+  pf::TNArgs a{};
+  a.n_items = (int)L->tn_items.size();
+  fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+  return tn_plan(pf::tn_items_total(a, L->b), T).ws;
+}
+
+pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *X,
+                        const void *Wblk, const void *U, const void *V, void *Y, void *T_lr,
+                        pf_epilogue epi, void *Y_pre, void *stream) {
+  pf_status st = check_layout_arg(L);
+  if (st != PF_OK) return st;
+  if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = need_ptr(X, "X")) != PF_OK || (st = need_ptr(Wblk, "Wblk")) != PF_OK ||
+      (st = need_ptr(Y, "Y")) != PF_OK)
+    return st;
+  if (r > 0 && ((st = need_ptr(U, "U")) != PF_OK || (st = need_ptr(V, "V")) != PF_OK ||
+                (st = need_ptr(T_lr, "T_lr")) != PF_OK))
+    return st;
+  if (epi != PF_EPI_NONE && epi != PF_EPI_GELU) return fail(PF_ERR_INVALID_ARG, "bad epilogue");
+  if (epi == PF_EPI_GELU && (st = need_ptr(Y_pre, "Y_pre")) != PF_OK) return st;
+  if (epi == PF_EPI_NONE && Y_pre) return fail(PF_ERR_INVALID_ARG, "Y_pre given without GELU epilogue");
+  if ((st = check_state(L)) != PF_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const int dt = (int)dtype, b = L->b;
+  if (r > 0) {
+    // T_lr = X V^T: dense NT over K, r/b output blocks.
+    st = dense_nt(dt, b, false, T, X, L->n_in, V, L->n_in, L->nb_in, r / b, T_lr, r, s, "T_lr kernel");
+    if (st != PF_OK) return st;
+  }
+  pf::NTArgs a{};
+  a.A = X; a.lda = L->n_in;
+  a.B = Wblk;
+  a.L = T_lr; a.ldl = r; a.R = U; a.ldr = r; a.nlr = r / b;
+  a.C = Y; a.ldc = L->n_out;
+  a.C2 = epi == PF_EPI_GELU ? Y_pre : nullptr;
+  a.epi = (int)epi;
+  a.M = T;
+  a.tiles = L->d_fwd_tiles; a.ntiles = (int)L->fwd_tiles.size();
+  a.kcols = L->d_kcols_fwd; a.blks = L->d_blks_fwd;
+  return hip_status(pf::launch_nt(dt, b, L->G_fwd, false, a, s), "forward kernel");
+}
+
+pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                             const void *dY, const void *Wblk, const void *U, const void *V,
+                             void *S, void *dX, pf_epilogue epi, const void *aux, void *stream) {
+  pf_status st = check_layout_arg(L);
+  if (st != PF_OK) return st;
+  if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = need_ptr(dY, "dY")) != PF_OK || (st = need_ptr(Wblk, "Wblk")) != PF_OK ||
+      (st = need_ptr(dX, "dX")) != PF_OK)
+    return st;
+  if (r > 0 && ((st = need_ptr(U, "U")) != PF_OK || (st = need_ptr(V, "V")) != PF_OK ||
+                (st = need_ptr(S, "S")) != PF_OK))
+    return st;
+  if (epi != PF_EPI_NONE && epi != PF_EPI_GELU) return fail(PF_ERR_INVALID_ARG, "bad epilogue");
+  if (epi == PF_EPI_GELU && (st = need_ptr(aux, "aux")) != PF_OK) return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  const int dt = (int)dtype, b = L->b;
+  if (r > 0) {
+    // S = dY U: dense over N with U read as [k][n].
+    st = dense_nt(dt, b, true, T, dY, L->n_out, U, r, L->nb_out, r / b, S, r, s, "S kernel");
+    if (st != PF_OK) return st;
+  }
+  pf::NTArgs a{};
+  a.A = dY; a.lda = L->n_out;
+  a.B = Wblk;
+  a.L = S; a.ldl = r; a.R = V; a.ldr = L->n_in; a.nlr = r / b;
+  a.C = dX; a.ldc = L->n_in;
+  a.aux = aux;
+  a.epi = (int)epi;
+  a.M = T;
+  a.tiles = L->d_bwd_tiles; a.ntiles = (int)L->bwd_tiles.size();
+  a.kcols = L->d_kcols_bwd; a.blks = L->d_blks_bwd;
+  return hip_status(pf::launch_nt(dt, b, L->G_bwd, true, a, s), "backward-data kernel");
+}
+
+pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                               const void *dY, const void *X, const void *T_lr, const void *S,
+                               void *dWblk, void *dU, void *dV, void *workspace, size_t ws_bytes,
+                               void *stream) {
+  pf_status st = check_layout_arg(L);
+  if (st != PF_OK) return st;
+  if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = need_ptr(dY, "dY")) != PF_OK || (st = need_ptr(X, "X")) != PF_OK ||
+      (st = need_ptr(dWblk, "dWblk")) != PF_OK)
+    return st;
+  if (r > 0 && ((st = need_ptr(T_lr, "T_lr")) != PF_OK || (st = need_ptr(S, "S")) != PF_OK ||
+                (st = need_ptr(dU, "dU")) != PF_OK || (st = need_ptr(dV, "dV")) != PF_OK))
+    return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  pf::TNArgs a{};
+  a.A = dY; a.lda = L->n_out;
+  a.B = X; a.ldb = L->n_in;
+  a.Wout = dWblk;
+  a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
+  fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
+  a.T = T;
+  TNPlan p = tn_plan(pf::tn_items_total(a, L->b), T);
+  if (p.ws > 0) {
+    if (ws_bytes < p.ws)
+      return fail(PF_ERR_WORKSPACE, "workspace needs " + std::to_string(p.ws) + " bytes");
+    if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
+  }
+  a.nsplit = p.nsplit;
+  a.chunk = p.chunk;
+  a.partials = (float *)workspace;
+  return hip_status(pf::launch_tn((int)dtype, L->b, a, (hipStream_t)stream), "weight-gradient kernel");
+}
+
+pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_pre, void *dH_pre,
+                      void *stream) {
+  if (dtype != PF_BF16 && dtype != PF_FP32) return fail(PF_ERR_INVALID_ARG, "bad dtype");
+  if (n < 0) return fail(PF_ERR_INVALID_ARG, "n must be >= 0");
+  if (n == 0) return PF_OK;
+  pf_status st;
+  if ((st = need_ptr(dH, "dH")) != PF_OK || (st = need_ptr(H_pre, "H_pre")) != PF_OK ||
+      (st = need_ptr(dH_pre, "dH_pre")) != PF_OK)
+    return st;
+  return hip_status(pf::launch_gelu_bwd((int)dtype, n, dH, H_pre, dH_pre, (hipStream_t)stream),
+                    "gelu backward kernel");
+}
+
+static pf_status attn_check(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d) {
+  pf_status st = check_layout_arg(L);
+  if (st != PF_OK) return st;
+  if (B < 1 || H < 1 || Sq < 1) return fail(PF_ERR_INVALID_ARG, "B, H, Sq must be >= 1");
+  if (L->n_out != L->n_in || L->n_out != Sq)
+    return fail(PF_ERR_INVALID_ARG, "attention layout must be square with side Sq");
+  if (L->b != 64 || d != 64) return fail(PF_ERR_UNSUPPORTED, "attention supports b = 64, d = 64");
+  if ((int64_t)B * H > 0x7fffffff / (Sq / 64)) return fail(PF_ERR_INVALID_ARG, "too many blocks");
+  return PF_OK;
+}
+
+pf_status pf_attn_fwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d, float scale,
+                      const void *Q, const void *K, const void *V, void *O, float *lse, void *stream) {
+  pf_status st = attn_check(L, B, H, Sq, d);
+  if (st != PF_OK) return st;
+  if ((st = need_ptr(Q, "Q")) != PF_OK || (st = need_ptr(K, "K")) != PF_OK ||
+      (st = need_ptr(V, "V")) != PF_OK || (st = need_ptr(O, "O")) != PF_OK ||
+      (st = need_ptr(lse, "lse")) != PF_OK)
+    return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  pf::AttnArgs a{};
+  a.Q = Q; a.K = K; a.V = V; a.Oout = O; a.lse = lse;
+  a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
+  a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
+  a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
+  return hip_status(pf::launch_attn_fwd(a, (hipStream_t)stream), "attention forward kernel");
+}
+
+size_t pf_attn_workspace_bytes(int32_t B, int32_t H, int32_t Sq) {
+  if (B < 1 || H < 1 || Sq < 1) return 0;
+  return ((size_t)B * H * Sq * sizeof(float) + 255) / 256 * 256;
+}
+
+pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d, float scale,
+                      const void *Q, const void *K, const void *V, const void *O, const float *lse,
+                      const void *dO, void *dQ, void *dK, void *dV, void *workspace, size_t ws_bytes,
+                      void *stream) {
+  pf_status st = attn_check(L, B, H, Sq, d);
+  if (st != PF_OK) return st;
+  if ((st = need_ptr(Q, "Q")) != PF_OK || (st = need_ptr(K, "K")) != PF_OK ||
+      (st = need_ptr(V, "V")) != PF_OK || (st = need_ptr(O, "O")) != PF_OK ||
+      (st = need_ptr(lse, "lse")) != PF_OK || (st = need_ptr(dO, "dO")) != PF_OK ||
+      (st = need_ptr(dQ, "dQ")) != PF_OK || (st = need_ptr(dK, "dK")) != PF_OK ||
+      (st = need_ptr(dV, "dV")) != PF_OK)
+    return st;
+  if (ws_bytes < pf_attn_workspace_bytes(B, H, Sq))
+    return fail(PF_ERR_WORKSPACE, "workspace too small");
+  if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  pf::AttnArgs a{};
+  a.Q = Q; a.K = K; a.V = V; a.O = O; a.dO = dO;
+  a.dQ = dQ; a.dK = dK; a.dV = dV;
+  a.lse_in = lse; a.delta = (float *)workspace;
+  a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
+  a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
+  a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
+  return hip_status(pf::launch_attn_bwd(a, (hipStream_t)stream), "attention backward kernels");
+}
+
+size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K) {
+  if (dtype != PF_BF16 && dtype != PF_FP32) return 0;
+  if (op != PF_OP_TN || M < 64 || N < 64 || K < 1 || M % 64 || N % 64) return 0;
+  int items = (int)(((M / 64 + 1) / 2) * ((N / 64 + 1) / 2));
+  return tn_plan(items, K).ws;
+}
+
+pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K,
+                        const void *A, const void *B, void *C, void *workspace, size_t ws_bytes,
+                        void *stream) {
+  if (dtype != PF_BF16 && dtype != PF_FP32) return fail(PF_ERR_INVALID_ARG, "bad dtype");
+  if (M < 1 || N < 1 || K < 1) return fail(PF_ERR_INVALID_ARG, "M, N, K must be >= 1");
+  if (M % 64 || N % 64) return fail(PF_ERR_UNSUPPORTED, "M and N must be multiples of 64");
+  if (op != PF_OP_TN && K % 64) return fail(PF_ERR_UNSUPPORTED, "K must be a multiple of 64");
+  if (M / 64 > (1 << 24) || N / 64 > (1 << 24) || K / 64 > (1 << 24))
+    return fail(PF_ERR_INVALID_ARG, "dimensions too large");
+  pf_status st;
+  if ((st = need_ptr(A, "A")) != PF_OK || (st = need_ptr(B, "B")) != PF_OK ||
+      (st = need_ptr(C, "C")) != PF_OK)
+    return st;
+  hipStream_t s = (hipStream_t)stream;
+  const int dt = (int)dtype;
+  switch (op) {
+    case PF_OP_NT:
+      return dense_nt(dt, 64, false, M, A, K, B, K, (int)(K / 64), (int)(N / 64), C, N, s, "dense NT");
+    case PF_OP_NN:
+      return dense_nt(dt, 64, true, M, A, K, B, N, (int)(K / 64), (int)(N / 64), C, N, s, "dense NN");
+    case PF_OP_TN: {
+      pf::TNArgs a{};
+      a.n_items = 0;
+      a.dr[0] = pf::TNDense{A, M, B, N, C, N, (int)(M / 64), (int)(N / 64)};
+      a.n_dense = 1;
+      a.T = K;
+      TNPlan p = tn_plan(pf::tn_items_total(a, 64), K);
+      if (p.ws > 0) {
+        if (ws_bytes < p.ws)
+          return fail(PF_ERR_WORKSPACE, "workspace needs " + std::to_string(p.ws) + " bytes");
+        if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
+      }
+      a.nsplit = p.nsplit;
+      a.chunk = p.chunk;
+      a.partials = (float *)workspace;
+      return hip_status(pf::launch_tn(dt, 64, a, s), "dense TN");
+    }
+  }
+  return fail(PF_ERR_INVALID_ARG, "bad op");
+}
+
+}  // extern "C"

@@ -1,0 +1,281 @@
+// Flat block butterfly layout builder (host only).
+//
+// Mask: Section 3.1 (block butterfly factor B_k: [[D1 D2],[D3 D4]] with
+// block-diagonal D_i; factor matrix: block-diagonal copies of one factor),
+// Section 3.2 (flat butterfly of maximum stride k = I + B_2 + ... + B_k).
+// In block units the support of B_k pairs p with p XOR k/2 (the two
+// diagonal positions of one factor that share the in-quadrant offset), so the
+// flat pattern keeps (p, q) iff p XOR q is 0 or a power of two below the
+// maximum stride.  A square side s that is not a power of two is the
+// power-of-two pattern cropped to s; rectangular weights repeat ("stretch")
+// the s x s square along the longer dimension (appendix on method details,
+// rectangular matrices).
+#include "layout.h"
+
+#include <algorithm>
+#include <map>
+#include <string>
+#include <vector>
+
+namespace pf {
+
+int max_group(int32_t b) {
+  if (b == 32 || b == 64) return 4;
+  if (b == 128) return 2;
+  return 1;
+}
+
+static int tn_group(int32_t b) {
+  int g = b > 0 ? 128 / b : 1;
+  return std::max(1, std::min(kTNMax, g));
+}
+
+static bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+// Choose the largest G (power of two <= gmax) whose partial tiles waste at
+// most a quarter of the tile rows.
+static int choose_group(const std::vector<std::vector<int32_t>> &groups,
+                        int gmax) {
+  int64_t rows = 0;
+  for (auto &g : groups) rows += (int64_t)g.size();
+  for (int G = gmax; G > 1; G /= 2) {
+    int64_t tiles = 0;
+    for (auto &g : groups) tiles += ((int64_t)g.size() + G - 1) / G;
+    if ((tiles * G - rows) * 4 <= rows) return G;
+  }
+  return 1;
+}
+
+// Group the block rows of a CSR-like structure by identical index lists.
+static std::vector<std::vector<int32_t>> group_identical(
+    const std::vector<int32_t> &ptr, const std::vector<int32_t> &idx) {
+  std::map<std::vector<int32_t>, int> where;
+  std::vector<std::vector<int32_t>> groups;
+  int n = (int)ptr.size() - 1;
+  for (int i = 0; i < n; ++i) {
+    std::vector<int32_t> key(idx.begin() + ptr[i], idx.begin() + ptr[i + 1]);
+    auto it = where.find(key);
+    if (it == where.end()) {
+      where.emplace(key, (int)groups.size());
+      groups.push_back({i});
+    } else {
+      groups[it->second].push_back(i);
+    }
+  }
+  return groups;
+}
+
+// NT tiles over the rows of (ptr, idx).  blk_of(row, slot) gives the packed
+// block index of the slot-th kept block of that row.
+template <class BlkOf>
+static void build_nt_tiles(const std::vector<int32_t> &ptr,
+                           const std::vector<int32_t> &idx, int gmax,
+                           BlkOf blk_of, int &G, std::vector<NTTile> &tiles,
+                           std::vector<int32_t> &kcols,
+                           std::vector<int32_t> &blks) {
+  auto groups = group_identical(ptr, idx);
+  G = choose_group(groups, gmax);
+  tiles.clear();
+  kcols.clear();
+  blks.clear();
+  for (auto &grp : groups) {
+    int r0 = grp[0];
+    int nsteps = ptr[r0 + 1] - ptr[r0];
+    int kcol_off = (int)kcols.size();
+    for (int c = 0; c < nsteps; ++c) kcols.push_back(idx[ptr[r0] + c]);
+    for (size_t t0 = 0; t0 < grp.size(); t0 += G) {
+      NTTile t{};
+      t.g = (int)std::min<size_t>(G, grp.size() - t0);
+      t.nsteps = nsteps;
+      t.kcol_off = kcol_off;
+      t.blk_off = (int)blks.size();
+      for (int g = 0; g < kMaxG; ++g)
+        t.out_blk[g] = g < t.g ? grp[t0 + g] : grp[t0];
+      for (int c = 0; c < nsteps; ++c)
+        for (int g = 0; g < G; ++g)
+          blks.push_back(blk_of(g < t.g ? grp[t0 + g] : grp[t0], c));
+      tiles.push_back(t);
+    }
+  }
+}
+
+static int32_t csr_pos(const pf_layout &L, int i, int j) {
+  auto b = L.col_idx.begin() + L.row_ptr[i], e = L.col_idx.begin() + L.row_ptr[i + 1];
+  auto it = std::lower_bound(b, e, j);
+  return (it != e && *it == j) ? (int32_t)(it - L.col_idx.begin()) : -1;
+}
+
+static void build_tn_items(pf_layout &L) {
+  const int GA = tn_group(L.b), GB = GA;
+  auto groups = group_identical(L.row_ptr, L.col_idx);
+  std::vector<std::vector<int32_t>> bundles;
+  std::vector<int32_t> leftover;
+  for (auto &grp : groups) {
+    size_t full = grp.size() / GA * GA;
+    for (size_t t = 0; t < full; t += GA)
+      bundles.emplace_back(grp.begin() + t, grp.begin() + t + GA);
+    for (size_t t = full; t < grp.size(); ++t) leftover.push_back(grp[t]);
+  }
+  std::sort(leftover.begin(), leftover.end());
+  for (size_t t = 0; t < leftover.size(); t += GA)
+    bundles.emplace_back(leftover.begin() + t,
+                         leftover.begin() + std::min(leftover.size(), t + GA));
+  L.tn_items.clear();
+  for (auto &bun : bundles) {
+    std::vector<int32_t> cols;
+    for (int i : bun)
+      cols.insert(cols.end(), L.col_idx.begin() + L.row_ptr[i],
+                  L.col_idx.begin() + L.row_ptr[i + 1]);
+    std::sort(cols.begin(), cols.end());
+    cols.erase(std::unique(cols.begin(), cols.end()), cols.end());
+    for (size_t c0 = 0; c0 < cols.size(); c0 += GB) {
+      TNItem it{};
+      it.na = (int)bun.size();
+      it.nb = (int)std::min<size_t>(GB, cols.size() - c0);
+      for (int a = 0; a < kTNMax; ++a) it.a_col[a] = a < it.na ? bun[a] : bun[0];
+      for (int b = 0; b < kTNMax; ++b) it.b_col[b] = b < it.nb ? cols[c0 + b] : cols[c0];
+      for (int a = 0; a < kTNMax; ++a)
+        for (int b = 0; b < kTNMax; ++b)
+          it.out_blk[a * kTNMax + b] =
+              (a < it.na && b < it.nb) ? csr_pos(L, bun[a], cols[c0 + b]) : -1;
+      L.tn_items.push_back(it);
+    }
+  }
+}
+
+std::string build_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
+                         int32_t max_stride) {
+  if (b < 1) return "block size b must be >= 1";
+  if (n_out < 1 || n_in < 1) return "n_out and n_in must be >= 1";
+  if (n_out % b || n_in % b) return "b must divide n_out and n_in";
+  if (!is_pow2(max_stride)) return "max_stride must be a power of two >= 1";
+  if (n_out / b > (1 << 30) || n_in / b > (1 << 30)) return "too many blocks";
+  L.n_out = n_out;
+  L.n_in = n_in;
+  L.b = b;
+  L.max_stride = max_stride;
+  L.nb_out = (int32_t)(n_out / b);
+  L.nb_in = (int32_t)(n_in / b);
+  L.s = std::min(L.nb_out, L.nb_in);
+  int64_t P = 1;
+  while (P < L.s) P *= 2;
+  L.eff_stride = (int32_t)std::min<int64_t>(max_stride, P);
+
+  // Kept in-square columns of each square row.
+  std::vector<std::vector<int32_t>> sq(L.s);
+  for (int32_t ii = 0; ii < L.s; ++ii)
+    for (int32_t jj = 0; jj < L.s; ++jj) {
+      int32_t x = ii ^ jj;
+      if (x == 0 || (is_pow2(x) && x < max_stride)) sq[ii].push_back(jj);
+    }
+  L.row_ptr.assign(1, 0);
+  L.col_idx.clear();
+  for (int32_t i = 0; i < L.nb_out; ++i) {
+    for (int64_t base = 0; base < L.nb_in; base += L.s)
+      for (int32_t jj : sq[i % L.s])
+        if (base + jj < L.nb_in) L.col_idx.push_back((int32_t)(base + jj));
+    L.row_ptr.push_back((int32_t)L.col_idx.size());
+  }
+  return finish_layout(L);
+}
+
+std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, int32_t b,
+                                   const uint8_t *mask) {
+  if (b < 1) return "block size b must be >= 1";
+  if (nb_out < 1 || nb_in < 1) return "nb_out and nb_in must be >= 1";
+  if (!mask) return "mask is NULL";
+  if ((int64_t)nb_out * b > ((int64_t)1 << 40) || (int64_t)nb_in * b > ((int64_t)1 << 40))
+    return "too large";
+  L.n_out = (int64_t)nb_out * b;
+  L.n_in = (int64_t)nb_in * b;
+  L.b = b;
+  L.max_stride = 0;
+  L.eff_stride = 0;
+  L.nb_out = nb_out;
+  L.nb_in = nb_in;
+  L.s = std::min(nb_out, nb_in);
+  L.row_ptr.assign(1, 0);
+  L.col_idx.clear();
+  for (int32_t i = 0; i < nb_out; ++i) {
+    for (int32_t j = 0; j < nb_in; ++j)
+      if (mask[(int64_t)i * nb_in + j]) L.col_idx.push_back(j);
+    if (L.col_idx.size() == (size_t)L.row_ptr.back())
+      return "every block row needs at least one kept block";
+    L.row_ptr.push_back((int32_t)L.col_idx.size());
+  }
+  return finish_layout(L);
+}
+
+// CSC, work lists and their self-check, from row_ptr / col_idx.
+std::string finish_layout(pf_layout &L) {
+  L.nnzb = (int64_t)L.col_idx.size();
+  if (L.nnzb > (int64_t)1 << 30) return "too many kept blocks";
+
+  // Transpose (CSC); rows ascending within a column.
+  L.col_ptr.assign(L.nb_in + 1, 0);
+  for (int32_t j : L.col_idx) L.col_ptr[j + 1]++;
+  for (int32_t j = 0; j < L.nb_in; ++j) L.col_ptr[j + 1] += L.col_ptr[j];
+  L.row_idx.assign(L.nnzb, 0);
+  L.tperm.assign(L.nnzb, 0);
+  std::vector<int32_t> fill(L.col_ptr.begin(), L.col_ptr.end() - 1);
+  for (int32_t i = 0; i < L.nb_out; ++i)
+    for (int32_t p = L.row_ptr[i]; p < L.row_ptr[i + 1]; ++p) {
+      int32_t q = fill[L.col_idx[p]]++;
+      L.row_idx[q] = i;
+      L.tperm[q] = p;
+    }
+
+  const int gmax = max_group(L.b);
+  build_nt_tiles(
+      L.row_ptr, L.col_idx, gmax,
+      [&](int row, int c) { return L.row_ptr[row] + c; }, L.G_fwd,
+      L.fwd_tiles, L.kcols_fwd, L.blks_fwd);
+  build_nt_tiles(
+      L.col_ptr, L.row_idx, gmax,
+      [&](int col, int c) { return L.tperm[L.col_ptr[col] + c]; }, L.G_bwd,
+      L.bwd_tiles, L.kcols_bwd, L.blks_bwd);
+  build_tn_items(L);
+  return check_layout(L);
+}
+
+std::string check_layout(const pf_layout &L) {
+  std::vector<int> seen(L.nnzb, 0);
+  auto sweep = [&](const std::vector<NTTile> &tiles,
+                   const std::vector<int32_t> &kcols,
+                   const std::vector<int32_t> &blks, int G,
+                   bool transposed) -> std::string {
+    std::fill(seen.begin(), seen.end(), 0);
+    for (auto &t : tiles) {
+      if (t.g < 1 || t.g > G) return "tile row count out of range";
+      for (int c = 0; c < t.nsteps; ++c)
+        for (int g = 0; g < t.g; ++g) {
+          int k = kcols[t.kcol_off + c], o = t.out_blk[g];
+          int32_t want = transposed ? csr_pos(L, k, o) : csr_pos(L, o, k);
+          int32_t got = blks[t.blk_off + c * G + g];
+          if (want < 0 || got != want) return "tile block index mismatch";
+          seen[got]++;
+        }
+    }
+    for (int v : seen)
+      if (v != 1) return "tiles do not cover each kept block exactly once";
+    return "";
+  };
+  std::string e = sweep(L.fwd_tiles, L.kcols_fwd, L.blks_fwd, L.G_fwd, false);
+  if (!e.empty()) return "forward: " + e;
+  e = sweep(L.bwd_tiles, L.kcols_bwd, L.blks_bwd, L.G_bwd, true);
+  if (!e.empty()) return "backward-data: " + e;
+  std::fill(seen.begin(), seen.end(), 0);
+  for (auto &it : L.tn_items)
+    for (int a = 0; a < it.na; ++a)
+      for (int b = 0; b < it.nb; ++b) {
+        int32_t p = it.out_blk[a * kTNMax + b];
+        if (p != csr_pos(L, it.a_col[a], it.b_col[b]))
+          return "weight-gradient item block index mismatch";
+        if (p >= 0) seen[p]++;
+      }
+  for (int v : seen)
+    if (v != 1) return "weight-gradient items do not cover each kept block once";
+  return "";
+}
+
+}  // namespace pf

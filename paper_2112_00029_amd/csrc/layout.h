@@ -1,0 +1,49 @@
+// Layout object: flat block butterfly block-CSR plus the kernel work lists.
+#pragma once
+
+#include <string>
+#include <vector>
+
+#include "pf_internal.h"
+#include "pixelfly.h"
+
+struct pf_layout {
+  int64_t n_out = 0, n_in = 0;
+  int32_t b = 0, max_stride = 0, eff_stride = 0, s = 0, nb_out = 0, nb_in = 0;
+  int64_t nnzb = 0;
+  std::vector<int32_t> row_ptr, col_idx, col_ptr, row_idx, tperm;
+
+  // Work lists.  Forward NT tiles cover output block rows (tiles of G_fwd
+  // rows with identical column sets); backward-data NT tiles cover block
+  // columns (tiles of G_bwd columns with identical row sets); TN items cover
+  // the kept blocks for the weight gradient.
+  int G_fwd = 1, G_bwd = 1;
+  std::vector<pf::NTTile> fwd_tiles, bwd_tiles;
+  std::vector<int32_t> kcols_fwd, blks_fwd, kcols_bwd, blks_bwd;
+  std::vector<pf::TNItem> tn_items;
+
+  // Device copies (valid after pf_layout_upload).
+  int device = -1;
+  void *dev_mem = nullptr;
+  const pf::NTTile *d_fwd_tiles = nullptr, *d_bwd_tiles = nullptr;
+  const int32_t *d_kcols_fwd = nullptr, *d_blks_fwd = nullptr;
+  const int32_t *d_kcols_bwd = nullptr, *d_blks_bwd = nullptr;
+  const pf::TNItem *d_tn_items = nullptr;
+  const int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
+  const int32_t *d_col_ptr = nullptr, *d_row_idx = nullptr;
+};
+
+namespace pf {
+// Build mask + block-CSR + work lists (host only).  Returns "" or an error.
+std::string build_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
+                         int32_t max_stride);
+// Same from an explicit nb_out x nb_in block mask (row-major, nonzero =
+// kept); every block row must keep at least one block.
+std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, int32_t b,
+                                   const uint8_t *mask);
+std::string finish_layout(pf_layout &L);
+// Re-verify the work lists against the block-CSR.  Returns "" or an error.
+std::string check_layout(const pf_layout &L);
+// Blocks per NT tile row-group the kernels are instantiated for.
+int max_group(int32_t b);
+}  // namespace pf

@@ -1,0 +1,114 @@
+// Internal declarations shared by the host library code and the HIP kernels.
+// Not part of the public ABI (see include/pixelfly.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pf {
+
+// Maximum block rows one NT output tile covers, and blocks per side of a TN
+// (weight-gradient) tile.
+constexpr int kMaxG = 8;
+constexpr int kTNMax = 4;
+
+// One output column-tile of the block-sparse "NT" GEMM
+//   C[:, out_blk[g]] = sum_c A[:, kcol(c)] . Bblk(g, c)^T  (+ low-rank)
+// used by the forward (blocks of M o W) and by backward-data (blocks of the
+// transposed layout).  All g rows of a tile share the same K-block list.
+struct NTTile {
+  int32_t g;         // valid block rows in this tile (<= the kernel's G)
+  int32_t nsteps;    // kept K blocks
+  int32_t kcol_off;  // offset into kcols: A column block of step c
+  int32_t blk_off;   // offset into blks: [nsteps][G] packed block index
+  int32_t out_blk[kMaxG];
+};
+
+// One weight-gradient tile: a (na*b) x (nb*b) slab of dY^T X of which the
+// blocks with out_blk[ga*kTNMax + gb] >= 0 are kept (that CSR position).
+struct TNItem {
+  int32_t na, nb;
+  int32_t a_col[kTNMax];  // dY column blocks (block rows of W)
+  int32_t b_col[kTNMax];  // X column blocks (block columns of W)
+  int32_t out_blk[kTNMax * kTNMax];
+};
+
+// Arguments of the NT kernel family.
+struct NTArgs {
+  const void *A;        // T x lda (X or dY)
+  int64_t lda;
+  const void *B;        // packed blocks (dense == 0) or a dense matrix
+  int64_t ldb;          // dense B row stride
+  int dense;            // 1: K-steps are 0..nsteps-1, B dense (comparator)
+  int dense_nsteps;     // dense mode: K / b
+  int dense_nblk;       // dense mode: output blocks (N / b)
+  const void *L;        // low-rank left operand T x r (T_lr or S), or null
+  int64_t ldl;
+  const void *R;        // low-rank right operand: U (N x r) or V (r x K)
+  int64_t ldr;
+  int nlr;              // r / b low-rank K-blocks
+  void *C;              // T x ldc output
+  int64_t ldc;
+  void *C2;             // GELU forward: pre-activation output
+  const void *aux;      // GELU backward: pre-activation input
+  int epi;
+  int64_t M;            // tokens
+  const NTTile *tiles;  // null in dense mode
+  int ntiles;           // output column tiles (dense mode: ceil(nblk / G))
+  const int32_t *kcols;
+  const int32_t *blks;
+};
+
+// A dense region of the TN kernel: out[a][b] = sum_t A[t][a] B[t][b] over
+// na_blk x nb_blk blocks (e.g. dU = dY^T T_lr, dV = S^T X).
+struct TNDense {
+  const void *A;
+  int64_t lda;
+  const void *B;
+  int64_t ldb;
+  void *out;
+  int64_t ldo;
+  int na_blk, nb_blk;   // in blocks
+};
+
+struct TNArgs {
+  const void *A;        // sparse region: dY (T x lda)
+  int64_t lda;
+  const void *B;        // sparse region: X (T x ldb)
+  int64_t ldb;
+  void *Wout;           // packed dW
+  const TNItem *items;
+  int n_items;
+  TNDense dr[2];
+  int n_dense;
+  int64_t T;
+  int nsplit;
+  int64_t chunk;        // tokens per split (multiple of 32)
+  float *partials;      // [items_total][nsplit][128*128] when nsplit > 1
+};
+
+struct AttnArgs {
+  const void *Q, *K, *V, *O, *dO;
+  void *Oout, *dQ, *dK, *dV;
+  float *lse;
+  const float *lse_in;
+  float *delta;
+  int BH, S, nbq;
+  float scale;
+  const int32_t *row_ptr, *col_idx, *col_ptr, *row_idx;
+};
+
+// Kernel launchers (gemm_kernels.hip / attn_kernels.hip).
+hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, const NTArgs &a,
+                     hipStream_t s);
+hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
+int tn_items_total(const TNArgs &a, int blk);
+hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
+                           const void *Hpre, void *out, hipStream_t s);
+hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s);
+hipError_t launch_attn_bwd(const AttnArgs &a, hipStream_t s);
+
+// Static counter array (one per device) for split-token reductions.
+constexpr int kMaxCounters = 1 << 16;
+
+}  // namespace pf

@@ -1,0 +1,214 @@
+"""GPU parity of the sparse + low-rank linear layer against the fp64 oracle.
+
+Every case runs forward, backward-data and backward-weight through the C ABI
+(libpixelfly.so) and compares each output with the oracle element by element
+(relative Frobenius error; bf16 <= 2e-2, fp32 <= 1e-5), plus bit-exact cases
+on integer-valued inputs.
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle import linear as ol
+from oracle import mask as om
+from tests._gpu_util import TOL, bf16_round, empty, rel_fro, to_dev, to_host, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(n_out, n_in, b, ms, T, r, dtype, seed=0, std=(0.02, 0.02, 0.02, 0.02), ints=None):
+    """Seeded inputs; W drawn directly as packed kept blocks (oracle CSR)."""
+    M, (row_ptr, col_idx, *_r) = om.layout(n_out, n_in, b, ms)
+    nnzb = int(M.sum())
+    sx, sw, suv, sdy = std
+    if ints is None:
+        X, Xr = synth.draw((T, n_in), sx, seed, 1, dtype)
+        W, Wr = synth.draw((nnzb, b, b), sw, seed, 2, dtype)
+        U, Ur = synth.draw((n_out, r), suv, seed, 3, dtype)
+        V, Vr = synth.draw((r, n_in), suv, seed, 4, dtype)
+        dY, dYr = synth.draw((T, n_out), sdy, seed, 5, dtype)
+    else:
+        lo, hi = ints
+        X, Xr = synth.draw_int((T, n_in), lo, hi, seed, 1, dtype)
+        W, Wr = synth.draw_int((nnzb, b, b), lo, hi, seed, 2, dtype)
+        U, Ur = synth.draw_int((n_out, r), lo, hi, seed, 3, dtype)
+        V, Vr = synth.draw_int((r, n_in), lo, hi, seed, 4, dtype)
+        dY, dYr = synth.draw_int((T, n_out), lo, hi, seed, 5, dtype)
+    Wd = ol.unpack(W, row_ptr, col_idx, n_out // b, n_in // b, b)
+    return dict(M=M, Mel=om.element_mask(M, b), X=X, W=W, Wd=Wd, U=U, V=V, dY=dY,
+                raw=dict(X=Xr, W=Wr, U=Ur, V=Vr, dY=dYr))
+
+
+def _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp):
+    """fwd, bwd-data, bwd-weight through the C ABI; returns float64 outputs."""
+    torch = torch_cuda()
+    from paper_2112_00029_amd import pixelfly as pf
+    print(f"[linear] n_out={n_out} n_in={n_in} b={b} ms={ms} T={T} r={r} {dtype}", flush=True)
+    L = pf.pf_layout_create(n_out, n_in, b, ms)
+    pf.pf_layout_upload(L)
+    d = {k: to_dev(v) for k, v in inp["raw"].items()}
+    Y = empty((T, n_out), dtype)
+    dX = empty((T, n_in), dtype)
+    dW = empty(tuple(d["W"].shape), dtype)
+    Tl = empty((T, max(r, 1)), dtype)
+    S = empty((T, max(r, 1)), dtype)
+    dU = empty((n_out, max(r, 1)), dtype)
+    dV = empty((max(r, 1), n_in), dtype)
+    U = d["U"] if r else None
+    V = d["V"] if r else None
+    pf.pf_linear_fwd(L, dtype, T, r, d["X"], d["W"], U, V, Y, Tl if r else None)
+    pf.pf_linear_bwd_data(L, dtype, T, r, d["dY"], d["W"], U, V, S if r else None, dX)
+    ws_bytes = pf.pf_workspace_bytes(L, T, r, dtype)
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    pf.pf_linear_bwd_weight(L, dtype, T, r, d["dY"], d["X"], Tl if r else None,
+                            S if r else None, dW, dU if r else None, dV if r else None,
+                            ws, ws_bytes)
+    torch.cuda.synchronize()
+    out = dict(Y=to_host(Y), dX=to_host(dX), dW=to_host(dW))
+    if r:
+        out.update(T_lr=to_host(Tl), S=to_host(S), dU=to_host(dU), dV=to_host(dV))
+    return out, L
+
+
+def _oracle(inp, r, b):
+    U = inp["U"] if r else None
+    V = inp["V"] if r else None
+    Y, Tlr = ol.forward(inp["X"], inp["Wd"], U, V)
+    g = ol.backward(inp["X"], inp["Wd"], inp["Mel"], inp["dY"], U, V)
+    ref = dict(Y=Y, dX=g["dX"], dW_dense=g["dW"])
+    if r:
+        ref.update(T_lr=Tlr, S=g["S"], dU=g["dU"], dV=g["dV"])
+    return ref
+
+
+def _pack_ref(ref, n_out, n_in, b, ms):
+    _, (row_ptr, col_idx, *_r) = om.layout(n_out, n_in, b, ms)
+    return ol.pack(ref["dW_dense"], row_ptr, col_idx, n_out // b, b)
+
+
+CASES = [
+    # (n_out, n_in, b, max_stride, T, r, dtype)
+    pytest.param(1024, 1024, 32, 32, 256, 32, "fp32", id="fp32_1024sq_b32_full"),
+    pytest.param(3072, 768, 32, 16, 4096, 96, "bf16", id="mlp_fc1_full"),
+    pytest.param(3072, 768, 32, 16, 300, 96, "bf16", id="mlp_fc1_ragged300"),
+    pytest.param(4096, 1024, 64, 16, 520, 128, "bf16", id="fc1_1024x4096_b64_T520"),
+    pytest.param(1024, 4096, 64, 16, 520, 128, "bf16", id="fc2_4096x1024_b64_T520"),
+    pytest.param(16384, 4096, 128, 32, 200, 256, "bf16", id="large_b128_T200"),
+    pytest.param(16384, 4096, 64, 32, 200, 256, "bf16", id="large_b64_T200"),
+    pytest.param(16384, 4096, 32, 32, 200, 256, "bf16", id="large_b32_T200"),
+    pytest.param(512, 512, 32, 1, 130, 0, "bf16", id="blockdiag_r0"),
+    pytest.param(128, 128, 64, 2, 1, 64, "bf16", id="dense_mask_T1"),
+    pytest.param(384, 640, 64, 1024, 77, 64, "bf16", id="clamped_stride_rect"),
+    pytest.param(768, 256, 128, 2, 129, 128, "fp32", id="fp32_b128"),
+    pytest.param(512, 256, 64, 4, 200, 64, "fp32", id="fp32_b64"),
+]
+
+
+@pytest.mark.parametrize("n_out,n_in,b,ms,T,r,dtype", CASES)
+def test_linear_parity(n_out, n_in, b, ms, T, r, dtype):
+    std = (1.0, 1.0 / np.sqrt(6 * 32), 1.0 / 32, 1.0) if dtype == "fp32" else (0.02,) * 4
+    inp = _inputs(n_out, n_in, b, ms, T, r, dtype, std=std)
+    got, _ = _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp)
+    ref = _oracle(inp, r, b)
+    ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
+    tol = TOL[dtype]
+    for k in ["Y", "dX", "dW"] + (["T_lr", "S", "dU", "dV"] if r else []):
+        e = rel_fro(got[k], ref[k])
+        print(f"  {k}: rel_fro={e:.3e}", flush=True)
+        assert e <= tol, (k, e)
+
+
+def test_fp32_integer_inputs_bit_exact():
+    """Integer inputs in [-2, 2], fp32 I/O: every partial sum is an integer
+    below 2^24, so the GPU result equals the oracle exactly."""
+    n_out, n_in, b, ms, T, r = 1024, 1024, 32, 32, 256, 32
+    inp = _inputs(n_out, n_in, b, ms, T, r, "fp32", ints=(-2, 2))
+    got, _ = _run_gpu(n_out, n_in, b, ms, T, r, "fp32", inp)
+    ref = _oracle(inp, r, b)
+    ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
+    for k in ["Y", "dX", "dW", "T_lr", "S", "dU", "dV"]:
+        assert np.array_equal(got[k], ref[k]), k
+
+
+@pytest.mark.parametrize("b", [32, 64])
+def test_bf16_integer_inputs_bit_exact(b):
+    """Values in [-1, 1] and small dims keep T_lr and S integers <= 256
+    (exact in bf16); outputs must equal the oracle rounded once to bf16."""
+    n_out, n_in, ms, T, r = 2 * b, 2 * b, 2, 96, b
+    inp = _inputs(n_out, n_in, b, ms, T, r, "bf16", ints=(-1, 1))
+    got, _ = _run_gpu(n_out, n_in, b, ms, T, r, "bf16", inp)
+    ref = _oracle(inp, r, b)
+    ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
+    assert np.abs(ref["T_lr"]).max() <= 256 and np.abs(ref["S"]).max() <= 256
+    for k in ["Y", "dX", "dW", "T_lr", "S", "dU", "dV"]:
+        assert np.array_equal(got[k], bf16_round(ref[k])), k
+
+
+def test_mlp_pair_gelu():
+    """Two layers 1024 -> 4096 -> GELU -> 1024 (b = 64, stride 16, r = 128)
+    with the GELU epilogues: forward keeps the pre-activation, backward-data
+    of the second layer applies gelu'(pre-activation)."""
+    torch = torch_cuda()
+    from paper_2112_00029_amd import pixelfly as pf
+    T, K, N, b, ms, r = 390, 1024, 4096, 64, 16, 128
+    dtype = "bf16"
+    l1 = _inputs(N, K, b, ms, T, r, dtype, seed=0)
+    l2 = _inputs(K, N, b, ms, T, r, dtype, seed=1)
+    print("[mlp_pair] T=390", flush=True)
+    L1 = pf.pf_layout_create(N, K, b, ms)
+    L2 = pf.pf_layout_create(K, N, b, ms)
+    pf.pf_layout_upload(L1)
+    pf.pf_layout_upload(L2)
+    X = to_dev(l1["raw"]["X"])
+    W1, U1, V1 = (to_dev(l1["raw"][k]) for k in ("W", "U", "V"))
+    W2, U2, V2 = (to_dev(l2["raw"][k]) for k in ("W", "U", "V"))
+    dY = to_dev(l2["raw"]["dY"])
+    Hpre, H, T1 = empty((T, N), dtype), empty((T, N), dtype), empty((T, r), dtype)
+    Y, T2 = empty((T, K), dtype), empty((T, r), dtype)
+    pf.pf_linear_fwd(L1, dtype, T, r, X, W1, U1, V1, H, T1, pf.PF_EPI_GELU, Hpre)
+    pf.pf_linear_fwd(L2, dtype, T, r, H, W2, U2, V2, Y, T2)
+    dHpre, S2, dX, S1 = empty((T, N), dtype), empty((T, r), dtype), empty((T, K), dtype), empty((T, r), dtype)
+    pf.pf_linear_bwd_data(L2, dtype, T, r, dY, W2, U2, V2, S2, dHpre, pf.PF_EPI_GELU, Hpre)
+    pf.pf_linear_bwd_data(L1, dtype, T, r, dHpre, W1, U1, V1, S1, dX)
+    dW1, dU1, dV1 = empty(tuple(W1.shape), dtype), empty((N, r), dtype), empty((r, K), dtype)
+    dW2, dU2, dV2 = empty(tuple(W2.shape), dtype), empty((K, r), dtype), empty((r, N), dtype)
+    ws_b = max(pf.pf_workspace_bytes(L1, T, r, dtype), pf.pf_workspace_bytes(L2, T, r, dtype))
+    ws = torch.empty(max(ws_b, 256), dtype=torch.uint8, device="cuda")
+    pf.pf_linear_bwd_weight(L2, dtype, T, r, dY, H, T2, S2, dW2, dU2, dV2, ws, ws_b)
+    pf.pf_linear_bwd_weight(L1, dtype, T, r, dHpre, X, T1, S1, dW1, dU1, dV1, ws, ws_b)
+    # standalone GELU backward agrees with the fused epilogue's definition
+    dHpre2 = empty((T, N), dtype)
+    dH_alone = empty((T, N), dtype)
+    pf.pf_linear_bwd_data(L2, dtype, T, r, dY, W2, U2, V2, S2, dH_alone)
+    pf.pf_gelu_bwd(dtype, T * N, dH_alone, Hpre, dHpre2)
+    torch.cuda.synchronize()
+
+    ref_f = ol.mlp_pair_forward(l1["X"], l1["Wd"], l1["U"], l1["V"], l2["Wd"], l2["U"], l2["V"])
+    ref_b = ol.mlp_pair_backward(l1["X"], l1["Wd"], l1["Mel"], l1["U"], l1["V"], l2["Wd"],
+                                 l2["Mel"], l2["U"], l2["V"], l2["dY"], fwd=ref_f)
+    _, (rp1, ci1, *_a) = om.layout(N, K, b, ms)
+    _, (rp2, ci2, *_b) = om.layout(K, N, b, ms)
+    checks = {
+        "H_pre": (Hpre, ref_f["H_pre"]), "H": (H, ref_f["H"]), "Y": (Y, ref_f["Y"]),
+        "dH_pre": (dHpre, ref_b["dH_pre"]), "dH_pre_standalone": (dHpre2, ref_b["dH_pre"]),
+        "dX": (dX, ref_b["l1"]["dX"]),
+        "dW2": (dW2, ol.pack(ref_b["l2"]["dW"], rp2, ci2, K // b, b)),
+        "dU2": (dU2, ref_b["l2"]["dU"]), "dV2": (dV2, ref_b["l2"]["dV"]),
+        "dW1": (dW1, ol.pack(ref_b["l1"]["dW"], rp1, ci1, N // b, b)),
+        "dU1": (dU1, ref_b["l1"]["dU"]), "dV1": (dV1, ref_b["l1"]["dV"]),
+    }
+    for k, (g, rf) in checks.items():
+        e = rel_fro(to_host(g), rf)
+        print(f"  {k}: rel_fro={e:.3e}", flush=True)
+        assert e <= TOL[dtype], (k, e)
+
+
+def test_repeat_calls_are_deterministic():
+    """Split-token weight gradients combine partials in a fixed order: two
+    runs give identical bits (and the completion counters reset)."""
+    n_out, n_in, b, ms, T, r = 3072, 768, 32, 16, 4096, 96
+    inp = _inputs(n_out, n_in, b, ms, T, r, "bf16", seed=3)
+    a, _ = _run_gpu(n_out, n_in, b, ms, T, r, "bf16", inp)
+    c, _ = _run_gpu(n_out, n_in, b, ms, T, r, "bf16", inp)
+    for k in a:
+        assert np.array_equal(a[k], c[k]), k
