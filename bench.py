@@ -111,9 +111,11 @@ class Linear:
     def call(self, name):
         pf, T, r, dt = self.pf, self.wl.T, self.wl.r, self.dtype
         if name == "fwd":
-            pf.pf_linear_fwd(self.L, dt, T, r, self.X, self.W, self.U, self.V, self.Y, self.Tl)
+            pf.pf_linear_fwd(self.L, dt, T, r, self.X, self.W, self.U, self.V, self.Y, self.Tl,
+                             workspace=self.ws, ws_bytes=self.wsb)
         elif name == "bwd_data":
-            pf.pf_linear_bwd_data(self.L, dt, T, r, self.dY, self.W, self.U, self.V, self.S, self.dX)
+            pf.pf_linear_bwd_data(self.L, dt, T, r, self.dY, self.W, self.U, self.V, self.S, self.dX,
+                                  workspace=self.ws, ws_bytes=self.wsb)
         else:
             pf.pf_linear_bwd_weight(self.L, dt, T, r, self.dY, self.X, self.Tl, self.S, self.dW,
                                     self.dU, self.dV, self.ws, self.wsb)
@@ -219,17 +221,19 @@ class MlpPair(Linear):
         pf, T, r, dt = self.pf, self.wl.T, self.wl.r, "bf16"
         if name == "fwd1":
             pf.pf_linear_fwd(self.L1, dt, T, r, self.X, self.W1, self.U1, self.V1, self.H, self.T1,
-                             pf.PF_EPI_GELU, self.Hpre)
+                             pf.PF_EPI_GELU, self.Hpre, self.ws, self.wsb)
         elif name == "fwd2":
-            pf.pf_linear_fwd(self.L2, dt, T, r, self.H, self.W2, self.U2, self.V2, self.Y, self.T2)
+            pf.pf_linear_fwd(self.L2, dt, T, r, self.H, self.W2, self.U2, self.V2, self.Y, self.T2,
+                             workspace=self.ws, ws_bytes=self.wsb)
         elif name == "bwd_data2":
             pf.pf_linear_bwd_data(self.L2, dt, T, r, self.dY, self.W2, self.U2, self.V2, self.S2,
-                                  self.dHpre, pf.PF_EPI_GELU, self.Hpre)
+                                  self.dHpre, pf.PF_EPI_GELU, self.Hpre, self.ws, self.wsb)
         elif name == "bwd_weight2":
             pf.pf_linear_bwd_weight(self.L2, dt, T, r, self.dY, self.H, self.T2, self.S2, self.dW2,
                                     self.dU2, self.dV2, self.ws, self.wsb)
         elif name == "bwd_data1":
-            pf.pf_linear_bwd_data(self.L1, dt, T, r, self.dHpre, self.W1, self.U1, self.V1, self.S1, self.dX)
+            pf.pf_linear_bwd_data(self.L1, dt, T, r, self.dHpre, self.W1, self.U1, self.V1, self.S1,
+                                  self.dX, workspace=self.ws, ws_bytes=self.wsb)
         else:
             pf.pf_linear_bwd_weight(self.L1, dt, T, r, self.dHpre, self.X, self.T1, self.S1, self.dW1,
                                     self.dU1, self.dV1, self.ws, self.wsb)
@@ -426,6 +430,10 @@ def main():
     R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention}[wl.kind](torch, pf, wl)
 
     calls = [c for c in args.calls_only.split(",") if c] or R.calls
+    if "dense" in calls:  # profiling aid: the dense comparator step as one call
+        R.dense_setup()
+        base_call = R.call
+        R.call = lambda c: R.dense_step() if c == "dense" else base_call(c)
     # warmup, then the timed region with events between calls
     for _ in range(args.warmup):
         for c in calls:

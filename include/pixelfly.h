@@ -24,12 +24,12 @@
  *     never allocate, never synchronise and return as soon as the kernels
  *     are enqueued on `stream`.
  *   - Calls that take a workspace need at least pf_workspace_bytes(...)
- *     bytes of device memory, 256-byte aligned, whose contents on entry do
- *     not matter.
- *   - Split-token reductions (pf_linear_bwd_weight, pf_dense_gemm with
- *     PF_OP_TN) use a static per-GPU array of completion counters inside
- *     the library (zero at load, left zero by every call); such calls must
- *     not run concurrently on different streams of one GPU.
+ *     bytes of device memory (16-byte aligned) whose contents on entry do
+ *     not matter; the library uses it for fp32 partial sums when it splits a
+ *     reduction over several workgroups.  Partials are summed in a fixed
+ *     order, so results are deterministic.  A workspace must not be shared
+ *     by calls that may run concurrently.  With a size of 0 the pointer may
+ *     be NULL.
  *   - No C++ exception crosses this ABI.  Kernel launch failures map to
  *     PF_ERR_HIP.
  */
@@ -141,8 +141,9 @@ pf_status pf_layout_upload(pf_layout *layout, void *stream);
  * must make sure no enqueued work still uses it. */
 void pf_layout_destroy(pf_layout *layout);
 
-/* Workspace bytes needed by pf_linear_bwd_weight for T tokens and rank r
- * (0 when none is needed).  Returns 0 on invalid arguments. */
+/* Workspace bytes needed by pf_linear_fwd, pf_linear_bwd_data and
+ * pf_linear_bwd_weight (the largest of the three) for T tokens and rank r;
+ * 0 when none is needed or on invalid arguments. */
 size_t pf_workspace_bytes(const pf_layout *layout, int64_t T, int32_t r,
                           pf_dtype dtype);
 
@@ -157,12 +158,13 @@ size_t pf_workspace_bytes(const pf_layout *layout, int64_t T, int32_t r,
  * epi = PF_EPI_GELU writes Y_pre (T x N) = the pre-activation and
  * Y = gelu(Y_pre); with PF_EPI_NONE Y_pre must be NULL.
  * Tokens T >= 1 is arbitrary (ragged last tile handled).
- * Errors: INVALID_ARG, UNSUPPORTED, STATE, HIP.
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, WORKSPACE, HIP.
  */
 pf_status pf_linear_fwd(const pf_layout *layout, pf_dtype dtype, int64_t T,
                         int32_t r, const void *X, const void *Wblk,
                         const void *U, const void *V, void *Y, void *T_lr,
-                        pf_epilogue epi, void *Y_pre, void *stream);
+                        pf_epilogue epi, void *Y_pre, void *workspace,
+                        size_t ws_bytes, void *stream);
 
 /*
  * Backward-data (gradient of the layer w.r.t. its input):
@@ -170,13 +172,14 @@ pf_status pf_linear_fwd(const pf_layout *layout, pf_dtype dtype, int64_t T,
  *     dX = dY (M o W) + S V             (T x K)
  * dY: T x N.  With epi = PF_EPI_GELU, aux is a T x K tensor (the previous
  * layer's Y_pre) and dX = (dY (M o W) + S V) * gelu'(aux).
- * Errors: INVALID_ARG, UNSUPPORTED, STATE, HIP.
+ * Errors: INVALID_ARG, UNSUPPORTED, STATE, WORKSPACE, HIP.
  */
 pf_status pf_linear_bwd_data(const pf_layout *layout, pf_dtype dtype,
                              int64_t T, int32_t r, const void *dY,
                              const void *Wblk, const void *U, const void *V,
                              void *S, void *dX, pf_epilogue epi,
-                             const void *aux, void *stream);
+                             const void *aux, void *workspace,
+                             size_t ws_bytes, void *stream);
 
 /*
  * Backward-weight, restricted to the mask (gradient Lemma and sparse
@@ -184,8 +187,7 @@ pf_status pf_linear_bwd_data(const pf_layout *layout, pf_dtype dtype,
  *     dW = (dY^T X) o M   stored packed like Wblk: only kept blocks
  *     dU = dY^T T_lr      (N x r)
  *     dV = S^T X          (r x K)
- * Reductions run over the T tokens; split-token partial sums are combined
- * in a fixed order, so results are deterministic.
+ * Reductions run over the T tokens.
  * Errors: INVALID_ARG, UNSUPPORTED, STATE, WORKSPACE, HIP.
  */
 pf_status pf_linear_bwd_weight(const pf_layout *layout, pf_dtype dtype,

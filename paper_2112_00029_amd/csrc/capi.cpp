@@ -69,18 +69,51 @@ int pow2_group(int gmax, int n) {
   return g;
 }
 
-// Dense-mode NT launch: C[T x nblk*b] = A[T x nsteps*b] . B^T (B [n][k]) or
-// A . B (B [k][n]).
-pf_status dense_nt(int dtype, int blk, bool b_kn, int64_t M, const void *A, int64_t lda,
+// Dense-mode NT launch: C[M x nblk*b] = A[M x nsteps*b] . B^T (B [n][k]) or
+// A . B (B [k][n]), with M-tile bm; split over K when ws gives room.
+pf_status dense_nt(int dtype, int blk, bool b_kn, int bm, int64_t M, const void *A, int64_t lda,
                    const void *B, int64_t ldb, int nsteps, int nblk, void *C, int64_t ldc,
-                   hipStream_t s, const char *what) {
+                   int nsplit, float *ws, hipStream_t s, const char *what) {
   pf::NTArgs a{};
   a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
   a.dense = 1; a.dense_nsteps = nsteps; a.dense_nblk = nblk;
   a.C = C; a.ldc = ldc; a.M = M;
-  int G = pow2_group(pf::max_group(blk), nblk);
+  const int G = 128 / blk;  // dense tiles are 128 columns wide
   a.ntiles = (nblk + G - 1) / G;
-  return hip_status(pf::launch_nt(dtype, blk, G, b_kn, a, s), what);
+  a.nsplit = nsplit;
+  a.partials = ws;
+  a.ldp = (int64_t)nblk * blk;
+  pf_status st = hip_status(pf::launch_nt(dtype, blk, G, b_kn, bm, a, s), what);
+  if (st != PF_OK || nsplit <= 1) return st;
+  return hip_status(pf::launch_reduce_rows(dtype, nsplit, ws, M, (int64_t)nblk * blk, C, ldc, s), what);
+}
+
+// Workgroups a launch aims for (2 per CU on 256 CUs) before splitting K.
+#ifndef PF_WG_TARGET
+#define PF_WG_TARGET 512
+#endif
+#ifndef PF_MAX_SPLIT
+#define PF_MAX_SPLIT 4
+#endif
+
+// Split of the skinny rank-r product (M = T tokens, K = kblocks * b,
+// r / b output blocks, M-tile 64, 128-column tiles, K-steps of 64 or 32).
+struct SkinnyPlan {
+  int nsplit;
+  size_t ws;
+};
+SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
+  SkinnyPlan p{1, 0};
+  if (r <= 0) return p;
+  const int64_t mtiles = (T + 63) / 64, ntiles = (r + 127) / 128;
+  const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
+  int64_t want = (PF_WG_TARGET + mtiles * ntiles - 1) / (mtiles * ntiles);
+  int64_t ns = std::min<int64_t>({want, PF_MAX_SPLIT, std::max<int64_t>(1, steps / 4)});
+  if (ns > 1) {
+    p.nsplit = (int)ns;
+    p.ws = (size_t)ns * T * r * sizeof(float);
+  }
+  return p;
 }
 
 // Split-token plan of the TN kernel.
@@ -90,15 +123,17 @@ struct TNPlan {
   size_t ws;
 };
 
-TNPlan tn_plan(int items, int64_t T) {
-  TNPlan p{1, ((T + 31) / 32) * 32, 0};
-  const int target = 2 * 256;
-  if (items < target && items <= pf::kMaxCounters) {
-    int64_t want = (target + items - 1) / items;
+// row_bytes: the largest operand row stride in bytes; one split's token
+// range must stay below 2^31 bytes of rows (32-bit buffer offsets).
+TNPlan tn_plan(int items, int64_t T, int64_t row_bytes) {
+  TNPlan p{1, ((T + 63) / 64) * 64, 0};
+  const int64_t min_split = (T * row_bytes + 0x7fffffffLL - 1) / 0x7fffffffLL;
+  if (items < PF_WG_TARGET || min_split > 1) {
+    int64_t want = (PF_WG_TARGET + items - 1) / items;
     int64_t maxs = std::max<int64_t>(1, T / 256);
-    int64_t ns = std::min<int64_t>(want, maxs);
+    int64_t ns = std::max(min_split, std::min<int64_t>({want, maxs, PF_MAX_SPLIT}));
     if (ns > 1) {
-      int64_t chunk = ((T + ns - 1) / ns + 31) / 32 * 32;
+      int64_t chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
       ns = (T + chunk - 1) / chunk;
       if (ns > 1) {
         p.nsplit = (int)ns;
@@ -307,12 +342,25 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
   pf::TNArgs a{};
   a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
-  return tn_plan(pf::tn_items_total(a, L->b), T).ws;
+  const int64_t es = dtype == PF_BF16 ? 2 : 4;
+  const size_t tn = tn_plan(pf::tn_items_total(a, L->b), T, std::max(L->n_out, L->n_in) * es).ws;
+  const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
+  const size_t bwd = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
+  return std::max({tn, fwd, bwd});
+}
+
+// Checks a caller workspace against a need of `need` bytes.
+static pf_status need_ws(size_t need, const void *ws, size_t ws_bytes) {
+  if (need == 0) return PF_OK;
+  if (ws_bytes < need)
+    return fail(PF_ERR_WORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
+  return need_ptr(ws, "workspace");
 }
 
 pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *X,
                         const void *Wblk, const void *U, const void *V, void *Y, void *T_lr,
-                        pf_epilogue epi, void *Y_pre, void *stream) {
+                        pf_epilogue epi, void *Y_pre, void *workspace, size_t ws_bytes,
+                        void *stream) {
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
@@ -325,12 +373,15 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   if (epi != PF_EPI_NONE && epi != PF_EPI_GELU) return fail(PF_ERR_INVALID_ARG, "bad epilogue");
   if (epi == PF_EPI_GELU && (st = need_ptr(Y_pre, "Y_pre")) != PF_OK) return st;
   if (epi == PF_EPI_NONE && Y_pre) return fail(PF_ERR_INVALID_ARG, "Y_pre given without GELU epilogue");
+  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_in, r);
+  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(dt, b, false, T, X, L->n_in, V, L->n_in, L->nb_in, r / b, T_lr, r, s, "T_lr kernel");
+    st = dense_nt(dt, b, false, 64, T, X, L->n_in, V, L->n_in, L->nb_in, r / b, T_lr, r, sp.nsplit,
+                  (float *)workspace, s, "T_lr kernel");
     if (st != PF_OK) return st;
   }
   pf::NTArgs a{};
@@ -343,12 +394,14 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   a.M = T;
   a.tiles = L->d_fwd_tiles; a.ntiles = (int)L->fwd_tiles.size();
   a.kcols = L->d_kcols_fwd; a.blks = L->d_blks_fwd;
-  return hip_status(pf::launch_nt(dt, b, L->G_fwd, false, a, s), "forward kernel");
+  a.nsplit = 1;
+  return hip_status(pf::launch_nt(dt, b, L->G_fwd, false, 128, a, s), "forward kernel");
 }
 
 pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
                              const void *dY, const void *Wblk, const void *U, const void *V,
-                             void *S, void *dX, pf_epilogue epi, const void *aux, void *stream) {
+                             void *S, void *dX, pf_epilogue epi, const void *aux,
+                             void *workspace, size_t ws_bytes, void *stream) {
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
@@ -360,12 +413,15 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
     return st;
   if (epi != PF_EPI_NONE && epi != PF_EPI_GELU) return fail(PF_ERR_INVALID_ARG, "bad epilogue");
   if (epi == PF_EPI_GELU && (st = need_ptr(aux, "aux")) != PF_OK) return st;
+  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
+  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // S = dY U: dense over N with U read as [k][n].
-    st = dense_nt(dt, b, true, T, dY, L->n_out, U, r, L->nb_out, r / b, S, r, s, "S kernel");
+    st = dense_nt(dt, b, true, 64, T, dY, L->n_out, U, r, L->nb_out, r / b, S, r, sp.nsplit,
+                  (float *)workspace, s, "S kernel");
     if (st != PF_OK) return st;
   }
   pf::NTArgs a{};
@@ -378,7 +434,8 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.M = T;
   a.tiles = L->d_bwd_tiles; a.ntiles = (int)L->bwd_tiles.size();
   a.kcols = L->d_kcols_bwd; a.blks = L->d_blks_bwd;
-  return hip_status(pf::launch_nt(dt, b, L->G_bwd, true, a, s), "backward-data kernel");
+  a.nsplit = 1;
+  return hip_status(pf::launch_nt(dt, b, L->G_bwd, true, 128, a, s), "backward-data kernel");
 }
 
 pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -402,12 +459,9 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
   a.T = T;
-  TNPlan p = tn_plan(pf::tn_items_total(a, L->b), T);
-  if (p.ws > 0) {
-    if (ws_bytes < p.ws)
-      return fail(PF_ERR_WORKSPACE, "workspace needs " + std::to_string(p.ws) + " bytes");
-    if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
-  }
+  TNPlan p = tn_plan(pf::tn_items_total(a, L->b), T,
+                     std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
+  if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
   a.nsplit = p.nsplit;
   a.chunk = p.chunk;
   a.partials = (float *)workspace;
@@ -490,7 +544,7 @@ size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_
   if (dtype != PF_BF16 && dtype != PF_FP32) return 0;
   if (op != PF_OP_TN || M < 64 || N < 64 || K < 1 || M % 64 || N % 64) return 0;
   int items = (int)(((M / 64 + 1) / 2) * ((N / 64 + 1) / 2));
-  return tn_plan(items, K).ws;
+  return tn_plan(items, K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4)).ws;
 }
 
 pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K,
@@ -510,21 +564,19 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
   const int dt = (int)dtype;
   switch (op) {
     case PF_OP_NT:
-      return dense_nt(dt, 64, false, M, A, K, B, K, (int)(K / 64), (int)(N / 64), C, N, s, "dense NT");
+      return dense_nt(dt, 64, false, 128, M, A, K, B, K, (int)(K / 64), (int)(N / 64), C, N, 1,
+                      nullptr, s, "dense NT");
     case PF_OP_NN:
-      return dense_nt(dt, 64, true, M, A, K, B, N, (int)(K / 64), (int)(N / 64), C, N, s, "dense NN");
+      return dense_nt(dt, 64, true, 128, M, A, K, B, N, (int)(K / 64), (int)(N / 64), C, N, 1,
+                      nullptr, s, "dense NN");
     case PF_OP_TN: {
       pf::TNArgs a{};
       a.n_items = 0;
       a.dr[0] = pf::TNDense{A, M, B, N, C, N, (int)(M / 64), (int)(N / 64)};
       a.n_dense = 1;
       a.T = K;
-      TNPlan p = tn_plan(pf::tn_items_total(a, 64), K);
-      if (p.ws > 0) {
-        if (ws_bytes < p.ws)
-          return fail(PF_ERR_WORKSPACE, "workspace needs " + std::to_string(p.ws) + " bytes");
-        if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
-      }
+      TNPlan p = tn_plan(pf::tn_items_total(a, 64), K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4));
+      if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
       a.nsplit = p.nsplit;
       a.chunk = p.chunk;
       a.partials = (float *)workspace;

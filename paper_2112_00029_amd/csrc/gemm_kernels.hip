@@ -8,19 +8,23 @@
 //             Backward-data:  A = dY, B = packed W blocks read as [k][n]
 //                             (the transposed layout), low-rank S . V.
 //             Dense mode (comparator and the skinny rank-r products): the
-//             K-steps run over every block of a dense B.
+//             K-steps run over every block of a dense B; the K range may be
+//             split over workgroups that write fp32 partial outputs, summed
+//             in split order by reduce_rows_kernel (deterministic).
 //  tn_kernel  out = A^T . B reduced over tokens, only for kept blocks
 //             (weight gradient restricted to the mask) plus dense regions
-//             (dU = dY^T T_lr, dV = S^T X).  Token range may be split across
-//             workgroups; partials are combined in split order by the last
-//             workgroup to finish an item (deterministic).
+//             (dU = dY^T T_lr, dV = S^T X).  The token range may be split
+//             over workgroups; tn_reduce_kernel sums the partials in split
+//             order (deterministic).
 //
-// Tiles: 256 threads = 4 waves of 64.  Operands stream global -> registers
-// -> LDS (double-buffered, one barrier per K-step of 32).  MFMA fragments
-// are read from LDS with 16-byte reads ([row][k] tiles) or with the gfx950
-// transpose read ds_read_b64_tr_b16 ([k][row] tiles): within each group of
-// 16 lanes, lanes 4m..4m+3 address row m (4 x 16-bit each) of a 4 x 16
-// tile and lane j receives column j, i.e. 4 consecutive k of one row.
+// Mainloop: 256 threads = 4 waves of 64.  The K dimension advances in steps
+// of 64 (bf16) / 32 (fp32).  Operands stream global -> registers -> LDS with
+// two register stages (the loads of step s+2 are issued before step s is
+// computed) and a double-buffered LDS tile, one barrier per step.  MFMA
+// fragments are read from LDS with 16-byte reads ([row][k] tiles) or with
+// the gfx950 transpose read ds_read_b64_tr_b16 ([k][row] tiles): within each
+// group of 16 lanes, lanes 4m..4m+3 address row m (4 x 16-bit each) of a
+// 4 x 16 tile and lane j receives column j, i.e. 4 consecutive k of one row.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -35,11 +39,9 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_t;  // bfloat16 storage
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));  // 16-byte chunk
-
-__device__ unsigned int g_tn_counters[kMaxCounters];
 
 __device__ __forceinline__ float bf2f(bf16_t h) {
   return __uint_as_float(((uint32_t)h) << 16);
@@ -84,7 +86,7 @@ __device__ __forceinline__ bf16x8 cat8(s16x4 lo, s16x4 hi) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// MFMA fragment of a 32-row operand stored [k][row] in LDS (row
+// MFMA (32x32x16) fragment of a 32-row operand stored [k][row] in LDS (row
 // contiguous): lane l gets row (l % 32), k = ks*16 + (l / 32)*8 + 0..7.
 __device__ __forceinline__ bf16x8 frag_kmajor(const bf16_t *base, int ld,
                                               int ks, int row0, int lane) {
@@ -94,7 +96,7 @@ __device__ __forceinline__ bf16x8 frag_kmajor(const bf16_t *base, int ld,
   return cat8(tr16(p), tr16(p + 4 * ld));
 }
 
-// MFMA fragment of a 32-row operand stored [row][k] in LDS.
+// MFMA (32x32x16) fragment of a 32-row operand stored [row][k] in LDS.
 __device__ __forceinline__ bf16x8 frag_rmajor(const bf16_t *base, int ld,
                                               int ks, int row0, int lane) {
   return *(const bf16x8 *)(base + (row0 + (lane & 31)) * ld + ks * 16 +
@@ -115,8 +117,6 @@ __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl<0, N>(f);
 }
 
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
-
 // Up to 8 staged 16-byte chunks in named registers (struct fields, unlike
 // array elements, cannot be addressed with a run-time index, so they always
 // stay in VGPRs).
@@ -136,30 +136,82 @@ struct Stage8 {
   }
 };
 
+// Double-buffered pipeline driver: load(s, ra, rb) issues the global loads
+// of step s into a register stage, store(ra, rb, buf) writes a register stage
+// to LDS buffer buf, compute(buf) runs the MFMAs of the step held in buf.
+// Register stage 0 carries even steps, stage 1 odd steps; step s lives in
+// LDS buffer s % 2.  The loads of step s+2 are in flight while step s is
+// computed.
+template <typename Load, typename Store, typename Compute>
+__device__ __forceinline__ void pipeline(int total, Stage8 &ra0, Stage8 &rb0, Stage8 &ra1,
+                                         Stage8 &rb1, Load &&load, Store &&store,
+                                         Compute &&compute) {
+  if (total <= 0) return;
+  load(0, ra0, rb0);
+  if (total > 1) load(1, ra1, rb1);
+  store(ra0, rb0, 0);
+  __syncthreads();
+  for (int s = 0; s < total; s += 2) {
+    if (s + 2 < total) load(s + 2, ra0, rb0);
+    compute(0);
+    if (s + 1 < total) store(ra1, rb1, 1);
+    __syncthreads();
+    if (s + 1 < total) {
+      if (s + 3 < total) load(s + 3, ra1, rb1);
+      compute(1);
+      if (s + 2 < total) store(ra0, rb0, 0);
+      __syncthreads();
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Buffer-resource loads: raw buffer loads return zeros outside [0, bytes),
+// which covers ragged token tiles and the zero padding of the K range
+// without per-lane branches.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t make_rsrc(const void *p, int64_t bytes) {
+  const int64_t b = bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)b, 0x00020000);
+}
+__device__ __forceinline__ u32x4 bload(rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // NT kernel
 // ---------------------------------------------------------------------------
-template <typename T, int BLK, int G, bool BKN>
-__global__ __launch_bounds__(256) void nt_kernel(NTArgs a) {
+// EPI: 0 plain store, 1 forward GELU (also store the pre-activation),
+// 2 backward GELU (scale by gelu' of the pre-activation a.aux).
+template <typename T, int BLK, int G, bool BKN, int BM, bool DENSE, int EPI>
+__global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
+  const NTArgs a = a_arg;  // local copy: lambdas below capture it by reference
   constexpr bool BF = std::is_same<T, bf16_t>::value;
-  constexpr int BM = 128, BK = 32, BN = G * BLK;
-  constexpr int KSUB = BLK / BK;
-  constexpr int VEC = 16 / (int)sizeof(T);
+  constexpr int ES = (int)sizeof(T);
+  constexpr int BK = BF ? 64 : 32;           // K per pipeline step
+  constexpr int BN = G * BLK;
+  constexpr int VEC = 16 / ES;               // elements per 16-byte chunk
+  constexpr int KW = BK < BLK ? BK : BLK;    // K width of one sub-block
+  constexpr int NH = BK / KW;                // sub-blocks per step (2: bf16, b = 32)
   constexpr int PADA = BF ? 8 : 4;
   constexpr int LDA_S = BK + PADA;
   constexpr int LDB_S = BKN ? (BN + (BF ? 16 : 4)) : (BK + PADA);
   constexpr int A_ELEMS = BM * LDA_S;
   constexpr int B_ELEMS = BKN ? BK * LDB_S : BN * LDB_S;
-  constexpr int WN = BN >= 64 ? 2 : 1, WM = 4 / WN;
-  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int WNN = BN == 32 ? 1 : 2;      // waves along N
+  constexpr int WMM = 4 / WNN;               // waves along M
+  constexpr int WTM = BM / WMM, WTN = BN / WNN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int A_CH = BM * BK / VEC;
-  constexpr int CPB = BLK * BK / VEC;  // 16-byte chunks of one block's K-slice
-  constexpr int B_CH = G * CPB;
-  constexpr int A_LD = A_CH / 256, B_LD = (B_CH + 255) / 256;
-  static_assert(A_CH % 256 == 0, "A tile chunks");
-  static_assert(CPB % 64 == 0, "a wave's chunks must lie in one block");
-  static_assert(TM >= 1 && TN >= 1, "wave tile");
+  // A tile: NH sub-blocks of BM rows x KW columns; B tile: G x NH pieces
+  // (tile row g, sub-block h) of BLK x KW.
+  constexpr int A_CPR = KW / VEC, A_CPH = BM * A_CPR, A_IPH = A_CPH / 256;
+  constexpr int A_LD = NH * A_IPH;
+  constexpr int B_CPP = BLK * KW / VEC;
+  constexpr int B_LD = G * NH * B_CPP / 256;
+  static_assert(A_CPH % 256 == 0 && B_CPP % 64 == 0 && (G * NH * B_CPP) % 256 == 0, "chunking");
+  static_assert(A_LD <= 8 && B_LD <= 8, "staging registers");
+  static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
 
   __shared__ __attribute__((aligned(16))) T smem[2 * (A_ELEMS + B_ELEMS)];
 
@@ -169,16 +221,26 @@ __global__ __launch_bounds__(256) void nt_kernel(NTArgs a) {
   const T *__restrict__ R = (const T *)a.R;
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = uniform(tid >> 6);
-  const int wm = wave / WN, wn = wave % WN;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WNN, wn = wave % WNN;
   const int ntn = a.ntiles;
+  const int mtiles = (int)((a.M + BM - 1) / BM);
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int mt = bid / ntn, nt = bid % ntn;
+  // Grouped order: consecutive ids (the workgroups resident on one XCD)
+  // cover GM m-tiles x a run of n-tiles, so both the token rows and the
+  // weight blocks they read are re-used from that XCD's L2.
+  constexpr int GM = 8;
+  const int split = bid / (mtiles * ntn);
+  const int lin = bid % (mtiles * ntn);
+  const int first_m = (lin / (GM * ntn)) * GM;
+  const int gsz = min(GM, mtiles - first_m);
+  const int within = lin - first_m * ntn;
+  const int mt = first_m + within % gsz, nt = within / gsz;
   const int64_t m0 = (int64_t)mt * BM;
 
   int g_valid, nsteps, kcol_off = 0, blk_off = 0;
-  const NTTile *tile = a.dense ? nullptr : a.tiles + nt;
-  if (a.dense) {
+  const NTTile *tile = DENSE ? nullptr : a.tiles + nt;
+  if constexpr (DENSE) {
     g_valid = min(G, a.dense_nblk - nt * G);
     nsteps = a.dense_nsteps;
   } else {
@@ -187,89 +249,119 @@ __global__ __launch_bounds__(256) void nt_kernel(NTArgs a) {
     kcol_off = tile->kcol_off;
     blk_off = tile->blk_off;
   }
-  // Output block of tile row g (g wave-uniform).
   auto out_blk = [&](int g) __attribute__((always_inline)) -> int {
-    return a.dense ? nt * G + min(g, g_valid - 1) : tile->out_blk[g];
+    if constexpr (DENSE) return nt * G + min(g, g_valid - 1);
+    else return tile->out_blk[g];
   };
-  const int total = (nsteps + a.nlr) * KSUB;
+  // Virtual K: the kept blocks, then the low-rank blocks, then zero padding.
+  const int vblocks = nsteps + a.nlr;
+  const int total_all = (vblocks * BLK + BK - 1) / BK;
+  const int per_split = (total_all + a.nsplit - 1) / a.nsplit;
+  const int s_begin = split * per_split;
+  const int total = max(0, min(total_all, s_begin + per_split) - s_begin);
 
-  // Base pointer of the B operand slice of step s for tile row g.
-  auto b_base = [&](int s, int g, int64_t &ldb_s) __attribute__((always_inline)) -> const T * {
-    const int c = s / KSUB, kk = (s % KSUB) * BK;
+  // Operand sources as (base, byte range); buffer resources are built at
+  // the point of use.  A byte range of 0 yields zeros (K padding).
+  const T *const a_base = A + m0 * a.lda;
+  const int64_t a_bytes = (a.M - m0) * a.lda * ES;
+  const T *const l_base = DENSE ? A : L + m0 * a.ldl;
+  const int64_t l_bytes = DENSE ? 0 : (a.M - m0) * a.ldl * ES;
+  constexpr int64_t BIG = 0x7fffffff;
+
+  // Sub-block h of step s (all arguments wave-uniform): A base, byte range,
+  // row stride and column offset in bytes.
+  auto a_src = [&](int s, int h, const T *&base, int64_t &bytes, uint32_t &ldb,
+                   uint32_t &colb) __attribute__((always_inline)) {
+    const int k0 = (s_begin + s) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
     if (c < nsteps) {
-      if (a.dense) {
-        ldb_s = a.ldb;
+      const int kcol = DENSE ? c : a.kcols[kcol_off + c];
+      base = a_base;
+      bytes = a_bytes;
+      ldb = (uint32_t)(a.lda * ES);
+      colb = (uint32_t)((kcol * BLK + kk) * ES);
+    } else {
+      base = l_base;
+      bytes = c < vblocks ? l_bytes : 0;
+      ldb = (uint32_t)(a.ldl * ES);
+      colb = (uint32_t)(((c - nsteps) * BLK + kk) * ES);
+    }
+  };
+  // Piece (g, h) of step s: B base at the piece, byte range, row stride.
+  auto b_src = [&](int s, int g, int h, const T *&base, int64_t &bytes,
+                   uint32_t &ldb) __attribute__((always_inline)) {
+    const int k0 = (s_begin + s) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
+    bytes = BIG;
+    if (c < nsteps) {
+      if constexpr (DENSE) {
+        ldb = (uint32_t)(a.ldb * ES);
         const int64_t ob = out_blk(g);
-        return BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
+        base = BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
                    : B + (ob * BLK) * a.ldb + (int64_t)c * BLK + kk;
+      } else {
+        ldb = BLK * ES;
+        const int64_t blk = a.blks[blk_off + c * G + g];
+        base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
       }
-      ldb_s = BLK;
-      const int64_t blk = a.blks[blk_off + c * G + g];
-      return B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
+      return;
+    }
+    ldb = (uint32_t)(a.ldr * ES);
+    if (c >= vblocks) {
+      base = B;
+      bytes = 0;
+      return;
     }
     const int cr = c - nsteps;
     const int64_t ob = out_blk(g);
-    ldb_s = a.ldr;
-    return BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
+    base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
                : R + (ob * BLK) * a.ldr + (int64_t)cr * BLK + kk;
   };
-  auto a_base = [&](int s, int64_t &lda_s) __attribute__((always_inline)) -> const T * {
-    const int c = s / KSUB, kk = (s % KSUB) * BK;
-    if (c < nsteps) {
-      const int kcol = a.dense ? c : a.kcols[kcol_off + c];
-      lda_s = a.lda;
-      return A + (int64_t)kcol * BLK + kk;
-    }
-    lda_s = a.ldl;
-    return L + (int64_t)(c - nsteps) * BLK + kk;
-  };
 
-  static_assert(A_LD <= 8 && B_LD <= 8, "staging registers");
-  Stage8 ra, rb;
-  auto gload = [&](int s) __attribute__((always_inline)) {
-    int64_t lda_s;
-    const T *ap = a_base(s, lda_s);
-    static_for<A_LD>([&](auto i) __attribute__((always_inline)) {
-      const int id = tid + i * 256;
-      const int row = id / (BK / VEC), cv = id % (BK / VEC);
-      const int64_t gm = m0 + row;
-      ra.template at<i>() = gm < a.M ? *(const u32x4 *)(ap + gm * lda_s + cv * VEC) : u32x4{0u, 0u, 0u, 0u};
+  auto load = [&](int s, Stage8 &ra, Stage8 &rb) __attribute__((always_inline)) {
+    static_for<NH>([&](auto h) __attribute__((always_inline)) {
+      const T *base;
+      int64_t bytes;
+      uint32_t ldb, colb;
+      a_src(s, h, base, bytes, ldb, colb);
+      const rsrc_t r = make_rsrc(base, bytes);
+      static_for<A_IPH>([&](auto j) __attribute__((always_inline)) {
+        const int id = tid + j * 256;
+        const uint32_t off = (uint32_t)(id / A_CPR) * ldb + colb + (uint32_t)(id % A_CPR) * 16;
+        ra.template at<h * A_IPH + j>() = bload(r, off);
+      });
     });
     static_for<B_LD>([&](auto i) __attribute__((always_inline)) {
       const int id = tid + i * 256;
-      if (i * 256 + 256 <= B_CH || id < B_CH) {
-        const int g = uniform(id / CPB), r = id % CPB;
-        int64_t ldb_s;
-        const T *bp = b_base(s, g, ldb_s);
-        if (!BKN) {
-          const int n = r / (BK / VEC), cv = r % (BK / VEC);
-          rb.template at<i>() = *(const u32x4 *)(bp + (int64_t)n * ldb_s + cv * VEC);
-        } else {
-          const int k = r / (BLK / VEC), nv = r % (BLK / VEC);
-          rb.template at<i>() = *(const u32x4 *)(bp + (int64_t)k * ldb_s + nv * VEC);
-        }
-      }
+      const int piece = B_CPP % 256 == 0 ? (i * 256) / B_CPP
+                                         : __builtin_amdgcn_readfirstlane(id / B_CPP);
+      const int rr = id % B_CPP;
+      const T *base;
+      int64_t bytes;
+      uint32_t ldb;
+      b_src(s, piece / NH, piece % NH, base, bytes, ldb);
+      const rsrc_t r = make_rsrc(base, bytes);
+      uint32_t off;
+      if constexpr (!BKN) off = (uint32_t)(rr / (KW / VEC)) * ldb + (uint32_t)(rr % (KW / VEC)) * 16;
+      else off = (uint32_t)(rr / (BLK / VEC)) * ldb + (uint32_t)(rr % (BLK / VEC)) * 16;
+      rb.template at<i>() = bload(r, off);
     });
   };
-  auto sstore = [&](int buf) __attribute__((always_inline)) {
+  auto store = [&](Stage8 &ra, Stage8 &rb, int buf) __attribute__((always_inline)) {
     T *As = smem + buf * (A_ELEMS + B_ELEMS);
     T *Bs = As + A_ELEMS;
     static_for<A_LD>([&](auto i) __attribute__((always_inline)) {
-      const int id = tid + i * 256;
-      const int row = id / (BK / VEC), cv = id % (BK / VEC);
-      *(u32x4 *)(As + row * LDA_S + cv * VEC) = ra.template at<i>();
+      constexpr int h = i / A_IPH;
+      const int id = tid + (i % A_IPH) * 256;
+      *(u32x4 *)(As + (id / A_CPR) * LDA_S + h * KW + (id % A_CPR) * VEC) = ra.template at<i>();
     });
     static_for<B_LD>([&](auto i) __attribute__((always_inline)) {
       const int id = tid + i * 256;
-      if (i * 256 + 256 <= B_CH || id < B_CH) {
-        const int g = id / CPB, r = id % CPB;
-        if (!BKN) {
-          const int n = r / (BK / VEC), cv = r % (BK / VEC);
-          *(u32x4 *)(Bs + (g * BLK + n) * LDB_S + cv * VEC) = rb.template at<i>();
-        } else {
-          const int k = r / (BLK / VEC), nv = r % (BLK / VEC);
-          *(u32x4 *)(Bs + k * LDB_S + g * BLK + nv * VEC) = rb.template at<i>();
-        }
+      const int piece = id / B_CPP, g = piece / NH, h = piece % NH, rr = id % B_CPP;
+      if constexpr (!BKN) {
+        *(u32x4 *)(Bs + (g * BLK + rr / (KW / VEC)) * LDB_S + h * KW + (rr % (KW / VEC)) * VEC) =
+            rb.template at<i>();
+      } else {
+        *(u32x4 *)(Bs + (h * KW + rr / (BLK / VEC)) * LDB_S + g * BLK + (rr % (BLK / VEC)) * VEC) =
+            rb.template at<i>();
       }
     });
   };
@@ -282,149 +374,252 @@ __global__ __launch_bounds__(256) void nt_kernel(NTArgs a) {
     });
   });
 
-  if (total > 0) {
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    for (int s = 0; s < total; ++s) {
-      const int cur = s & 1;
-      if (s + 1 < total) gload(s + 1);
-      const T *As = smem + cur * (A_ELEMS + B_ELEMS);
-      const T *Bs = As + A_ELEMS;
-      if constexpr (BF) {
-        static_for<BK / 16>([&](auto ks) __attribute__((always_inline)) {
-          bf16x8 af[TM], bfg[TN];
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            af[tm] = frag_rmajor((const bf16_t *)As, LDA_S, ks, wm * WTM + tm * 32, lane);
-          });
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const T *As = smem + buf * (A_ELEMS + B_ELEMS);
+    const T *Bs = As + A_ELEMS;
+    if constexpr (BF) {
+      static_for<BK / 16>([&](auto ks) __attribute__((always_inline)) {
+        bf16x8 af[TM], bfg[TN];
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+          af[tm] = frag_rmajor((const bf16_t *)As, LDA_S, ks, wm * WTM + tm * 32, lane);
+        });
+        static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+          bfg[tn] = BKN ? frag_kmajor((const bf16_t *)Bs, LDB_S, ks, wn * WTN + tn * 32, lane)
+                        : frag_rmajor((const bf16_t *)Bs, LDB_S, ks, wn * WTN + tn * 32, lane);
+        });
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-            bfg[tn] = BKN ? frag_kmajor((const bf16_t *)Bs, LDB_S, ks, wn * WTN + tn * 32, lane)
-                          : frag_rmajor((const bf16_t *)Bs, LDB_S, ks, wn * WTN + tn * 32, lane);
-          });
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
-            });
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
-      } else {
-        static_for<BK / 2>([&](auto ks) __attribute__((always_inline)) {
-          float af[TM], bfg[TN];
-          const int kq = ks * 2 + (lane >> 5);
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            af[tm] = As[(wm * WTM + tm * 32 + (lane & 31)) * LDA_S + kq];
-          });
+      });
+    } else {
+      static_for<BK / 2>([&](auto ks) __attribute__((always_inline)) {
+        float af[TM], bfg[TN];
+        const int kq = ks * 2 + (lane >> 5);
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+          af[tm] = As[(wm * WTM + tm * 32 + (lane & 31)) * LDA_S + kq];
+        });
+        static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+          const int n = wn * WTN + tn * 32 + (lane & 31);
+          bfg[tn] = BKN ? Bs[kq * LDB_S + n] : Bs[n * LDB_S + kq];
+        });
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-            const int n = wn * WTN + tn * 32 + (lane & 31);
-            bfg[tn] = BKN ? Bs[kq * LDB_S + n] : Bs[n * LDB_S + kq];
-          });
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
-            });
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
-      }
-      if (s + 1 < total) sstore(cur ^ 1);
-      __syncthreads();
-    }
-  }
-
-  // Epilogue: lane holds column (lane % 32) and rows (j/4)*8 + (lane/32)*4
-  // + j%4 of each 32 x 32 accumulator tile.
-  T *C = (T *)a.C;
-  static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-    const int g = (wn * WTN + tn * 32) / BLK;  // wave-uniform
-    if (g < g_valid) {
-      const int64_t col = (int64_t)out_blk(g) * BLK + ((wn * WTN + tn * 32) % BLK) + (lane & 31);
-      static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int64_t row = m0 + wm * WTM + tm * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-          if (row < a.M) {
-            float v = acc[tm][tn][j];
-            const int64_t o = row * a.ldc + col;
-            if (a.epi == 1) {
-              if (a.C2) {  // forward GELU: keep the pre-activation
-                ((T *)a.C2)[o] = from_f<T>(v);
-                v = gelu_f(v);
-              } else {     // backward GELU: scale by gelu'(pre-activation)
-                v *= gelu_grad_f(to_f<T>(((const T *)a.aux)[o]));
-              }
-            }
-            C[o] = from_f<T>(v);
-          }
-        }
       });
     }
+  };
+
+  Stage8 ra0, rb0, ra1, rb1;
+  pipeline(total, ra0, rb0, ra1, rb1, load, store, compute);
+
+  // Epilogue.  The accumulators (lane: column lane % 32, rows (j/4)*8 +
+  // (lane/32)*4 + j%4 of each 32 x 32 tile) go to an fp32 tile in LDS, then
+  // each thread writes 8 consecutive columns of one row (16-byte stores).
+  constexpr int CS = BN + 4;
+  static_assert(BM * CS * 4 <= (int)sizeof(smem), "epilogue tile");
+  float *Cs = (float *)smem;
+  __syncthreads();
+  static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+    static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+      const int col = wn * WTN + tn * 32 + (lane & 31);
+#pragma unroll
+      for (int j = 0; j < 16; ++j)
+        Cs[(wm * WTM + tm * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3)) * CS + col] = acc[tm][tn][j];
+    });
   });
+  __syncthreads();
+  int ob[G];
+  static_for<G>([&](auto g) __attribute__((always_inline)) { ob[g] = out_blk(g); });
+  T *C = (T *)a.C;
+  constexpr int RCH = BN / 8;  // 8-column chunks per row
+  static_for<(BM * RCH) / 256>([&](auto it) __attribute__((always_inline)) {
+    const int q = tid + it * 256;
+    const int row = q / RCH, c8 = (q % RCH) * 8;
+    const int g = c8 / BLK;
+    int obg = ob[0];
+    static_for<G>([&](auto gg) __attribute__((always_inline)) { if (g == gg) obg = ob[gg]; });
+    const int64_t gm = m0 + row;
+    if (gm < a.M && g < g_valid) {
+      const int64_t col = (int64_t)obg * BLK + (c8 % BLK);
+      const f32x4 lo = *(const f32x4 *)(Cs + row * CS + c8);
+      const f32x4 hi = *(const f32x4 *)(Cs + row * CS + c8 + 4);
+      float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      if (a.nsplit > 1) {
+        float *P = a.partials + ((int64_t)split * a.M + gm) * a.ldp + col;
+        *(f32x4 *)P = lo;
+        *(f32x4 *)(P + 4) = hi;
+        return;
+      }
+      const int64_t o = gm * a.ldc + col;
+      if constexpr (EPI == 1) {  // forward GELU: keep the pre-activation
+        if constexpr (BF) {
+          u32x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            w[e] = (uint32_t)f2bf(v[2 * e]) | ((uint32_t)f2bf(v[2 * e + 1]) << 16);
+          *(u32x4 *)((T *)a.C2 + o) = w;
+        } else {
+          *(f32x4 *)((T *)a.C2 + o) = lo;
+          *(f32x4 *)((T *)a.C2 + o + 4) = hi;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = gelu_f(v[e]);
+      } else if constexpr (EPI == 2) {  // backward GELU: scale by gelu'(pre-activation)
+        const T *ax = (const T *)a.aux + o;
+        if constexpr (BF) {
+          const u32x4 w = *(const u32x4 *)ax;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[2 * e] *= gelu_grad_f(__uint_as_float(w[e] << 16));
+            v[2 * e + 1] *= gelu_grad_f(__uint_as_float(w[e] & 0xffff0000u));
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] *= gelu_grad_f(ax[e]);
+        }
+      }
+      if constexpr (BF) {
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          w[e] = (uint32_t)f2bf(v[2 * e]) | ((uint32_t)f2bf(v[2 * e + 1]) << 16);
+        *(u32x4 *)(C + o) = w;
+      } else {
+        *(f32x4 *)(C + o) = f32x4{v[0], v[1], v[2], v[3]};
+        *(f32x4 *)(C + o + 4) = f32x4{v[4], v[5], v[6], v[7]};
+      }
+    }
+  });
+}
+
+// Sum of split partials, in split order: C[row][col] = sum_s P[s][row][col].
+template <typename T>
+__global__ __launch_bounds__(256) void reduce_rows_kernel(int nsplit, const float *__restrict__ P,
+                                                          int64_t M, int64_t ncols, T *C,
+                                                          int64_t ldc) {
+  const int64_t n4 = M * ncols / 4;  // ncols is a multiple of 32
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n4; q += (int64_t)gridDim.x * 256) {
+    f32x4 v = *(const f32x4 *)(P + q * 4);
+    for (int s = 1; s < nsplit; ++s) v += *(const f32x4 *)(P + (int64_t)s * M * ncols + q * 4);
+    const int64_t e = q * 4, row = e / ncols, col = e % ncols;
+    T *o = C + row * ldc + col;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = from_f<T>(v[i]);
+  }
 }
 
 // ---------------------------------------------------------------------------
 // TN kernel: 128 x 128 output tiles, reduction over tokens.
 // ---------------------------------------------------------------------------
 template <typename T, int BLK>
-__global__ __launch_bounds__(256) void tn_kernel(TNArgs a) {
+struct TNItemView {
+  static constexpr int GT = 128 / BLK;
+  bool sparse;
+  const TNItem *it;
+  int na, nb, ag, bg;
+  const T *Ab, *Bb;
+  int64_t lda, ldb, ldo;
+  T *dout;
+
+  __device__ __forceinline__ void decode(const TNArgs &a, int item) {
+    const int n0 = a.n_dense > 0 ? ((a.dr[0].na_blk + GT - 1) / GT) * ((a.dr[0].nb_blk + GT - 1) / GT) : 0;
+    sparse = item < a.n_items;
+    it = sparse ? a.items + item : nullptr;
+    ag = bg = 0;
+    dout = nullptr;
+    ldo = 0;
+    if (sparse) {
+      Ab = (const T *)a.A; lda = a.lda;
+      Bb = (const T *)a.B; ldb = a.ldb;
+      na = it->na; nb = it->nb;
+    } else {
+      int q = item - a.n_items, r = 0;
+      if (q >= n0) { q -= n0; r = 1; }
+      const TNDense &d = a.dr[r];
+      const int nbg = (d.nb_blk + GT - 1) / GT;
+      ag = q / nbg; bg = q % nbg;
+      Ab = (const T *)d.A; lda = d.lda;
+      Bb = (const T *)d.B; ldb = d.ldb;
+      na = min(GT, d.na_blk - ag * GT);
+      nb = min(GT, d.nb_blk - bg * GT);
+      dout = (T *)d.out;
+      ldo = d.ldo;
+    }
+  }
+  __device__ __forceinline__ int acol(int g) const { return sparse ? it->a_col[g] : ag * GT + min(g, na - 1); }
+  __device__ __forceinline__ int bcol(int g) const { return sparse ? it->b_col[g] : bg * GT + min(g, nb - 1); }
+  __device__ __forceinline__ int oblk(int ga, int gb) const {
+    return sparse ? it->out_blk[ga * kTNMax + gb] : ((ga < na && gb < nb) ? 0 : -1);
+  }
+  // Store one 32 x 32 accumulator tile at (rl0, cl0) of the 128 x 128 item.
+  __device__ __forceinline__ void store_tile(const TNArgs &a, const f32x16 &acc, int rl0, int cl0,
+                                             int lane) const {
+    const int ga = rl0 / BLK, gb = cl0 / BLK;
+    const int cl = cl0 % BLK + (lane & 31);
+    if (sparse) {
+      T *o = (T *)a.Wout + (int64_t)oblk(ga, gb) * (BLK * BLK) + cl;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int rl = rl0 % BLK + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+        o[rl * BLK] = from_f<T>(acc[j]);
+      }
+    } else {
+      T *o = dout + ((int64_t)acol(ga) * BLK) * ldo + (int64_t)bcol(gb) * BLK + cl;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int rl = rl0 % BLK + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+        o[(int64_t)rl * ldo] = from_f<T>(acc[j]);
+      }
+    }
+  }
+};
+
+__device__ __forceinline__ int tn_items_total_dev(const TNArgs &a, int GT) {
+  int n = a.n_items;
+  for (int r = 0; r < a.n_dense; ++r)
+    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
+  return n;
+}
+
+// Partial-sum index of (wave, tm, tn, j, lane): lane-contiguous.
+__device__ __forceinline__ int tn_pidx(int wave, int tm, int tn, int j, int lane) {
+  return (((wave * 2 + tm) * 2 + tn) * 16 + j) * 64 + lane;
+}
+
+template <typename T, int BLK>
+__global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
+  const TNArgs a = a_arg;  // local copy: lambdas below capture it by reference
   constexpr bool BF = std::is_same<T, bf16_t>::value;
   constexpr int GT = 128 / BLK;  // blocks per tile side
-  constexpr int BKT = 32, TILE = 128;
+  constexpr int BKT = BF ? 64 : 32, TILE = 128;
   constexpr int VEC = 16 / (int)sizeof(T);
   constexpr int LDS_S = TILE + (BF ? 16 : 4);
   constexpr int OP_ELEMS = BKT * LDS_S;
   constexpr int CPB = BKT * BLK / VEC;  // chunks of one block column slab
   constexpr int CH = GT * CPB, LD = CH / 256;
   constexpr int TM = 2, TN = 2;  // 4 waves as 2 x 2, 64 x 64 each
-  static_assert(CH % 256 == 0 && CPB % 64 == 0, "chunking");
+  static_assert(CPB % 256 == 0 && LD <= 8, "chunking");
 
   __shared__ __attribute__((aligned(16))) T smem[2 * 2 * OP_ELEMS];
-  __shared__ int s_last;
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = uniform(tid >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
-  const int n_dense_items0 = a.n_dense > 0
-      ? ((a.dr[0].na_blk + GT - 1) / GT) * ((a.dr[0].nb_blk + GT - 1) / GT) : 0;
-  const int n_dense_items1 = a.n_dense > 1
-      ? ((a.dr[1].na_blk + GT - 1) / GT) * ((a.dr[1].nb_blk + GT - 1) / GT) : 0;
-  const int items_total = a.n_items + n_dense_items0 + n_dense_items1;
+  const int items_total = tn_items_total_dev(a, GT);
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
   const int split = bid / items_total, item = bid % items_total;
 
-  // Decode the item.
-  const bool sparse = item < a.n_items;
-  const TNItem *it = sparse ? a.items + item : nullptr;
-  const T *Ab, *Bb;
-  int64_t lda, ldb, ldo = 0;
-  int na, nb, ag = 0, bg = 0;
-  T *dout = nullptr;
-  if (sparse) {
-    Ab = (const T *)a.A; lda = a.lda;
-    Bb = (const T *)a.B; ldb = a.ldb;
-    na = it->na; nb = it->nb;
-  } else {
-    int q = item - a.n_items, r = 0;
-    if (q >= n_dense_items0) { q -= n_dense_items0; r = 1; }
-    const TNDense &d = a.dr[r];
-    const int nbg = (d.nb_blk + GT - 1) / GT;
-    ag = q / nbg; bg = q % nbg;
-    Ab = (const T *)d.A; lda = d.lda;
-    Bb = (const T *)d.B; ldb = d.ldb;
-    na = min(GT, d.na_blk - ag * GT);
-    nb = min(GT, d.nb_blk - bg * GT);
-    dout = (T *)d.out;
-    ldo = d.ldo;
-  }
-  // Column blocks and kept-ness (arguments wave-uniform).
-  auto acol = [&](int g) __attribute__((always_inline)) -> int { return sparse ? it->a_col[g] : ag * GT + min(g, na - 1); };
-  auto bcol = [&](int g) __attribute__((always_inline)) -> int { return sparse ? it->b_col[g] : bg * GT + min(g, nb - 1); };
-  auto oblk = [&](int ga, int gb) __attribute__((always_inline)) -> int {
-    return sparse ? it->out_blk[ga * kTNMax + gb] : ((ga < na && gb < nb) ? 0 : -1);
-  };
+  TNItemView<T, BLK> v;
+  v.decode(a, item);
 
   bool live[TM][TN];
   static_for<TM>([&](auto tm) __attribute__((always_inline)) {
     static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-      live[tm][tn] = oblk((wm * 64 + tm * 32) / BLK, (wn * 64 + tn * 32) / BLK) >= 0;
+      live[tm][tn] = v.oblk((wm * 64 + tm * 32) / BLK, (wn * 64 + tn * 32) / BLK) >= 0;
     });
   });
 
@@ -432,32 +627,37 @@ __global__ __launch_bounds__(256) void tn_kernel(TNArgs a) {
   const int64_t t_end = min(a.T, t_begin + a.chunk);
   const int nsteps = t_end > t_begin ? (int)((t_end - t_begin + BKT - 1) / BKT) : 0;
 
-  static_assert(LD <= 8, "staging registers");
-  Stage8 ra, rb;
-  auto gload = [&](int s) __attribute__((always_inline)) {
+  // Token rows past t_end read as zeros (buffer range).  Column offsets of
+  // each chunk are fixed for the whole loop.
+  const T *const a_base = v.Ab + t_begin * v.lda, *const b_base = v.Bb + t_begin * v.ldb;
+  const int64_t a_bytes = (t_end - t_begin) * v.lda * (int64_t)sizeof(T);
+  const int64_t b_bytes = (t_end - t_begin) * v.ldb * (int64_t)sizeof(T);
+  const uint32_t lda_b = (uint32_t)(v.lda * sizeof(T)), ldb_b = (uint32_t)(v.ldb * sizeof(T));
+  uint32_t offA[LD], offB[LD];
+  static_for<LD>([&](auto i) __attribute__((always_inline)) {
+    constexpr int g = (i * 256) / CPB;
+    const int r = (tid + i * 256) % CPB;
+    const uint32_t t = r / (BLK / VEC), cb = (r % (BLK / VEC)) * 16;
+    offA[i] = t * lda_b + (uint32_t)(v.acol(g) * BLK * sizeof(T)) + cb;
+    offB[i] = t * ldb_b + (uint32_t)(v.bcol(g) * BLK * sizeof(T)) + cb;
+  });
+  auto load = [&](int s, Stage8 &ra, Stage8 &rb) __attribute__((always_inline)) {
+    const rsrc_t rA = make_rsrc(a_base, a_bytes), rB = make_rsrc(b_base, b_bytes);
+    const uint32_t sa = (uint32_t)(s * BKT) * lda_b, sb = (uint32_t)(s * BKT) * ldb_b;
     static_for<LD>([&](auto i) __attribute__((always_inline)) {
-      const int id = tid + i * 256;
-      const int g = uniform(id / CPB), r = id % CPB;
-      const int t = r / (BLK / VEC), cv = r % (BLK / VEC);
-      const int64_t gt = t_begin + (int64_t)s * BKT + t;
-      if (gt < t_end) {
-        ra.template at<i>() = *(const u32x4 *)(Ab + gt * lda + (int64_t)acol(g) * BLK + cv * VEC);
-        rb.template at<i>() = *(const u32x4 *)(Bb + gt * ldb + (int64_t)bcol(g) * BLK + cv * VEC);
-      } else {
-        ra.template at<i>() = u32x4{0u, 0u, 0u, 0u};
-        rb.template at<i>() = u32x4{0u, 0u, 0u, 0u};
-      }
+      ra.template at<i>() = bload(rA, sa + offA[i]);
+      rb.template at<i>() = bload(rB, sb + offB[i]);
     });
   };
-  auto sstore = [&](int buf) __attribute__((always_inline)) {
+  auto store = [&](Stage8 &ra, Stage8 &rb, int buf) __attribute__((always_inline)) {
     T *As = smem + buf * 2 * OP_ELEMS;
     T *Bs = As + OP_ELEMS;
     static_for<LD>([&](auto i) __attribute__((always_inline)) {
-      const int id = tid + i * 256;
-      const int g = id / CPB, r = id % CPB;
-      const int t = r / (BLK / VEC), cv = r % (BLK / VEC);
-      *(u32x4 *)(As + t * LDS_S + g * BLK + cv * VEC) = ra.template at<i>();
-      *(u32x4 *)(Bs + t * LDS_S + g * BLK + cv * VEC) = rb.template at<i>();
+      constexpr int g = (i * 256) / CPB;
+      const int r = (tid + i * 256) % CPB;
+      const int t = r / (BLK / VEC), c = g * BLK + (r % (BLK / VEC)) * VEC;
+      *(u32x4 *)(As + t * LDS_S + c) = ra.template at<i>();
+      *(u32x4 *)(Bs + t * LDS_S + c) = rb.template at<i>();
     });
   };
 
@@ -469,113 +669,126 @@ __global__ __launch_bounds__(256) void tn_kernel(TNArgs a) {
     });
   });
 
-  if (nsteps > 0) {
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    for (int s = 0; s < nsteps; ++s) {
-      const int cur = s & 1;
-      if (s + 1 < nsteps) gload(s + 1);
-      const T *As = smem + cur * 2 * OP_ELEMS;
-      const T *Bs = As + OP_ELEMS;
-      if constexpr (BF) {
-        static_for<BKT / 16>([&](auto ks) __attribute__((always_inline)) {
-          bf16x8 af[TM], bfg[TN];
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            af[tm] = frag_kmajor((const bf16_t *)As, LDS_S, ks, wm * 64 + tm * 32, lane);
-          });
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const T *As = smem + buf * 2 * OP_ELEMS;
+    const T *Bs = As + OP_ELEMS;
+    if constexpr (BF) {
+      static_for<BKT / 16>([&](auto ks) __attribute__((always_inline)) {
+        bf16x8 af[TM], bfg[TN];
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+          af[tm] = frag_kmajor((const bf16_t *)As, LDS_S, ks, wm * 64 + tm * 32, lane);
+        });
+        static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+          bfg[tn] = frag_kmajor((const bf16_t *)Bs, LDS_S, ks, wn * 64 + tn * 32, lane);
+        });
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-            bfg[tn] = frag_kmajor((const bf16_t *)Bs, LDS_S, ks, wn * 64 + tn * 32, lane);
-          });
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-              if (live[tm][tn])
-                acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
-            });
+            if (live[tm][tn])
+              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
-      } else {
-        static_for<BKT / 2>([&](auto ks) __attribute__((always_inline)) {
-          float af[TM], bfg[TN];
-          const int kq = ks * 2 + (lane >> 5);
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) { af[tm] = As[kq * LDS_S + wm * 64 + tm * 32 + (lane & 31)]; });
-          static_for<TN>([&](auto tn) __attribute__((always_inline)) { bfg[tn] = Bs[kq * LDS_S + wn * 64 + tn * 32 + (lane & 31)]; });
-          static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-            static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-              if (live[tm][tn])
-                acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
-            });
+      });
+    } else {
+      static_for<BKT / 2>([&](auto ks) __attribute__((always_inline)) {
+        float af[TM], bfg[TN];
+        const int kq = ks * 2 + (lane >> 5);
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+          af[tm] = As[kq * LDS_S + wm * 64 + tm * 32 + (lane & 31)];
+        });
+        static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+          bfg[tn] = Bs[kq * LDS_S + wn * 64 + tn * 32 + (lane & 31)];
+        });
+        static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+          static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+            if (live[tm][tn])
+              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
-      }
-      if (s + 1 < nsteps) sstore(cur ^ 1);
-      __syncthreads();
+      });
     }
-  }
+  };
+
+  Stage8 ra0, rb0, ra1, rb1;
+  pipeline(nsteps, ra0, rb0, ra1, rb1, load, store, compute);
 
   if (a.nsplit > 1) {
-    // Partial sums in a lane-contiguous order: [wave][tm][tn][j][lane].
-    float *part = a.partials + ((int64_t)item * a.nsplit) * (TILE * TILE);
-    auto pidx = [&](int tm, int tn, int j) __attribute__((always_inline)) {
-      return (((wave * TM + tm) * TN + tn) * 16 + j) * 64 + lane;
-    };
+    float *part = a.partials + ((int64_t)item * a.nsplit + split) * (TILE * TILE);
     static_for<TM>([&](auto tm) __attribute__((always_inline)) {
       static_for<TN>([&](auto tn) __attribute__((always_inline)) {
         if (live[tm][tn]) {
 #pragma unroll
-          for (int j = 0; j < 16; ++j)
-            part[(int64_t)split * (TILE * TILE) + pidx(tm, tn, j)] = acc[tm][tn][j];
+          for (int j = 0; j < 16; ++j) part[tn_pidx(wave, tm, tn, j, lane)] = acc[tm][tn][j];
         }
       });
     });
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-      unsigned prev = atomicAdd(&g_tn_counters[item], 1u);
-      s_last = (prev == (unsigned)(a.nsplit - 1));
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-      static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-        if (live[tm][tn]) {
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            float v = 0.f;
-            for (int sp = 0; sp < a.nsplit; ++sp)
-              v += (sp == split) ? acc[tm][tn][j]
-                                 : __builtin_nontemporal_load(&part[(int64_t)sp * (TILE * TILE) + pidx(tm, tn, j)]);
-            acc[tm][tn][j] = v;
-          }
-        }
-      });
-    });
-    if (tid == 0) atomicExch(&g_tn_counters[item], 0u);
+    return;
   }
-
-  // Store kept blocks.
+  // Stage the 128 x 128 tile in LDS (fp32), then write each kept b x b block
+  // with 16-byte stores of 8 consecutive columns.
+  constexpr int CS = TILE + 4;
+  static_assert(TILE * CS * 4 <= (int)sizeof(smem), "epilogue tile");
+  float *Cs = (float *)smem;
+  __syncthreads();
   static_for<TM>([&](auto tm) __attribute__((always_inline)) {
     static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-      if (live[tm][tn]) {
-        const int rl0 = wm * 64 + tm * 32, cl0 = wn * 64 + tn * 32;
-        const int ga = rl0 / BLK, gb = cl0 / BLK;
-        const int cl = cl0 % BLK + (lane & 31);
-        if (sparse) {
-          T *o = (T *)a.Wout + (int64_t)oblk(ga, gb) * (BLK * BLK) + cl;
+      const int col = wn * 64 + tn * 32 + (lane & 31);
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int rl = rl0 % BLK + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-            o[rl * BLK] = from_f<T>(acc[tm][tn][j]);
-          }
+      for (int j = 0; j < 16; ++j)
+        Cs[(wm * 64 + tm * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3)) * CS + col] = acc[tm][tn][j];
+    });
+  });
+  __syncthreads();
+  constexpr int RCH = BLK / 8;  // 8-column chunks per block row
+  static_for<GT * GT>([&](auto q) __attribute__((always_inline)) {
+    constexpr int ga = q / GT, gb = q % GT;
+    const int blk = v.oblk(ga, gb);
+    if (blk >= 0) {
+      for (int c = tid; c < BLK * RCH; c += 256) {
+        const int rl = c / RCH, c8 = (c % RCH) * 8;
+        const float *src = Cs + (ga * BLK + rl) * CS + gb * BLK + c8;
+        const f32x4 lo = *(const f32x4 *)src, hi = *(const f32x4 *)(src + 4);
+        T *dst = v.sparse ? (T *)a.Wout + (int64_t)blk * (BLK * BLK) + rl * BLK + c8
+                          : v.dout + ((int64_t)v.acol(ga) * BLK + rl) * v.ldo + (int64_t)v.bcol(gb) * BLK + c8;
+        if constexpr (BF) {
+          u32x4 w;
+          w[0] = (uint32_t)f2bf(lo[0]) | ((uint32_t)f2bf(lo[1]) << 16);
+          w[1] = (uint32_t)f2bf(lo[2]) | ((uint32_t)f2bf(lo[3]) << 16);
+          w[2] = (uint32_t)f2bf(hi[0]) | ((uint32_t)f2bf(hi[1]) << 16);
+          w[3] = (uint32_t)f2bf(hi[2]) | ((uint32_t)f2bf(hi[3]) << 16);
+          *(u32x4 *)dst = w;
         } else {
-          T *o = dout + ((int64_t)acol(ga) * BLK) * ldo + (int64_t)bcol(gb) * BLK + cl;
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int rl = rl0 % BLK + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-            o[(int64_t)rl * ldo] = from_f<T>(acc[tm][tn][j]);
-          }
+          *(f32x4 *)dst = lo;
+          *(f32x4 *)(dst + 4) = hi;
         }
+      }
+    }
+  });
+}
+
+// Second pass of a split TN product: per item, sum the split partials in
+// split order and store the kept blocks.
+template <typename T, int BLK>
+__global__ __launch_bounds__(256) void tn_reduce_kernel(TNArgs a_arg) {
+  const TNArgs a = a_arg;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int item = xcd_remap(blockIdx.x, gridDim.x);
+  TNItemView<T, BLK> v;
+  v.decode(a, item);
+  const float *part = a.partials + (int64_t)item * a.nsplit * (128 * 128);
+  static_for<2>([&](auto tm) __attribute__((always_inline)) {
+    static_for<2>([&](auto tn) __attribute__((always_inline)) {
+      if (v.oblk((wm * 64 + tm * 32) / BLK, (wn * 64 + tn * 32) / BLK) >= 0) {
+        f32x16 acc;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int q = tn_pidx(wave, tm, tn, j, lane);
+          float s = part[q];
+          for (int sp = 1; sp < a.nsplit; ++sp) s += part[(int64_t)sp * (128 * 128) + q];
+          acc[j] = s;
+        }
+        v.store_tile(a, acc, wm * 64 + tm * 32, wn * 64 + tn * 32, lane);
       }
     });
   });
@@ -593,41 +806,73 @@ __global__ __launch_bounds__(256) void gelu_bwd_kernel(int64_t n, const T *dH, c
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
-template <typename T, int BLK, int G, bool BKN>
+template <typename T, int BLK, int G, bool BKN, int BM, bool DENSE>
 static hipError_t nt_go(const NTArgs &a, hipStream_t s) {
-  const int64_t mtiles = (a.M + 127) / 128;
-  const int64_t grid = mtiles * a.ntiles;
+  const int64_t mtiles = (a.M + BM - 1) / BM;
+  const int64_t grid = mtiles * a.ntiles * std::max(1, a.nsplit);
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  // Epilogue variants: the forward takes the GELU-forward one, the
+  // backward-data (B read as [k][n]) the GELU-backward one.
+  if (!DENSE && a.epi == 1) {
+    if constexpr (!DENSE) {
+      if constexpr (BKN) hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN, BM, DENSE, 2>), dim3((unsigned)grid), dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN, BM, DENSE, 1>), dim3((unsigned)grid), dim3(256), 0, s, a);
+    }
+  } else {
+    hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN, BM, DENSE, 0>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
+// Instantiated tiles: sparse tiles with BM = 128 and G * b <= 128; dense
+// tiles (comparator, skinny rank-r products) with G * b = 128 and BM = 128
+// or 64.
 template <typename T, int BLK, bool BKN>
-static hipError_t nt_dispatch_g(int G, const NTArgs &a, hipStream_t s) {
-  switch (G) {
-    case 1: return nt_go<T, BLK, 1, BKN>(a, s);
-    case 2: return nt_go<T, BLK, 2, BKN>(a, s);
-    case 4:
-      if constexpr (BLK <= 64) return nt_go<T, BLK, 4, BKN>(a, s);
-      else return hipErrorInvalidValue;
-    default: return hipErrorInvalidValue;
+static hipError_t nt_dispatch_g(int G, int bm, bool dense, const NTArgs &a, hipStream_t s) {
+  constexpr int GMAX = 128 / BLK;
+  if (dense) {
+    if (G != GMAX) return hipErrorInvalidValue;
+    return bm == 64 ? nt_go<T, BLK, GMAX, BKN, 64, true>(a, s) : nt_go<T, BLK, GMAX, BKN, 128, true>(a, s);
   }
+  if (bm != 128) return hipErrorInvalidValue;
+  if (G == 1) return nt_go<T, BLK, 1, BKN, 128, false>(a, s);
+  if constexpr (GMAX >= 2)
+    if (G == 2) return nt_go<T, BLK, 2, BKN, 128, false>(a, s);
+  if constexpr (GMAX >= 4)
+    if (G == 4) return nt_go<T, BLK, 4, BKN, 128, false>(a, s);
+  return hipErrorInvalidValue;
 }
 
 template <typename T, bool BKN>
-static hipError_t nt_dispatch_b(int blk, int G, const NTArgs &a, hipStream_t s) {
+static hipError_t nt_dispatch_b(int blk, int G, int bm, bool dense, const NTArgs &a, hipStream_t s) {
   switch (blk) {
-    case 32: return nt_dispatch_g<T, 32, BKN>(G, a, s);
-    case 64: return nt_dispatch_g<T, 64, BKN>(G, a, s);
-    case 128: return nt_dispatch_g<T, 128, BKN>(G, a, s);
+    case 32: return nt_dispatch_g<T, 32, BKN>(G, bm, dense, a, s);
+    case 64: return nt_dispatch_g<T, 64, BKN>(G, bm, dense, a, s);
+    case 128: return nt_dispatch_g<T, 128, BKN>(G, bm, dense, a, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, const NTArgs &a, hipStream_t s) {
+hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a, hipStream_t s) {
+  const bool dense = a.dense != 0;
   if (dtype == 0)
-    return b_kn ? nt_dispatch_b<bf16_t, true>(blk, G, a, s) : nt_dispatch_b<bf16_t, false>(blk, G, a, s);
-  return b_kn ? nt_dispatch_b<float, true>(blk, G, a, s) : nt_dispatch_b<float, false>(blk, G, a, s);
+    return b_kn ? nt_dispatch_b<bf16_t, true>(blk, G, bm, dense, a, s)
+                : nt_dispatch_b<bf16_t, false>(blk, G, bm, dense, a, s);
+  return b_kn ? nt_dispatch_b<float, true>(blk, G, bm, dense, a, s)
+              : nt_dispatch_b<float, false>(blk, G, bm, dense, a, s);
+}
+
+hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
+                              void *C, int64_t ldc, hipStream_t s) {
+  const int64_t n4 = M * ncols / 4;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n4 + 255) / 256, 4096));
+  if (dtype == 0)
+    hipLaunchKernelGGL((reduce_rows_kernel<bf16_t>), dim3((unsigned)blocks), dim3(256), 0, s, nsplit, P,
+                       M, ncols, (bf16_t *)C, ldc);
+  else
+    hipLaunchKernelGGL((reduce_rows_kernel<float>), dim3((unsigned)blocks), dim3(256), 0, s, nsplit, P,
+                       M, ncols, (float *)C, ldc);
+  return hipGetLastError();
 }
 
 int tn_items_total(const TNArgs &a, int blk) {
@@ -640,9 +885,13 @@ int tn_items_total(const TNArgs &a, int blk) {
 
 template <typename T, int BLK>
 static hipError_t tn_go(const TNArgs &a, hipStream_t s) {
-  const int64_t grid = (int64_t)tn_items_total(a, BLK) * a.nsplit;
+  const int64_t items = tn_items_total(a, BLK);
+  const int64_t grid = items * a.nsplit;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((tn_kernel<T, BLK>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.nsplit <= 1) return e;
+  hipLaunchKernelGGL((tn_reduce_kernel<T, BLK>), dim3((unsigned)items), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -19,10 +19,14 @@
 
 namespace pf {
 
+// Widest NT output tile in columns (the tile is G blocks of b columns).
+#ifndef PF_MAX_BN
+#define PF_MAX_BN 128
+#endif
+
 int max_group(int32_t b) {
-  if (b == 32 || b == 64) return 4;
-  if (b == 128) return 2;
-  return 1;
+  if (b != 32 && b != 64 && b != 128) return 1;
+  return std::max(1, std::min(4, PF_MAX_BN / b));
 }
 
 static int tn_group(int32_t b) {

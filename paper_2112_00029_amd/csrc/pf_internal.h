@@ -57,6 +57,11 @@ struct NTArgs {
   int ntiles;           // output column tiles (dense mode: ceil(nblk / G))
   const int32_t *kcols;
   const int32_t *blks;
+  // Split of the K-steps across workgroups (dense mode only): each split
+  // writes fp32 partial outputs P[split][M][ldp]; reduce_rows sums them.
+  int nsplit;
+  float *partials;
+  int64_t ldp;
 };
 
 // A dense region of the TN kernel: out[a][b] = sum_t A[t][a] B[t][b] over
@@ -83,7 +88,7 @@ struct TNArgs {
   int n_dense;
   int64_t T;
   int nsplit;
-  int64_t chunk;        // tokens per split (multiple of 32)
+  int64_t chunk;        // tokens per split (multiple of 64)
   float *partials;      // [items_total][nsplit][128*128] when nsplit > 1
 };
 
@@ -98,17 +103,19 @@ struct AttnArgs {
   const int32_t *row_ptr, *col_idx, *col_ptr, *row_idx;
 };
 
-// Kernel launchers (gemm_kernels.hip / attn_kernels.hip).
-hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, const NTArgs &a,
+// Kernel launchers (gemm_kernels.hip / attn_kernels.hip).  bm is the
+// M-tile (tokens per workgroup): 128, or 64 for the skinny rank-r products.
+hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a,
                      hipStream_t s);
+// Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
+hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
+                              void *C, int64_t ldc, hipStream_t s);
+// The TN kernel; with a.nsplit > 1 it also launches its reduce pass.
 hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
 int tn_items_total(const TNArgs &a, int blk);
 hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
                            const void *Hpre, void *out, hipStream_t s);
 hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s);
 hipError_t launch_attn_bwd(const AttnArgs &a, hipStream_t s);
-
-// Static counter array (one per device) for split-token reductions.
-constexpr int kMaxCounters = 1 << 16;
 
 }  // namespace pf

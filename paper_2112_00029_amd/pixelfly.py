@@ -69,8 +69,9 @@ _SIGS = {
     "pf_layout_upload": (_i32, [_p, _p]),
     "pf_layout_destroy": (None, [_p]),
     "pf_workspace_bytes": (_sz, [_p, _i64, _i32, _i32]),
-    "pf_linear_fwd": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _i32, _p, _p]),
-    "pf_linear_bwd_data": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _i32, _p, _p]),
+    "pf_linear_fwd": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _i32, _p, _p, _sz, _p]),
+    "pf_linear_bwd_data": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _i32, _p, _p, _sz,
+                                  _p]),
     "pf_linear_bwd_weight": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p]),
     "pf_gelu_bwd": (_i32, [_i32, _i64, _p, _p, _p, _p]),
     "pf_attn_fwd": (_i32, [_p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p]),
@@ -207,16 +208,17 @@ def pf_workspace_bytes(layout: Layout, T: int, r: int, dtype) -> int:
 
 
 def pf_linear_fwd(layout, dtype, T, r, X, Wblk, U, V, Y, T_lr, epi=PF_EPI_NONE,
-                  Y_pre=None, stream=None) -> None:
+                  Y_pre=None, workspace=None, ws_bytes=0, stream=None) -> None:
     _check(_lib.pf_linear_fwd(layout.handle, _dt(dtype), T, r, _ptr(X), _ptr(Wblk), _ptr(U),
-                              _ptr(V), _ptr(Y), _ptr(T_lr), epi, _ptr(Y_pre), _stream(stream)))
+                              _ptr(V), _ptr(Y), _ptr(T_lr), epi, _ptr(Y_pre), _ptr(workspace),
+                              ws_bytes, _stream(stream)))
 
 
 def pf_linear_bwd_data(layout, dtype, T, r, dY, Wblk, U, V, S, dX, epi=PF_EPI_NONE,
-                       aux=None, stream=None) -> None:
+                       aux=None, workspace=None, ws_bytes=0, stream=None) -> None:
     _check(_lib.pf_linear_bwd_data(layout.handle, _dt(dtype), T, r, _ptr(dY), _ptr(Wblk),
                                    _ptr(U), _ptr(V), _ptr(S), _ptr(dX), epi, _ptr(aux),
-                                   _stream(stream)))
+                                   _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def pf_linear_bwd_weight(layout, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, workspace,

@@ -61,11 +61,14 @@ def test_tiled_layouts_group_rows():
     # tiled copies along the output dim form 4-row tiles for the forward
     st = pf.pf_layout_plan_get(pf.pf_layout_create(3072, 768, 32, 16))
     assert st["G_fwd"] == 4 and st["fwd_tiles"] == 24
+    # tiles are at most 128 columns wide
     st = pf.pf_layout_plan_get(pf.pf_layout_create(16384, 4096, 128, 32))
-    assert st["G_fwd"] == 2 and st["fwd_tiles"] == 64
-    # tiled copies along the input dim form 4-column tiles for backward-data
+    assert st["G_fwd"] == 1 and st["fwd_tiles"] == 128
+    st = pf.pf_layout_plan_get(pf.pf_layout_create(16384, 4096, 64, 32))
+    assert st["G_fwd"] == 2 and st["fwd_tiles"] == 128
+    # tiled copies along the input dim form 2-column tiles for backward-data
     st = pf.pf_layout_plan_get(pf.pf_layout_create(1024, 4096, 64, 16))
-    assert st["G_bwd"] == 4 and st["bwd_tiles"] == 16
+    assert st["G_bwd"] == 2 and st["bwd_tiles"] == 32
 
 
 def test_layout_create_errors():
@@ -146,8 +149,9 @@ def test_workspace_sizes():
     ws = pf.pf_workspace_bytes(L, 4096, 96, pf.PF_BF16)
     assert ws > 0 and ws % 4 == 0
     assert pf.pf_workspace_bytes(L, 4096, 95, pf.PF_BF16) == 0
-    # tiny token counts need no split, so no workspace
-    assert pf.pf_workspace_bytes(L, 64, 96, pf.PF_BF16) == 0
+    # split partials scale with the tokens
+    assert pf.pf_workspace_bytes(L, 64, 96, pf.PF_BF16) < ws
+    assert pf.pf_workspace_bytes(L, 4096, 0, pf.PF_BF16) <= ws
     assert pf.pf_attn_workspace_bytes(8, 12, 4096) >= 8 * 12 * 4096 * 4
     assert pf.pf_dense_workspace_bytes(pf.PF_BF16, pf.PF_OP_NT, 128, 128, 128) == 0
 

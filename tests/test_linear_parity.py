@@ -56,10 +56,12 @@ def _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp):
     dV = empty((max(r, 1), n_in), dtype)
     U = d["U"] if r else None
     V = d["V"] if r else None
-    pf.pf_linear_fwd(L, dtype, T, r, d["X"], d["W"], U, V, Y, Tl if r else None)
-    pf.pf_linear_bwd_data(L, dtype, T, r, d["dY"], d["W"], U, V, S if r else None, dX)
     ws_bytes = pf.pf_workspace_bytes(L, T, r, dtype)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
+    pf.pf_linear_fwd(L, dtype, T, r, d["X"], d["W"], U, V, Y, Tl if r else None,
+                     workspace=ws, ws_bytes=ws_bytes)
+    pf.pf_linear_bwd_data(L, dtype, T, r, d["dY"], d["W"], U, V, S if r else None, dX,
+                          workspace=ws, ws_bytes=ws_bytes)
     pf.pf_linear_bwd_weight(L, dtype, T, r, d["dY"], d["X"], Tl if r else None,
                             S if r else None, dW, dU if r else None, dV if r else None,
                             ws, ws_bytes)
@@ -163,23 +165,24 @@ def test_mlp_pair_gelu():
     W1, U1, V1 = (to_dev(l1["raw"][k]) for k in ("W", "U", "V"))
     W2, U2, V2 = (to_dev(l2["raw"][k]) for k in ("W", "U", "V"))
     dY = to_dev(l2["raw"]["dY"])
-    Hpre, H, T1 = empty((T, N), dtype), empty((T, N), dtype), empty((T, r), dtype)
-    Y, T2 = empty((T, K), dtype), empty((T, r), dtype)
-    pf.pf_linear_fwd(L1, dtype, T, r, X, W1, U1, V1, H, T1, pf.PF_EPI_GELU, Hpre)
-    pf.pf_linear_fwd(L2, dtype, T, r, H, W2, U2, V2, Y, T2)
-    dHpre, S2, dX, S1 = empty((T, N), dtype), empty((T, r), dtype), empty((T, K), dtype), empty((T, r), dtype)
-    pf.pf_linear_bwd_data(L2, dtype, T, r, dY, W2, U2, V2, S2, dHpre, pf.PF_EPI_GELU, Hpre)
-    pf.pf_linear_bwd_data(L1, dtype, T, r, dHpre, W1, U1, V1, S1, dX)
-    dW1, dU1, dV1 = empty(tuple(W1.shape), dtype), empty((N, r), dtype), empty((r, K), dtype)
-    dW2, dU2, dV2 = empty(tuple(W2.shape), dtype), empty((K, r), dtype), empty((r, N), dtype)
     ws_b = max(pf.pf_workspace_bytes(L1, T, r, dtype), pf.pf_workspace_bytes(L2, T, r, dtype))
     ws = torch.empty(max(ws_b, 256), dtype=torch.uint8, device="cuda")
+    W = dict(workspace=ws, ws_bytes=ws_b)
+    Hpre, H, T1 = empty((T, N), dtype), empty((T, N), dtype), empty((T, r), dtype)
+    Y, T2 = empty((T, K), dtype), empty((T, r), dtype)
+    pf.pf_linear_fwd(L1, dtype, T, r, X, W1, U1, V1, H, T1, pf.PF_EPI_GELU, Hpre, **W)
+    pf.pf_linear_fwd(L2, dtype, T, r, H, W2, U2, V2, Y, T2, **W)
+    dHpre, S2, dX, S1 = empty((T, N), dtype), empty((T, r), dtype), empty((T, K), dtype), empty((T, r), dtype)
+    pf.pf_linear_bwd_data(L2, dtype, T, r, dY, W2, U2, V2, S2, dHpre, pf.PF_EPI_GELU, Hpre, **W)
+    pf.pf_linear_bwd_data(L1, dtype, T, r, dHpre, W1, U1, V1, S1, dX, **W)
+    dW1, dU1, dV1 = empty(tuple(W1.shape), dtype), empty((N, r), dtype), empty((r, K), dtype)
+    dW2, dU2, dV2 = empty(tuple(W2.shape), dtype), empty((K, r), dtype), empty((r, N), dtype)
     pf.pf_linear_bwd_weight(L2, dtype, T, r, dY, H, T2, S2, dW2, dU2, dV2, ws, ws_b)
     pf.pf_linear_bwd_weight(L1, dtype, T, r, dHpre, X, T1, S1, dW1, dU1, dV1, ws, ws_b)
     # standalone GELU backward agrees with the fused epilogue's definition
     dHpre2 = empty((T, N), dtype)
     dH_alone = empty((T, N), dtype)
-    pf.pf_linear_bwd_data(L2, dtype, T, r, dY, W2, U2, V2, S2, dH_alone)
+    pf.pf_linear_bwd_data(L2, dtype, T, r, dY, W2, U2, V2, S2, dH_alone, **W)
     pf.pf_gelu_bwd(dtype, T * N, dH_alone, Hpre, dHpre2)
     torch.cuda.synchronize()
 
