@@ -269,51 +269,40 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
   constexpr int64_t BIG = 0x7fffffff;
 
   // Sub-block h of step s (all arguments wave-uniform): A base, byte range,
-  // row stride and column offset in bytes.
+  // row stride and column offset in bytes.  Branch-free: the index tables
+  // are read at a clamped position and the phase (kept block, low-rank
+  // block, zero padding) is applied with selects.
   auto a_src = [&](int s, int h, const T *&base, int64_t &bytes, uint32_t &ldb,
                    uint32_t &colb) __attribute__((always_inline)) {
     const int k0 = (s_begin + s) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
-    if (c < nsteps) {
-      const int kcol = DENSE ? c : a.kcols[kcol_off + c];
-      base = a_base;
-      bytes = a_bytes;
-      ldb = (uint32_t)(a.lda * ES);
-      colb = (uint32_t)((kcol * BLK + kk) * ES);
-    } else {
-      base = l_base;
-      bytes = c < vblocks ? l_bytes : 0;
-      ldb = (uint32_t)(a.ldl * ES);
-      colb = (uint32_t)(((c - nsteps) * BLK + kk) * ES);
-    }
+    const bool sp = c < nsteps;
+    const int kcol = DENSE ? c : a.kcols[kcol_off + min(c, nsteps - 1)];
+    base = sp ? a_base : l_base;
+    bytes = sp ? a_bytes : (c < vblocks ? l_bytes : 0);
+    ldb = (uint32_t)((sp ? a.lda : a.ldl) * ES);
+    colb = (uint32_t)(((sp ? kcol : c - nsteps) * BLK + kk) * ES);
   };
   // Piece (g, h) of step s: B base at the piece, byte range, row stride.
   auto b_src = [&](int s, int g, int h, const T *&base, int64_t &bytes,
                    uint32_t &ldb) __attribute__((always_inline)) {
     const int k0 = (s_begin + s) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
-    bytes = BIG;
-    if (c < nsteps) {
-      if constexpr (DENSE) {
-        ldb = (uint32_t)(a.ldb * ES);
-        const int64_t ob = out_blk(g);
-        base = BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
-                   : B + (ob * BLK) * a.ldb + (int64_t)c * BLK + kk;
-      } else {
-        ldb = BLK * ES;
-        const int64_t blk = a.blks[blk_off + c * G + g];
-        base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
-      }
-      return;
-    }
-    ldb = (uint32_t)(a.ldr * ES);
-    if (c >= vblocks) {
-      base = B;
-      bytes = 0;
-      return;
-    }
-    const int cr = c - nsteps;
     const int64_t ob = out_blk(g);
-    base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
-               : R + (ob * BLK) * a.ldr + (int64_t)cr * BLK + kk;
+    if constexpr (DENSE) {
+      ldb = (uint32_t)(a.ldb * ES);
+      base = BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
+                 : B + (ob * BLK) * a.ldb + (int64_t)c * BLK + kk;
+      bytes = c < nsteps ? BIG : 0;
+    } else {
+      const bool sp = c < nsteps;
+      const int64_t blk = a.blks[blk_off + min(c, nsteps - 1) * G + g];
+      const int cr = c - nsteps;
+      const T *sp_base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
+      const T *lr_base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
+                             : R + (ob * BLK) * a.ldr + (int64_t)cr * BLK + kk;
+      base = sp ? sp_base : lr_base;
+      bytes = (sp || c < vblocks) ? BIG : 0;
+      ldb = (uint32_t)(sp ? BLK * ES : a.ldr * ES);
+    }
   };
 
   auto load = [&](int s, Stage8 &ra, Stage8 &rb) __attribute__((always_inline)) {
@@ -555,27 +544,6 @@ struct TNItemView {
   __device__ __forceinline__ int oblk(int ga, int gb) const {
     return sparse ? it->out_blk[ga * kTNMax + gb] : ((ga < na && gb < nb) ? 0 : -1);
   }
-  // Store one 32 x 32 accumulator tile at (rl0, cl0) of the 128 x 128 item.
-  __device__ __forceinline__ void store_tile(const TNArgs &a, const f32x16 &acc, int rl0, int cl0,
-                                             int lane) const {
-    const int ga = rl0 / BLK, gb = cl0 / BLK;
-    const int cl = cl0 % BLK + (lane & 31);
-    if (sparse) {
-      T *o = (T *)a.Wout + (int64_t)oblk(ga, gb) * (BLK * BLK) + cl;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int rl = rl0 % BLK + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-        o[rl * BLK] = from_f<T>(acc[j]);
-      }
-    } else {
-      T *o = dout + ((int64_t)acol(ga) * BLK) * ldo + (int64_t)bcol(gb) * BLK + cl;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int rl = rl0 % BLK + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
-        o[(int64_t)rl * ldo] = from_f<T>(acc[j]);
-      }
-    }
-  }
 };
 
 __device__ __forceinline__ int tn_items_total_dev(const TNArgs &a, int GT) {
@@ -765,33 +733,37 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
   });
 }
 
-// Second pass of a split TN product: per item, sum the split partials in
-// split order and store the kept blocks.
+// Second pass of a split TN product: sum the split partials in split order
+// and store the kept blocks.  Workgroup (item, part): 16 parts of 1024
+// partial sums per item; each thread takes 4 consecutive partial sums
+// (4 consecutive columns of one output row in the lane-contiguous order).
 template <typename T, int BLK>
 __global__ __launch_bounds__(256) void tn_reduce_kernel(TNArgs a_arg) {
   const TNArgs a = a_arg;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int item = xcd_remap(blockIdx.x, gridDim.x);
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int item = bid / 16, part = bid % 16;
   TNItemView<T, BLK> v;
   v.decode(a, item);
-  const float *part = a.partials + (int64_t)item * a.nsplit * (128 * 128);
-  static_for<2>([&](auto tm) __attribute__((always_inline)) {
-    static_for<2>([&](auto tn) __attribute__((always_inline)) {
-      if (v.oblk((wm * 64 + tm * 32) / BLK, (wn * 64 + tn * 32) / BLK) >= 0) {
-        f32x16 acc;
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int q = tn_pidx(wave, tm, tn, j, lane);
-          float s = part[q];
-          for (int sp = 1; sp < a.nsplit; ++sp) s += part[(int64_t)sp * (128 * 128) + q];
-          acc[j] = s;
-        }
-        v.store_tile(a, acc, wm * 64 + tm * 32, wn * 64 + tn * 32, lane);
-      }
-    });
-  });
+  const int q = (part * 256 + threadIdx.x) * 4;  // partial index
+  const int lane = q % 64, j = (q / 64) % 16, tn = (q / 1024) % 2, tm = (q / 2048) % 2, wave = q / 4096;
+  const int rl = (wave >> 1) * 64 + tm * 32 + (j >> 2) * 8 + (lane >> 5) * 4 + (j & 3);
+  const int cl = (wave & 1) * 64 + tn * 32 + (lane & 31);
+  const int ga = rl / BLK, gb = cl / BLK;
+  const int blk = v.oblk(ga, gb);
+  if (blk < 0) return;
+  const float *part_p = a.partials + (int64_t)item * a.nsplit * (128 * 128) + q;
+  f32x4 acc = *(const f32x4 *)part_p;
+  for (int sp = 1; sp < a.nsplit; ++sp) acc += *(const f32x4 *)(part_p + (int64_t)sp * (128 * 128));
+  T *dst = v.sparse ? (T *)a.Wout + (int64_t)blk * (BLK * BLK) + (rl % BLK) * BLK + (cl % BLK)
+                    : v.dout + ((int64_t)v.acol(ga) * BLK + (rl % BLK)) * v.ldo + (int64_t)v.bcol(gb) * BLK + (cl % BLK);
+  if constexpr (std::is_same<T, bf16_t>::value) {
+    uint2 w;
+    w.x = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
+    w.y = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
+    *(uint2 *)dst = w;
+  } else {
+    *(f32x4 *)dst = acc;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -891,7 +863,7 @@ static hipError_t tn_go(const TNArgs &a, hipStream_t s) {
   hipLaunchKernelGGL((tn_kernel<T, BLK>), dim3((unsigned)grid), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsplit <= 1) return e;
-  hipLaunchKernelGGL((tn_reduce_kernel<T, BLK>), dim3((unsigned)items), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((tn_reduce_kernel<T, BLK>), dim3((unsigned)(items * 16)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
