@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libpixelfly.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["layout.cpp", "capi.cpp", "gemm_kernels.hip", "attn_kernels.hip"]
+SOURCES = ["layout.cpp", "capi.cpp", "gemm_kernels.hip", "gemm_dma.hip", "attn_kernels.hip"]
 
 FLAGS = [
     "-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",

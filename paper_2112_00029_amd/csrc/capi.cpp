@@ -69,6 +69,17 @@ int pow2_group(int gmax, int n) {
   return g;
 }
 
+// NT launch: bf16 tiles 128 columns wide go to the direct-to-LDS kernel
+// family, everything else to the register-staged one.
+#ifndef PF_NTD
+#define PF_NTD 1
+#endif
+hipError_t nt_launch(int dtype, int blk, int G, bool b_kn, int bm, const pf::NTArgs &a,
+                     hipStream_t s) {
+  if (PF_NTD && dtype == 0 && bm == 128 && G * blk == 128) return pf::launch_ntd(blk, G, b_kn, 0, a, s);
+  return pf::launch_nt(dtype, blk, G, b_kn, bm, a, s);
+}
+
 // Dense-mode NT launch: C[M x nblk*b] = A[M x nsteps*b] . B^T (B [n][k]) or
 // A . B (B [k][n]), with M-tile bm; split over K when ws gives room.
 pf_status dense_nt(int dtype, int blk, bool b_kn, int bm, int64_t M, const void *A, int64_t lda,
@@ -83,7 +94,7 @@ pf_status dense_nt(int dtype, int blk, bool b_kn, int bm, int64_t M, const void 
   a.nsplit = nsplit;
   a.partials = ws;
   a.ldp = (int64_t)nblk * blk;
-  pf_status st = hip_status(pf::launch_nt(dtype, blk, G, b_kn, bm, a, s), what);
+  pf_status st = hip_status(nt_launch(dtype, blk, G, b_kn, bm, a, s), what);
   if (st != PF_OK || nsplit <= 1) return st;
   return hip_status(pf::launch_reduce_rows(dtype, nsplit, ws, M, (int64_t)nblk * blk, C, ldc, s), what);
 }
@@ -395,7 +406,7 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   a.tiles = L->d_fwd_tiles; a.ntiles = (int)L->fwd_tiles.size();
   a.kcols = L->d_kcols_fwd; a.blks = L->d_blks_fwd;
   a.nsplit = 1;
-  return hip_status(pf::launch_nt(dt, b, L->G_fwd, false, 128, a, s), "forward kernel");
+  return hip_status(nt_launch(dt, b, L->G_fwd, false, 128, a, s), "forward kernel");
 }
 
 pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -435,7 +446,7 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.tiles = L->d_bwd_tiles; a.ntiles = (int)L->bwd_tiles.size();
   a.kcols = L->d_kcols_bwd; a.blks = L->d_blks_bwd;
   a.nsplit = 1;
-  return hip_status(pf::launch_nt(dt, b, L->G_bwd, true, 128, a, s), "backward-data kernel");
+  return hip_status(nt_launch(dt, b, L->G_bwd, true, 128, a, s), "backward-data kernel");
 }
 
 pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,

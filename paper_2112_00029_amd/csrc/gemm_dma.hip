@@ -1,0 +1,518 @@
+// bf16 NT GEMM family for gfx950 with direct global -> LDS operand loads.
+//
+// Same products as the NT kernel of gemm_kernels.hip (forward and
+// backward-data block-sparse products with the fused low-rank K-blocks, the
+// dense comparator, the skinny rank-r products), restructured around the
+// CDNA4 memory path:
+//
+//  * Operands move global -> LDS with buffer_load_dwordx4 ... lds: lane i of
+//    a wave deposits its 16 bytes at LDS base + 16 i, so one wave instruction
+//    fills a 1 KiB "window" and no VGPRs or ds_write instructions are spent
+//    on staging.  The lane -> global address map places each 16-byte chunk
+//    at an XOR-swizzled position so that the MFMA fragment reads below are
+//    free of LDS bank conflicts.
+//  * NS pipeline stages live in separate LDS arrays; the step loop is
+//    unrolled by NS so every LDS access names its array at compile time.
+//    The compiler tracks the LDS DMA of each array separately and therefore
+//    only waits for the stage it is about to read.  The cross-wave handoff is
+//    an explicit vmcnt wait (this wave's copies of the step have landed)
+//    followed by s_barrier (every wave's have).
+//  * Operands are swapped in the MFMA (D = W-tile . X-tile^T) so that each
+//    lane ends up holding 4 consecutive output columns of one token row; the
+//    epilogue transposes each wave's tile through LDS so that every store
+//    covers whole 128-byte row segments.
+//
+// Tile: BM tokens x BN = G * BLK output columns, 4 waves as 2 x 2.  The
+// virtual K range of a tile is its kept blocks, then the r / BLK low-rank
+// blocks, then zero padding to a multiple of BK.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <type_traits>
+
+#include "pf_internal.h"
+
+namespace pf {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((address_space(3))) void lds_void;
+
+template <int I, int N, typename F>
+__device__ __forceinline__ void sfor_impl(F &&f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    sfor_impl<I + 1, N>(f);
+  }
+}
+template <int N, typename F>
+__device__ __forceinline__ void sfor(F &&f) {
+  sfor_impl<0, N>(f);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+}
+__device__ __forceinline__ float gelu(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+__device__ __forceinline__ float gelu_grad(float x) {
+  const float Phi = 0.5f * (1.0f + erff(x * 0.70710678118654752f));
+  return Phi + x * 0.39894228040143268f * __expf(-0.5f * x * x);
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs; remap so that
+// consecutive logical ids run on the same XCD (and share its L2).
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  constexpr int X = 8;
+  const int q = n / X, rem = n % X, x = bid % X, slot = bid / X;
+  return x * q + min(x, rem) + slot;
+}
+
+// Buffer resource over [p, p + bytes): loads outside the range return zero
+// (ragged token tiles, K padding).
+__device__ __forceinline__ rsrc_t make_rsrc(const void *p, int64_t bytes) {
+  const int64_t b = bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)b, 0x00020000);
+}
+
+// One 1 KiB window: lane i copies 16 bytes from rsrc + voff + soff to
+// lds + 16 i.
+__device__ __forceinline__ void dma16(rsrc_t r, uint8_t *lds, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, (int)voff, (int)soff, 0, 0);
+}
+
+// Wait until at most VM vector-memory operations of this wave are in flight
+// and all of its LDS reads have returned.
+template <int VM>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(VM >= 0 && VM < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
+}
+__device__ __forceinline__ void barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// XOR swizzle of the 16-byte chunk index in a [row][chunk] LDS region with
+// CPR chunks per row (row-major operand, read with 16-byte fragment reads:
+// 16 consecutive rows at a fixed chunk hit distinct banks).
+template <int CPR>
+__device__ __forceinline__ int swz_row(int r) {
+  if constexpr (CPR == 4) return (r >> 2) & 3;
+  else return (r >> 1) & 7;
+}
+// Same for a [k][n] region read with the transpose read (4 consecutive k
+// rows x 32 bytes hit distinct banks).
+template <int CPR>
+__device__ __forceinline__ int swz_k(int k) {
+  if constexpr (CPR == 4) return 0;
+  else if constexpr (CPR == 8) return ((k >> 1) & 1) << 2;
+  else return (k & 3) << 2;
+}
+
+// MFMA 32x32x16 operand (lane l: row l % 32, k = (l / 32) * 8 + 0..7 of
+// k-slice kq) from a swizzled [row][chunk] region with row stride RB bytes.
+template <int RB>
+__device__ __forceinline__ bf16x8 frag_rows(const uint8_t *region, int r0, int kq, int lane) {
+  constexpr int CPR = RB / 16;
+  const int r = r0 + (lane & 31);
+  const int c = kq * 2 + (lane >> 5);
+  return *(const bf16x8 *)(region + r * RB + ((c ^ swz_row<CPR>(r)) << 4));
+}
+
+__device__ __forceinline__ s16x4 tr16(const uint8_t *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(p));
+}
+
+// Same operand from a swizzled [k][n] region (n contiguous, RB bytes per k
+// row): rows are n0 + l % 32, read with ds_read_b64_tr_b16 (within each
+// 16-lane group, lanes 4m..4m+3 address k row m and lane j receives the 4
+// k values of column j).
+template <int RB>
+__device__ __forceinline__ bf16x8 frag_kn(const uint8_t *region, int n0, int kq, int lane) {
+  constexpr int CPR = RB / 16;
+  const int g16 = lane >> 4, i = lane & 15;
+  const int n = n0 + (g16 & 1) * 16 + (i & 3) * 4;
+  const int k = kq * 16 + (g16 >> 1) * 8 + (i >> 2);
+  const int c = n >> 3, half = ((n >> 2) & 1) << 3;
+  const s16x4 lo = tr16(region + k * RB + ((c ^ swz_k<CPR>(k)) << 4) + half);
+  const s16x4 hi = tr16(region + (k + 4) * RB + ((c ^ swz_k<CPR>(k + 4)) << 4) + half);
+  const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int BLK, int G, bool BKN, int BM, int BK, int NS, bool DENSE, int EPI, int OCC>
+__global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
+  const NTArgs a = a_arg;
+  constexpr int BN = G * BLK;
+  constexpr int KW = BK < BLK ? BK : BLK;  // K width of one sub-block
+  constexpr int NH = BK / KW;              // sub-blocks per step
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  // A region: NH sub-blocks of [BM][KW]; B region: G x NH pieces of [BLK][KW]
+  // (NT) or [KW][BLK] (B read as [k][n]).
+  constexpr int RBA = KW * 2, RPWA = 1024 / RBA;
+  constexpr int RBB = BKN ? BLK * 2 : KW * 2, RPWB = 1024 / RBB;
+  constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int PIECE = BLK * KW * 2;
+  constexpr int AWW = A_BYTES / 4096, BWW = B_BYTES / 4096;  // windows per wave
+  constexpr int WPH = BM / RPWA;                             // A windows per sub-block
+  constexpr int WPP = PIECE / 1024;                          // B windows per piece
+  constexpr int DPS = AWW + BWW;                             // copies per wave per step
+  static_assert(A_BYTES % 4096 == 0 && B_BYTES % 4096 == 0, "windows");
+  static_assert(WPH % AWW == 0, "one sub-block per wave and step");
+  static_assert(WPP % BWW == 0 || BWW % WPP == 0, "piece split");
+  static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+  static_assert(NS >= 2 && NS <= 4 && DPS * (NS - 2) < 64, "stages");
+  // The lane swizzle of 8-chunk rows alternates between even and odd
+  // windows; every wave's first window of a sub-block or piece is even.
+  static_assert(AWW % 2 == 0 && BWW % 2 == 0 && WPP % 2 == 0, "window parity");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t st0[STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1[STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t st2[NS > 2 ? STAGE : 16];
+  __shared__ __attribute__((aligned(1024))) uint8_t st3[NS > 3 ? STAGE : 16];
+  // Each stage is a distinct LDS object so that the compiler's LDS-DMA
+  // dependency tracking can tell the stages apart.
+  auto stage = [&](auto j) __attribute__((always_inline)) -> uint8_t * {
+    constexpr int J = decltype(j)::value;
+    if constexpr (J == 0) return st0;
+    else if constexpr (J == 1) return st1;
+    else if constexpr (J == 2) return st2;
+    else return st3;
+  };
+
+  const bf16_t *__restrict__ A = (const bf16_t *)a.A;
+  const bf16_t *__restrict__ B = (const bf16_t *)a.B;
+  const bf16_t *__restrict__ L = (const bf16_t *)a.L;
+  const bf16_t *__restrict__ R = (const bf16_t *)a.R;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  const int ntn = a.ntiles;
+  const int mtiles = (int)((a.M + BM - 1) / BM);
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  constexpr int GM = 8;  // grouped order: GM m-tiles x a run of n-tiles
+  const int split = bid / (mtiles * ntn);
+  const int lin = bid % (mtiles * ntn);
+  const int first_m = (lin / (GM * ntn)) * GM;
+  const int gsz = min(GM, mtiles - first_m);
+  const int within = lin - first_m * ntn;
+  const int mt = first_m + within % gsz, nt = within / gsz;
+  const int64_t m0 = (int64_t)mt * BM;
+
+  int g_valid, nsteps, kcol_off = 0, blk_off = 0;
+  const NTTile *tile = DENSE ? nullptr : a.tiles + nt;
+  if constexpr (DENSE) {
+    g_valid = min(G, a.dense_nblk - nt * G);
+    nsteps = a.dense_nsteps;
+  } else {
+    g_valid = tile->g;
+    nsteps = tile->nsteps;
+    kcol_off = tile->kcol_off;
+    blk_off = tile->blk_off;
+  }
+  auto out_blk = [&](int g) __attribute__((always_inline)) -> int {
+    if constexpr (DENSE) return nt * G + min(g, g_valid - 1);
+    else return tile->out_blk[g];
+  };
+  const int vblocks = nsteps + a.nlr;
+  const int total_all = (vblocks * BLK + BK - 1) / BK;
+  const int per_split = (total_all + a.nsplit - 1) / a.nsplit;
+  const int s_begin = split * per_split;
+  const int total = max(0, min(total_all, s_begin + per_split) - s_begin);
+
+  const bf16_t *const a_base = A + m0 * a.lda;
+  const int64_t a_bytes = (a.M - m0) * a.lda * 2;
+  const bf16_t *const l_base = DENSE ? A : L + m0 * a.ldl;
+  const int64_t l_bytes = DENSE ? 0 : (a.M - m0) * a.ldl * 2;
+  constexpr int64_t BIG = 0x7fffffff;
+
+  // Sub-block h of step t: A base, byte range, row stride and column offset
+  // (bytes).  Kept block, low-rank block or zero padding, chosen by selects.
+  auto a_src = [&](int t, int h, const bf16_t *&base, int64_t &bytes, uint32_t &ldb,
+                   uint32_t &colb) __attribute__((always_inline)) {
+    const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
+    const bool sp = c < nsteps;
+    const int kcol = DENSE ? c : a.kcols[kcol_off + min(c, nsteps - 1)];
+    base = sp ? a_base : l_base;
+    bytes = sp ? a_bytes : (c < vblocks ? l_bytes : 0);
+    ldb = (uint32_t)((sp ? a.lda : a.ldl) * 2);
+    colb = (uint32_t)(((sp ? kcol : c - nsteps) * BLK + kk) * 2);
+  };
+  // Piece (g, h) of step t: B base at the piece, byte range, row stride.
+  auto b_src = [&](int t, int g, int h, const bf16_t *&base, int64_t &bytes,
+                   uint32_t &ldb) __attribute__((always_inline)) {
+    const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
+    const int64_t ob = out_blk(g);
+    if constexpr (DENSE) {
+      ldb = (uint32_t)(a.ldb * 2);
+      base = BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
+                 : B + (ob * BLK) * a.ldb + (int64_t)c * BLK + kk;
+      bytes = c < nsteps ? BIG : 0;
+    } else {
+      const bool sp = c < nsteps;
+      const int64_t blk = a.blks[blk_off + min(c, nsteps - 1) * G + g];
+      const int cr = c - nsteps;
+      const bf16_t *sp_base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
+      const bf16_t *lr_base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
+                                  : R + (ob * BLK) * a.ldr + (int64_t)cr * BLK + kk;
+      base = sp ? sp_base : lr_base;
+      bytes = (sp || c < vblocks) ? BIG : 0;
+      ldb = (uint32_t)(sp ? BLK * 2 : a.ldr * 2);
+    }
+  };
+
+  // Lane part of the copy addresses: row within the window and the
+  // swizzled chunk (two variants for 8-chunk rows: even / odd window).
+  constexpr int CPRA = RBA / 16, CPRB = RBB / 16;
+  const uint32_t a_row = (uint32_t)(lane / CPRA);
+  uint32_t a_c16[2];
+  {
+    const int pos = lane % CPRA;
+    a_c16[0] = (uint32_t)((pos ^ ((lane >> 4) & 3)) << 4);
+    a_c16[1] = (uint32_t)((pos ^ (((lane >> 4) & 3) | (CPRA == 8 ? 4 : 0))) << 4);
+  }
+  const uint32_t b_row = (uint32_t)(lane / CPRB);
+  uint32_t b_c16[2];
+  {
+    const int pos = lane % CPRB;
+    if constexpr (!BKN) {
+      b_c16[0] = (uint32_t)((pos ^ ((lane >> 4) & 3)) << 4);
+      b_c16[1] = (uint32_t)((pos ^ (((lane >> 4) & 3) | (CPRB == 8 ? 4 : 0))) << 4);
+    } else {
+      const int x = CPRB == 4 ? 0 : (CPRB == 8 ? (((lane >> 4) & 1) << 2) : ((lane >> 4) << 2));
+      b_c16[0] = b_c16[1] = (uint32_t)((pos ^ x) << 4);
+    }
+  }
+
+  // Issue this wave's copies of step t into stage buffer sb.
+  auto issue = [&](int t, uint8_t *sb) __attribute__((always_inline)) {
+    {
+      const int wa0 = w * AWW;
+      const int h = wa0 / WPH, wr0 = wa0 % WPH;
+      const bf16_t *base;
+      int64_t bytes;
+      uint32_t ldb, colb;
+      a_src(t, h, base, bytes, ldb, colb);
+      const rsrc_t r = make_rsrc(base, bytes);
+      const uint32_t vrow = a_row * ldb;
+      sfor<AWW>([&](auto i) __attribute__((always_inline)) {
+        const int wr = wr0 + i;
+        dma16(r, sb + (wa0 + i) * 1024, vrow + a_c16[i & 1],
+              (uint32_t)(wr * RPWA) * ldb + colb);
+      });
+    }
+    constexpr int PPW = BWW > WPP ? BWW / WPP : 1;  // pieces per wave
+    constexpr int WIN = BWW > WPP ? WPP : BWW;      // windows per piece and wave
+    sfor<PPW>([&](auto pi) __attribute__((always_inline)) {
+      const int wb0 = w * BWW + pi * WIN;
+      const int piece = wb0 / WPP, wi0 = wb0 % WPP;
+      const bf16_t *base;
+      int64_t bytes;
+      uint32_t ldb;
+      b_src(t, piece / NH, piece % NH, base, bytes, ldb);
+      const rsrc_t r = make_rsrc(base, bytes);
+      const uint32_t vrow = b_row * ldb;
+      sfor<WIN>([&](auto i) __attribute__((always_inline)) {
+        dma16(r, sb + A_BYTES + (wb0 + i) * 1024, vrow + b_c16[i & 1],
+              (uint32_t)((wi0 + i) * RPWB) * ldb);
+      });
+    });
+  };
+
+  f32x16 acc[TN][TM];
+  sfor<TN>([&](auto i) __attribute__((always_inline)) {
+    sfor<TM>([&](auto j) __attribute__((always_inline)) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    });
+  });
+
+  auto compute = [&](const uint8_t *sb) __attribute__((always_inline)) {
+    sfor<BK / 16>([&](auto ks) __attribute__((always_inline)) {
+      constexpr int h = (ks * 16) / KW, kq = ks % (KW / 16);
+      bf16x8 xf[TM], wf[TN];
+      sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+        xf[tm] = frag_rows<RBA>(sb + h * (BM * RBA), wm * WTM + tm * 32, kq, lane);
+      });
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        const int n0 = wn * WTN + tn * 32;
+        const int g = n0 / BLK, nl = n0 % BLK;
+        const uint8_t *piece = sb + A_BYTES + (g * NH + h) * PIECE;
+        if constexpr (BKN) wf[tn] = frag_kn<RBB>(piece, nl, kq, lane);
+        else wf[tn] = frag_rows<RBB>(piece, nl, kq, lane);
+      });
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+          acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[tn], xf[tm], acc[tn][tm], 0, 0, 0);
+        });
+      });
+    });
+  };
+
+  // Pipeline: steps 0 .. NS-2 in flight before the loop; at step t the
+  // copies of step t + NS - 1 go into the stage freed by step t - 1.
+  sfor<NS - 1>([&](auto j) __attribute__((always_inline)) {
+    if (j < total) issue(j, stage(j));
+  });
+  for (int t0 = 0; t0 < total; t0 += NS) {
+    bool done = false;
+    sfor<NS>([&](auto j) __attribute__((always_inline)) {
+      if (done) return;
+      const int t = t0 + j;
+      if (t >= total) {
+        done = true;
+        return;
+      }
+      // Copies of steps t+1 .. t+NS-2 that were issued may still be in
+      // flight; step t's must have landed.
+      const int ahead = min(NS - 2, total - 1 - t);
+      if constexpr (NS == 2) {
+        wait_vm<0>();
+      } else if constexpr (NS == 3) {
+        if (ahead >= 1) wait_vm<DPS>(); else wait_vm<0>();
+      } else {
+        if (ahead >= 2) wait_vm<2 * DPS>();
+        else if (ahead == 1) wait_vm<DPS>();
+        else wait_vm<0>();
+      }
+      barrier();
+      if (t + NS - 1 < total) issue(t + NS - 1, stage(std::integral_constant<int, (j + NS - 1) % NS>{}));
+      compute(stage(j));
+    });
+  }
+
+  // Epilogue.  Lane l of accumulator (tn, tm) holds token row tm*32 + l%32
+  // and, for q = 0..3, output columns tn*32 + q*8 + (l/32)*4 + 0..3.  Full
+  // 128-byte row segments store far faster than 8-byte pieces scattered
+  // over 32 rows, so each wave transposes its tile through LDS, 32 rows at a
+  // time (fp32, 16-byte chunks XOR-swizzled by row), and every lane then
+  // writes 8 consecutive columns of one row.  The staging area is the stage
+  // buffer no wave reads in the last step; it needs no barrier because each
+  // wave only touches its own slice and a wave's LDS accesses are ordered.
+  constexpr int SROW = WTN * 4, SCH = SROW / 16;  // staged row bytes, chunks
+  constexpr int SP = 32;                          // rows per pass
+  constexpr int LPR = WTN / 8, RPI = 64 / LPR;    // lanes per row, rows per store step
+  static_assert(4 * SP * SROW <= STAGE && (SCH & (SCH - 1)) == 0 && SP % RPI == 0, "staging");
+  const int rem = total % NS;
+  uint8_t *const stg = (rem == 0 ? st0 : rem == 1 ? st1 : rem == 2 ? st2 : st3) + w * (SP * SROW);
+  int ob[G];
+  sfor<G>([&](auto g) __attribute__((always_inline)) { ob[g] = out_blk(g); });
+  bf16_t *C = (bf16_t *)a.C;
+  const int jl = lane % LPR, rl = lane / LPR;
+  const int cn = wn * WTN + jl * 8;  // first of this lane's 8 columns in the tile
+  const int gcol = cn / BLK;
+  int obg = ob[0];
+  sfor<G>([&](auto gg) __attribute__((always_inline)) { if (gcol == gg) obg = ob[gg]; });
+  const int64_t col = (int64_t)obg * BLK + cn % BLK;
+  const bool col_ok = gcol < g_valid;
+  sfor<TM * (32 / SP)>([&](auto pass) __attribute__((always_inline)) {
+    constexpr int tm = pass / (32 / SP), half = pass % (32 / SP);
+    if ((lane & 31) / SP == half) {
+      const int r = (lane & 31) % SP;
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        sfor<4>([&](auto q) __attribute__((always_inline)) {
+          const int c = tn * 8 + q * 2 + (lane >> 5);
+          *(f32x4 *)(stg + r * SROW + ((c ^ (r & (SCH - 1))) << 4)) =
+              f32x4{acc[tn][tm][q * 4 + 0], acc[tn][tm][q * 4 + 1], acc[tn][tm][q * 4 + 2],
+                    acc[tn][tm][q * 4 + 3]};
+        });
+      });
+    }
+    sfor<SP / RPI>([&](auto it) __attribute__((always_inline)) {
+      const int r = it * RPI + rl;
+      const f32x4 lo = *(const f32x4 *)(stg + r * SROW + (((2 * jl) ^ (r & (SCH - 1))) << 4));
+      const f32x4 hi = *(const f32x4 *)(stg + r * SROW + (((2 * jl + 1) ^ (r & (SCH - 1))) << 4));
+      const int64_t gm = m0 + wm * WTM + tm * 32 + half * SP + r;
+      if (gm >= a.M || !col_ok) return;
+      float v[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      if (a.nsplit > 1) {
+        float *P = a.partials + ((int64_t)split * a.M + gm) * a.ldp + col;
+        *(f32x4 *)P = lo;
+        *(f32x4 *)(P + 4) = hi;
+        return;
+      }
+      const int64_t o = gm * a.ldc + col;
+      if constexpr (EPI == 1) {  // forward GELU: keep the pre-activation
+        *(u32x4 *)((bf16_t *)a.C2 + o) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                               pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = gelu(v[e]);
+      } else if constexpr (EPI == 2) {  // backward GELU: scale by gelu'(pre-activation)
+        const u32x4 x = *(const u32x4 *)((const bf16_t *)a.aux + o);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[2 * e] *= gelu_grad(__uint_as_float(x[e] << 16));
+          v[2 * e + 1] *= gelu_grad(__uint_as_float(x[e] & 0xffff0000u));
+        }
+      }
+      *(u32x4 *)(C + o) = u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+    });
+  });
+}
+
+template <int BLK, int G, bool BKN, int BM, int BK, int NS, bool DENSE, int OCC>
+hipError_t ntd_go(const NTArgs &a, hipStream_t s) {
+  const int64_t mtiles = (a.M + BM - 1) / BM;
+  const int64_t grid = mtiles * a.ntiles * std::max(1, a.nsplit);
+  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
+  if (!DENSE && a.epi == 1) {
+    if constexpr (!DENSE) {
+      if constexpr (BKN)
+        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, DENSE, 2, OCC>), dim3((unsigned)grid),
+                           dim3(256), 0, s, a);
+      else
+        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, DENSE, 1, OCC>), dim3((unsigned)grid),
+                           dim3(256), 0, s, a);
+    }
+  } else {
+    hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, DENSE, 0, OCC>), dim3((unsigned)grid),
+                       dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+// Tile configurations (output tiles are 128 columns wide): 0 = 128 x 128,
+// K-steps of 64, two stages, two workgroups per CU.
+template <int BLK, bool BKN, bool DENSE>
+hipError_t ntd_cfg(int cfg, const NTArgs &a, hipStream_t s) {
+  constexpr int G = 128 / BLK;
+  if (cfg == 0) return ntd_go<BLK, G, BKN, 128, 64, 2, DENSE, 2>(a, s);
+  return hipErrorInvalidValue;
+}
+
+template <int BLK, bool BKN>
+hipError_t ntd_g(int G, int cfg, bool dense, const NTArgs &a, hipStream_t s) {
+  if (G != 128 / BLK) return hipErrorInvalidValue;
+  return dense ? ntd_cfg<BLK, BKN, true>(cfg, a, s) : ntd_cfg<BLK, BKN, false>(cfg, a, s);
+}
+
+}  // namespace
+
+hipError_t launch_ntd(int blk, int G, bool b_kn, int cfg, const NTArgs &a, hipStream_t s) {
+  const bool dense = a.dense != 0;
+  switch (blk) {
+    case 32: return b_kn ? ntd_g<32, true>(G, cfg, dense, a, s) : ntd_g<32, false>(G, cfg, dense, a, s);
+    case 64: return b_kn ? ntd_g<64, true>(G, cfg, dense, a, s) : ntd_g<64, false>(G, cfg, dense, a, s);
+    case 128: return b_kn ? ntd_g<128, true>(G, cfg, dense, a, s) : ntd_g<128, false>(G, cfg, dense, a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace pf

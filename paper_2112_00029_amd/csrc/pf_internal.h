@@ -107,6 +107,9 @@ struct AttnArgs {
 // M-tile (tokens per workgroup): 128, or 64 for the skinny rank-r products.
 hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a,
                      hipStream_t s);
+// bf16 NT family with direct global -> LDS operand copies (gemm_dma.hip).
+// G * blk is 128; cfg 0 = 128-token tiles (two workgroups per CU).
+hipError_t launch_ntd(int blk, int G, bool b_kn, int cfg, const NTArgs &a, hipStream_t s);
 // Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
 hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
                               void *C, int64_t ldc, hipStream_t s);
