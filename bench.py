@@ -13,9 +13,12 @@ Prints ONE JSON line.  `value` is nonzero-block TFLOP/s of the step (only the
 kept b x b blocks' FLOPs of the three block-sparse products, or of the six
 attention block products), the metric of the workload table.  The same line
 carries the fraction of the bf16 MFMA peak, the speedup over the dense layer
-of the same shape run with the library's own dense MFMA GEMM, per-call times
-measured with HIP events on the compute stream, a roofline entry for the
-dominant call, and the CPU oracle timed on a bounded sample of the workload.
+of the same shape run with the library's own dense MFMA GEMM, and the CPU
+oracle timed on a bounded sample of the workload.  The timed region holds
+only the steps between two events; a second region repeats the steps with
+events between the calls and the library's per-launch events (kernel timing
+hook), which give per_call_ms, per_kernel and the roofline entry of the
+dominant kernel.
 """
 from __future__ import annotations
 
@@ -47,6 +50,8 @@ def parse():
     p.add_argument("--workload", default="mlp_fc1_768x3072", choices=sorted(synth.WORKLOADS))
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true")
+    p.add_argument("--no-kernel-timing", action="store_true",
+                   help="skip the per-kernel HIP events of the second region (no roofline entry)")
     p.add_argument("--calls-only", default="", help="comma list of calls to loop (profiling aid)")
     return p.parse_args()
 
@@ -127,19 +132,11 @@ class Linear:
         dense = 3 * 2 * wl.T * wl.N * wl.K
         return sparse, lowrank, dense
 
-    def call_work(self, name):
-        """(flops, algorithmic bytes) of one call: each operand read once,
-        each output written once."""
+    def kernel_work(self):
+        """Algorithmic (flops, bytes) per step of each kernel class: every
+        operand read once, every output written once."""
         wl, e = self.wl, (2 if self.dtype == "bf16" else 4)
-        T, K, N, r, w = wl.T, wl.K, wl.N, wl.r, self.nnzb * wl.b * wl.b
-        fl = 2 * T * w + 2 * T * r * (K + N)
-        if name == "fwd":
-            by = T * K + w + N * r + r * K + T * N + T * r
-        elif name == "bwd_data":
-            by = T * N + w + N * r + r * K + T * K + T * r
-        else:
-            by = T * N + T * K + 2 * T * r + w + N * r + r * K
-        return fl, by * e
+        return _layer_work(wl.T, wl.K, wl.N, wl.r, self.nnzb * wl.b * wl.b, e)
 
     def dense_setup(self):
         torch, wl = self.torch, self.wl
@@ -245,20 +242,17 @@ class MlpPair(Linear):
         dense = 2 * 3 * 2 * wl.T * wl.N * wl.K
         return sparse, lowrank, dense
 
-    def call_work(self, name):
+    def kernel_work(self):
         wl = self.wl
-        T, r = wl.T, wl.r
-        K, N, nz = (wl.K, wl.N, self.nnzb1) if name.endswith("1") else (wl.N, wl.K, self.nnzb2)
-        w = nz * wl.b * wl.b
-        fl = 2 * T * w + 2 * T * r * (K + N)
-        gelu = T * wl.N  # the extra pre-activation tensor
-        if name.startswith("fwd"):
-            by = T * K + w + N * r + r * K + T * N + T * r + (gelu if name == "fwd1" else 0)
-        elif name.startswith("bwd_data"):
-            by = T * N + w + N * r + r * K + T * K + T * r + (gelu if name == "bwd_data2" else 0)
-        else:
-            by = T * N + T * K + 2 * T * r + w + N * r + r * K
-        return fl, 2 * by
+        w1 = _layer_work(wl.T, wl.K, wl.N, wl.r, self.nnzb1 * wl.b * wl.b, 2)
+        w2 = _layer_work(wl.T, wl.N, wl.K, wl.r, self.nnzb2 * wl.b * wl.b, 2)
+        out = {k: (w1[k][0] + w2[k][0], w1[k][1] + w2[k][1]) for k in w1}
+        # GELU: the forward of layer 1 also writes the pre-activation, the
+        # backward-data of layer 2 also reads it.
+        gelu = 2 * wl.T * wl.N
+        out["spmm_fwd"] = (out["spmm_fwd"][0], out["spmm_fwd"][1] + gelu)
+        out["spmm_bwd_data"] = (out["spmm_bwd_data"][0], out["spmm_bwd_data"][1] + gelu)
+        return out
 
     def dense_setup(self):
         torch, wl = self.torch, self.wl
@@ -350,14 +344,17 @@ class Attention:
         per = 2 * wl.b * wl.b * wl.d * self.nnzb * wl.B * wl.H
         return 6 * per, 0, 6 * 2 * wl.S * wl.S * wl.d * wl.B * wl.H
 
-    def call_work(self, name):
+    def kernel_work(self):
+        """Useful flops: two b x b x d block products per kept block in the
+        forward, four in the backward (dP and dQ in the dQ kernel, dV and dK
+        in the dK/dV kernel); recomputed scores are not counted."""
         wl = self.wl
         per = 2 * wl.b * wl.b * wl.d * self.nnzb * wl.B * wl.H
         t = wl.B * wl.H * wl.S * wl.d * 2
         rows = wl.B * wl.H * wl.S * 4
-        if name == "attn_fwd":
-            return 2 * per, 4 * t + rows
-        return 4 * per, 7 * t + rows
+        return {"attn_fwd": (2 * per, 4 * t + rows),            # Q, K, V -> O, lse
+                "attn_bwd_dq": (2 * per, 6 * t + 2 * rows),     # Q, K, V, O, dO, lse -> dQ, delta
+                "attn_bwd_dkv": (2 * per, 6 * t + 2 * rows)}    # Q, K, V, dO, lse, delta -> dK, dV
 
     def dense_setup(self):
         torch, wl = self.torch, self.wl
@@ -391,6 +388,17 @@ class Attention:
                 break
         fl = 6 * 2 * wl.b * wl.b * wl.d * int(M.sum()) * reps
         return fl / el / 1e12, f"oracle fwd+bwd (fp64, dense masked) on {reps} heads of {wl.B * wl.H}, {el:.1f} s"
+
+
+def _layer_work(T, K, N, r, w, e):
+    """(flops, bytes) per step of the kernel classes of one K -> N layer with
+    w kept weight elements, r-rank factors and e-byte elements."""
+    return {
+        "spmm_fwd": (2 * T * (w + r * N), e * (T * K + w + T * r + N * r + T * N)),
+        "spmm_bwd_data": (2 * T * (w + r * K), e * (T * N + w + T * r + r * K + T * K)),
+        "sddmm": (2 * T * (w + N * r + r * K), e * (T * N + T * K + 2 * T * r + w + N * r + r * K)),
+        "skinny": (2 * T * r * (K + N), e * (T * K + r * K + T * N + N * r + 2 * T * r)),
+    }
 
 
 def blas_threads():
@@ -434,26 +442,43 @@ def main():
         R.dense_setup()
         base_call = R.call
         R.call = lambda c: R.dense_step() if c == "dense" else base_call(c)
-    # warmup, then the timed region with events between calls
+    # Warmup, then the timed region: K whole steps bracketed by two events
+    # only (nothing else recorded in between), which gives ms_per_step.
     for _ in range(args.warmup):
         for c in calls:
             R.call(c)
     torch.cuda.synchronize()
-    timer = Timer(torch, calls)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
+    for _ in range(args.steps):
+        for c in calls:
+            R.call(c)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+
+    # Kernel-timing region: the same K steps again with events between the
+    # calls and the library's per-launch events (pf_timing_begin); event
+    # records add gaps between kernels, so this region only supplies the
+    # per-call and per-kernel durations.
+    timer = Timer(torch, calls)
+    kernel_timing = not args.no_kernel_timing
+    if kernel_timing:
+        pf.pf_timing_begin(args.steps * 8)
     for _ in range(args.steps):
         ev = timer.step_events()
         for i, c in enumerate(calls):
             ev[i].record()
             R.call(c)
         ev[-1].record()
-    end.record()
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
     per_call = timer.per_call_ms()
+    kt = pf.pf_timing_end() if kernel_timing else {}
+    per_kernel = {c: {"launches_per_step": n / args.steps, "avg_ms": avg,
+                      "ms_per_step": n * avg / args.steps} for c, (n, avg) in kt.items() if n}
     if args.calls_only:
-        print(json.dumps({"calls_only": calls, "ms_per_step": ms, "per_call_ms": per_call}))
+        print(json.dumps({"calls_only": calls, "ms_per_step": ms, "per_call_ms": per_call,
+                          "per_kernel": per_kernel}))
         return
 
     sparse, lowrank, dense_fl = R.flops()
@@ -467,19 +492,33 @@ def main():
         if wl.kind != "attention":
             torch_ms = timed(torch, R.torch_dense_step, max(5, args.steps // 4), 3)
 
-    # roofline for the dominant call
-    dom = max(per_call, key=per_call.get)
-    fl, by = R.call_work(dom)
-    t = per_call[dom] * 1e-3
-    ai = fl / by
-    if R.dtype == "bf16" and ai >= RIDGE_BF16:
-        roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
-    roof.update({"call": dom, "ms": per_call[dom], "algorithmic_bytes": by, "flops": fl,
-                 "flop_per_byte": ai})
+    # Roofline of the dominant kernel: the kernel class with the most time
+    # per step, its algorithmic work per launch over its mean launch time
+    # (HIP events recorded by the library around each launch, in the
+    # kernel-timing region, on the stream the kernel ran on).
+    roof = None
+    work = R.kernel_work()
+    cand = {c: v for c, v in per_kernel.items() if c in work}
+    if cand:
+        dom = max(cand, key=lambda c: cand[c]["ms_per_step"])
+        lps, t = cand[dom]["launches_per_step"], cand[dom]["avg_ms"] * 1e-3
+        fl, by = work[dom][0] / lps, work[dom][1] / lps
+        ai = fl / by
+        if R.dtype == "bf16" and ai >= RIDGE_BF16:
+            roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+        elif R.dtype == "bf16":
+            roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        else:  # fp32: MFMA fp32 peak vs HBM by the same ridge rule
+            if ai >= PEAK_FP32_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+                roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
+            else:
+                roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+        roof["frac"] = roof["achieved"] / roof["peak"]
+        roof["traffic"] = None
+        roof.update({"kernel": dom, "avg_launch_ms": cand[dom]["avg_ms"], "launches_per_step": lps,
+                     "algorithmic_bytes_per_launch": by, "flops_per_launch": fl,
+                     "flop_per_byte": ai,
+                     "tflops_per_launch": fl / t / 1e12, "gbs_per_launch": by / t / 1e9})
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -503,6 +542,7 @@ def main():
         "dense_tflops": (dense_fl / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
         "torch_dense_ms_per_step": torch_ms,
         "per_call_ms": per_call,
+        "per_kernel": per_kernel,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

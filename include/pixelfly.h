@@ -250,6 +250,38 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N,
 size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M,
                                 int64_t N, int64_t K);
 
+/*
+ * Kernel timing (a measurement aid, not part of the compute path).
+ *
+ * Every kernel the library launches belongs to one class below.  After
+ * pf_timing_begin(n), the library records a HIP event pair on the launch
+ * stream immediately before and after each of the next n launches of every
+ * class (the events are created here, so the compute calls still allocate
+ * nothing).  pf_timing_end waits for the recorded events, writes for each
+ * class the number of timed launches and their mean duration in ms into
+ * counts[PF_KERNEL_COUNT] / avg_ms[PF_KERNEL_COUNT] (either may be NULL),
+ * and disarms the hook.  Recording is process-wide; timing calls must not
+ * overlap compute calls issued from other threads.
+ * Errors: INVALID_ARG (n < 1 or n > 2^20), STATE (end without begin),
+ * NOMEM, HIP.
+ */
+typedef enum {
+  PF_KERNEL_SPMM_FWD = 0,       /* forward block-sparse product (+ low-rank) */
+  PF_KERNEL_SPMM_BWD_DATA = 1,  /* backward-data block-sparse product (+ low-rank) */
+  PF_KERNEL_SDDMM = 2,          /* weight gradient on the mask, dU, dV */
+  PF_KERNEL_SKINNY = 3,         /* rank-r products T_lr = X V^T, S = dY U */
+  PF_KERNEL_REDUCE = 4,         /* sums of split partial results */
+  PF_KERNEL_GELU_BWD = 5,       /* standalone GELU backward */
+  PF_KERNEL_ATTN_FWD = 6,
+  PF_KERNEL_ATTN_BWD_DQ = 7,    /* dQ (and the row terms delta) */
+  PF_KERNEL_ATTN_BWD_DKV = 8,   /* dK, dV */
+  PF_KERNEL_DENSE = 9,          /* dense comparator GEMM */
+  PF_KERNEL_COUNT = 10
+} pf_kernel_class;
+
+pf_status pf_timing_begin(int32_t max_launches_per_class);
+pf_status pf_timing_end(int32_t *counts, double *avg_ms);
+
 /* Static text of a status code. */
 const char *pf_status_string(pf_status s);
 

@@ -418,12 +418,16 @@ hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bwd(const AttnArgs &a, hipStream_t s) {
+hipError_t launch_attn_bwd_dq(const AttnArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.BH * a.nbq;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(attn_bwd_dq_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_bwd_dkv(const AttnArgs &a, hipStream_t s) {
+  const int64_t grid = (int64_t)a.BH * a.nbq;
+  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL(attn_bwd_dkv_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }

@@ -3,10 +3,13 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "layout.h"
 #include "pf_internal.h"
@@ -22,6 +25,48 @@ pf_status fail(pf_status s, const std::string &msg) {
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15) == 0; }
+
+// Kernel timing hook (pf_timing_begin / pf_timing_end): per kernel class,
+// event pairs recorded around the next `cap` launches.
+struct KernelTimer {
+  std::mutex mu;
+  std::atomic<int> armed{0};
+  int cap = 0;
+  std::vector<hipEvent_t> ev[PF_KERNEL_COUNT];  // 2 * cap each: start, end
+  int n[PF_KERNEL_COUNT] = {};
+
+  void release() {
+    for (auto &v : ev) {
+      for (hipEvent_t e : v)
+        if (e) (void)hipEventDestroy(e);
+      v.clear();
+    }
+    std::fill(n, n + PF_KERNEL_COUNT, 0);
+    cap = 0;
+  }
+};
+KernelTimer g_kt;
+
+// Scope around one kernel launch: records the start event on entry and the
+// end event on exit when the hook is armed and the class has room.
+class Timed {
+ public:
+  Timed(pf_kernel_class k, hipStream_t s) : k_(k), s_(s) {
+    if (!g_kt.armed.load(std::memory_order_acquire) || g_kt.n[k] >= g_kt.cap) return;
+    on_ = hipEventRecord(g_kt.ev[k][2 * g_kt.n[k]], s) == hipSuccess;
+  }
+  ~Timed() {
+    if (!on_) return;
+    if (hipEventRecord(g_kt.ev[k_][2 * g_kt.n[k_] + 1], s_) == hipSuccess) g_kt.n[k_]++;
+  }
+  Timed(const Timed &) = delete;
+  Timed &operator=(const Timed &) = delete;
+
+ private:
+  pf_kernel_class k_;
+  hipStream_t s_;
+  bool on_ = false;
+};
 
 pf_status need_ptr(const void *p, const char *name) {
   if (!p) return fail(PF_ERR_INVALID_ARG, std::string(name) + " is NULL");
@@ -74,17 +119,18 @@ int pow2_group(int gmax, int n) {
 #ifndef PF_NTD
 #define PF_NTD 1
 #endif
-hipError_t nt_launch(int dtype, int blk, int G, bool b_kn, int bm, const pf::NTArgs &a,
-                     hipStream_t s) {
+hipError_t nt_launch(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm,
+                     const pf::NTArgs &a, hipStream_t s) {
+  Timed t(kc, s);
   if (PF_NTD && dtype == 0 && bm == 128 && G * blk == 128) return pf::launch_ntd(blk, G, b_kn, 0, a, s);
   return pf::launch_nt(dtype, blk, G, b_kn, bm, a, s);
 }
 
 // Dense-mode NT launch: C[M x nblk*b] = A[M x nsteps*b] . B^T (B [n][k]) or
 // A . B (B [k][n]), with M-tile bm; split over K when ws gives room.
-pf_status dense_nt(int dtype, int blk, bool b_kn, int bm, int64_t M, const void *A, int64_t lda,
-                   const void *B, int64_t ldb, int nsteps, int nblk, void *C, int64_t ldc,
-                   int nsplit, float *ws, hipStream_t s, const char *what) {
+pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, bool b_kn, int bm, int64_t M,
+                   const void *A, int64_t lda, const void *B, int64_t ldb, int nsteps, int nblk,
+                   void *C, int64_t ldc, int nsplit, float *ws, hipStream_t s, const char *what) {
   pf::NTArgs a{};
   a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
   a.dense = 1; a.dense_nsteps = nsteps; a.dense_nblk = nblk;
@@ -94,8 +140,9 @@ pf_status dense_nt(int dtype, int blk, bool b_kn, int bm, int64_t M, const void 
   a.nsplit = nsplit;
   a.partials = ws;
   a.ldp = (int64_t)nblk * blk;
-  pf_status st = hip_status(nt_launch(dtype, blk, G, b_kn, bm, a, s), what);
+  pf_status st = hip_status(nt_launch(kc, dtype, blk, G, b_kn, bm, a, s), what);
   if (st != PF_OK || nsplit <= 1) return st;
+  Timed t(PF_KERNEL_REDUCE, s);
   return hip_status(pf::launch_reduce_rows(dtype, nsplit, ws, M, (int64_t)nblk * blk, C, ldc, s), what);
 }
 
@@ -184,6 +231,53 @@ const char *pf_status_string(pf_status s) {
 }
 
 const char *pf_last_error(void) { return g_err.c_str(); }
+
+pf_status pf_timing_begin(int32_t max_launches_per_class) {
+  if (max_launches_per_class < 1 || max_launches_per_class > (1 << 20))
+    return fail(PF_ERR_INVALID_ARG, "max_launches_per_class must be in [1, 2^20]");
+  std::lock_guard<std::mutex> lk(g_kt.mu);
+  g_kt.armed.store(0, std::memory_order_release);
+  g_kt.release();
+  try {
+    for (auto &v : g_kt.ev) v.assign(2 * (size_t)max_launches_per_class, nullptr);
+  } catch (const std::bad_alloc &) {
+    g_kt.release();
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  }
+  for (auto &v : g_kt.ev)
+    for (hipEvent_t &e : v)
+      if (hipEventCreate(&e) != hipSuccess) {
+        e = nullptr;
+        g_kt.release();
+        return fail(PF_ERR_HIP, "hipEventCreate failed");
+      }
+  g_kt.cap = max_launches_per_class;
+  g_kt.armed.store(1, std::memory_order_release);
+  return PF_OK;
+}
+
+pf_status pf_timing_end(int32_t *counts, double *avg_ms) {
+  std::lock_guard<std::mutex> lk(g_kt.mu);
+  if (!g_kt.armed.load(std::memory_order_acquire)) return fail(PF_ERR_STATE, "timing not begun");
+  g_kt.armed.store(0, std::memory_order_release);
+  pf_status st = PF_OK;
+  for (int k = 0; k < PF_KERNEL_COUNT; ++k) {
+    double sum = 0;
+    for (int i = 0; i < g_kt.n[k]; ++i) {
+      float ms = 0;
+      if (hipEventSynchronize(g_kt.ev[k][2 * i + 1]) != hipSuccess ||
+          hipEventElapsedTime(&ms, g_kt.ev[k][2 * i], g_kt.ev[k][2 * i + 1]) != hipSuccess) {
+        st = fail(PF_ERR_HIP, "reading timing events failed");
+        break;
+      }
+      sum += ms;
+    }
+    if (counts) counts[k] = g_kt.n[k];
+    if (avg_ms) avg_ms[k] = g_kt.n[k] ? sum / g_kt.n[k] : 0.0;
+  }
+  g_kt.release();
+  return st;
+}
 
 pf_status pf_layout_create(int64_t n_out, int64_t n_in, int32_t b, int32_t max_stride,
                            pf_layout **out) {
@@ -391,7 +485,8 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(dt, b, false, 64, T, X, L->n_in, V, L->n_in, L->nb_in, r / b, T_lr, r, sp.nsplit,
+    st = dense_nt(PF_KERNEL_SKINNY, dt, b, false, 64, T, X, L->n_in, V, L->n_in, L->nb_in, r / b,
+                  T_lr, r, sp.nsplit,
                   (float *)workspace, s, "T_lr kernel");
     if (st != PF_OK) return st;
   }
@@ -406,7 +501,7 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   a.tiles = L->d_fwd_tiles; a.ntiles = (int)L->fwd_tiles.size();
   a.kcols = L->d_kcols_fwd; a.blks = L->d_blks_fwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(dt, b, L->G_fwd, false, 128, a, s), "forward kernel");
+  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, L->G_fwd, false, 128, a, s), "forward kernel");
 }
 
 pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -431,7 +526,8 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // S = dY U: dense over N with U read as [k][n].
-    st = dense_nt(dt, b, true, 64, T, dY, L->n_out, U, r, L->nb_out, r / b, S, r, sp.nsplit,
+    st = dense_nt(PF_KERNEL_SKINNY, dt, b, true, 64, T, dY, L->n_out, U, r, L->nb_out, r / b, S,
+                  r, sp.nsplit,
                   (float *)workspace, s, "S kernel");
     if (st != PF_OK) return st;
   }
@@ -446,7 +542,8 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.tiles = L->d_bwd_tiles; a.ntiles = (int)L->bwd_tiles.size();
   a.kcols = L->d_kcols_bwd; a.blks = L->d_blks_bwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(dt, b, L->G_bwd, true, 128, a, s), "backward-data kernel");
+  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, L->G_bwd, true, 128, a, s),
+                    "backward-data kernel");
 }
 
 pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -476,7 +573,15 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   a.nsplit = p.nsplit;
   a.chunk = p.chunk;
   a.partials = (float *)workspace;
-  return hip_status(pf::launch_tn((int)dtype, L->b, a, (hipStream_t)stream), "weight-gradient kernel");
+  hipStream_t s = (hipStream_t)stream;
+  {
+    Timed t(PF_KERNEL_SDDMM, s);
+    if ((st = hip_status(pf::launch_tn((int)dtype, L->b, a, s), "weight-gradient kernel")) != PF_OK)
+      return st;
+  }
+  if (a.nsplit <= 1) return PF_OK;
+  Timed t(PF_KERNEL_REDUCE, s);
+  return hip_status(pf::launch_tn_reduce((int)dtype, L->b, a, s), "weight-gradient reduction");
 }
 
 pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_pre, void *dH_pre,
@@ -488,6 +593,7 @@ pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_p
   if ((st = need_ptr(dH, "dH")) != PF_OK || (st = need_ptr(H_pre, "H_pre")) != PF_OK ||
       (st = need_ptr(dH_pre, "dH_pre")) != PF_OK)
     return st;
+  Timed t(PF_KERNEL_GELU_BWD, (hipStream_t)stream);
   return hip_status(pf::launch_gelu_bwd((int)dtype, n, dH, H_pre, dH_pre, (hipStream_t)stream),
                     "gelu backward kernel");
 }
@@ -517,6 +623,7 @@ pf_status pf_attn_fwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
   a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
+  Timed t(PF_KERNEL_ATTN_FWD, (hipStream_t)stream);
   return hip_status(pf::launch_attn_fwd(a, (hipStream_t)stream), "attention forward kernel");
 }
 
@@ -548,7 +655,13 @@ pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
   a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
-  return hip_status(pf::launch_attn_bwd(a, (hipStream_t)stream), "attention backward kernels");
+  hipStream_t s = (hipStream_t)stream;
+  {
+    Timed t(PF_KERNEL_ATTN_BWD_DQ, s);
+    if ((st = hip_status(pf::launch_attn_bwd_dq(a, s), "attention dQ kernel")) != PF_OK) return st;
+  }
+  Timed t(PF_KERNEL_ATTN_BWD_DKV, s);
+  return hip_status(pf::launch_attn_bwd_dkv(a, s), "attention dK/dV kernel");
 }
 
 size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K) {
@@ -575,11 +688,11 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
   const int dt = (int)dtype;
   switch (op) {
     case PF_OP_NT:
-      return dense_nt(dt, 64, false, 128, M, A, K, B, K, (int)(K / 64), (int)(N / 64), C, N, 1,
-                      nullptr, s, "dense NT");
+      return dense_nt(PF_KERNEL_DENSE, dt, 64, false, 128, M, A, K, B, K, (int)(K / 64),
+                      (int)(N / 64), C, N, 1, nullptr, s, "dense NT");
     case PF_OP_NN:
-      return dense_nt(dt, 64, true, 128, M, A, K, B, N, (int)(K / 64), (int)(N / 64), C, N, 1,
-                      nullptr, s, "dense NN");
+      return dense_nt(PF_KERNEL_DENSE, dt, 64, true, 128, M, A, K, B, N, (int)(K / 64),
+                      (int)(N / 64), C, N, 1, nullptr, s, "dense NN");
     case PF_OP_TN: {
       pf::TNArgs a{};
       a.n_items = 0;
@@ -591,7 +704,13 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
       a.nsplit = p.nsplit;
       a.chunk = p.chunk;
       a.partials = (float *)workspace;
-      return hip_status(pf::launch_tn(dt, 64, a, s), "dense TN");
+      {
+        Timed t(PF_KERNEL_DENSE, s);
+        if ((st = hip_status(pf::launch_tn(dt, 64, a, s), "dense TN")) != PF_OK) return st;
+      }
+      if (a.nsplit <= 1) return PF_OK;
+      Timed t(PF_KERNEL_REDUCE, s);
+      return hip_status(pf::launch_tn_reduce(dt, 64, a, s), "dense TN reduction");
     }
   }
   return fail(PF_ERR_INVALID_ARG, "bad op");

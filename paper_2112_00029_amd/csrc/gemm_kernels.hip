@@ -857,12 +857,16 @@ int tn_items_total(const TNArgs &a, int blk) {
 
 template <typename T, int BLK>
 static hipError_t tn_go(const TNArgs &a, hipStream_t s) {
-  const int64_t items = tn_items_total(a, BLK);
-  const int64_t grid = items * a.nsplit;
+  const int64_t grid = (int64_t)tn_items_total(a, BLK) * a.nsplit;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((tn_kernel<T, BLK>), dim3((unsigned)grid), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nsplit <= 1) return e;
+  return hipGetLastError();
+}
+
+template <typename T, int BLK>
+static hipError_t tn_reduce_go(const TNArgs &a, hipStream_t s) {
+  const int64_t items = tn_items_total(a, BLK);
+  if (items <= 0 || items * 16 > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((tn_reduce_kernel<T, BLK>), dim3((unsigned)(items * 16)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -879,6 +883,23 @@ hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s) {
       case 32: return tn_go<float, 32>(a, s);
       case 64: return tn_go<float, 64>(a, s);
       case 128: return tn_go<float, 128>(a, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s) {
+  if (dtype == 0) {
+    switch (blk) {
+      case 32: return tn_reduce_go<bf16_t, 32>(a, s);
+      case 64: return tn_reduce_go<bf16_t, 64>(a, s);
+      case 128: return tn_reduce_go<bf16_t, 128>(a, s);
+    }
+  } else {
+    switch (blk) {
+      case 32: return tn_reduce_go<float, 32>(a, s);
+      case 64: return tn_reduce_go<float, 64>(a, s);
+      case 128: return tn_reduce_go<float, 128>(a, s);
     }
   }
   return hipErrorInvalidValue;

@@ -113,12 +113,14 @@ hipError_t launch_ntd(int blk, int G, bool b_kn, int cfg, const NTArgs &a, hipSt
 // Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
 hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
                               void *C, int64_t ldc, hipStream_t s);
-// The TN kernel; with a.nsplit > 1 it also launches its reduce pass.
+// The TN kernel, and (a.nsplit > 1) the pass that sums its split partials.
 hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
+hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s);
 int tn_items_total(const TNArgs &a, int blk);
 hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
                            const void *Hpre, void *out, hipStream_t s);
 hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s);
-hipError_t launch_attn_bwd(const AttnArgs &a, hipStream_t s);
+hipError_t launch_attn_bwd_dq(const AttnArgs &a, hipStream_t s);
+hipError_t launch_attn_bwd_dkv(const AttnArgs &a, hipStream_t s);
 
 }  // namespace pf

@@ -25,6 +25,10 @@ PF_ERR_WORKSPACE, PF_ERR_HIP, PF_ERR_NOMEM, PF_ERR_STATE = -3, -4, -5, -6
 PF_BF16, PF_FP32 = 0, 1
 PF_EPI_NONE, PF_EPI_GELU = 0, 1
 PF_OP_NT, PF_OP_NN, PF_OP_TN = 0, 1, 2
+# Kernel classes of the timing hook (pf_kernel_class).
+KERNEL_CLASSES = ["spmm_fwd", "spmm_bwd_data", "sddmm", "skinny", "reduce", "gelu_bwd",
+                  "attn_fwd", "attn_bwd_dq", "attn_bwd_dkv", "dense"]
+PF_KERNEL_COUNT = len(KERNEL_CLASSES)
 
 
 class PixelflyError(RuntimeError):
@@ -80,6 +84,8 @@ _SIGS = {
     "pf_attn_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "pf_dense_gemm": (_i32, [_i32, _i32, _i64, _i64, _i64, _p, _p, _p, _p, _sz, _p]),
     "pf_dense_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64]),
+    "pf_timing_begin": (_i32, [_i32]),
+    "pf_timing_end": (_i32, [ctypes.POINTER(_i32), ctypes.POINTER(ctypes.c_double)]),
     "pf_status_string": (ctypes.c_char_p, [_i32]),
     "pf_last_error": (ctypes.c_char_p, []),
 }
@@ -255,6 +261,18 @@ def pf_dense_gemm(dtype, op, M, N, K, A, B, C, workspace=None, ws_bytes=0, strea
 
 def pf_dense_workspace_bytes(dtype, op, M, N, K) -> int:
     return int(_lib.pf_dense_workspace_bytes(_dt(dtype), op, M, N, K))
+
+
+def pf_timing_begin(max_launches_per_class: int) -> None:
+    _check(_lib.pf_timing_begin(max_launches_per_class))
+
+
+def pf_timing_end() -> dict:
+    """{class name: (timed launches, mean duration in ms)}."""
+    counts = (_i32 * PF_KERNEL_COUNT)()
+    avg = (ctypes.c_double * PF_KERNEL_COUNT)()
+    _check(_lib.pf_timing_end(counts, avg))
+    return {n: (int(counts[i]), float(avg[i])) for i, n in enumerate(KERNEL_CLASSES)}
 
 
 def pf_status_string(status: int) -> str:

@@ -172,3 +172,13 @@ def test_layout_from_mask():
             assert pf.pf_layout_plan_get(L)["tn_kept"] == M.sum()
     with pytest.raises(pf.PixelflyError):
         pf.pf_layout_create_from_mask(2, 2, 32, np.array([[1, 0], [0, 0]]))
+
+
+def test_timing_hook_errors_before_any_hip_call():
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_timing_begin(0)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_timing_end()
+    assert e.value.status == pf.PF_ERR_STATE
+    assert len(pf.KERNEL_CLASSES) == pf.PF_KERNEL_COUNT == 10
