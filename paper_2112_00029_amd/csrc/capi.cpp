@@ -154,19 +154,34 @@ pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, bool b_kn, int bm, in
 #define PF_MAX_SPLIT 4
 #endif
 
-// Split of the skinny rank-r product (M = T tokens, K = kblocks * b,
-// r / b output blocks, M-tile 64, 128-column tiles, K-steps of 64 or 32).
+// Plan of a skinny rank-r product (M = T tokens, K = kblocks * b, r / b
+// output blocks): token tile bm and the split of the K range over
+// workgroups.  bf16 runs on the direct-to-LDS kernel with 128 x 128 tiles
+// and K-steps of 64; it splits until about 512 workgroups are in flight but
+// keeps at least 6 steps per split (the fp32 partials and their reduction
+// cost more than they save below that).  fp32 uses 64-token tiles, K-steps
+// of 32 and at most PF_MAX_SPLIT splits.
 struct SkinnyPlan {
+  int bm;
   int nsplit;
   size_t ws;
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
-  SkinnyPlan p{1, 0};
+  SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0};
   if (r <= 0) return p;
-  const int64_t mtiles = (T + 63) / 64, ntiles = (r + 127) / 128;
+  const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + 127) / 128;
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
-  int64_t want = (PF_WG_TARGET + mtiles * ntiles - 1) / (mtiles * ntiles);
-  int64_t ns = std::min<int64_t>({want, PF_MAX_SPLIT, std::max<int64_t>(1, steps / 4)});
+  int64_t ns;
+  if (dtype == 0) {
+    const int64_t want = std::max<int64_t>(1, 512 / (mtiles * ntiles));
+    const int64_t cap = std::max<int64_t>(1, steps / 6);
+    ns = 1;
+    while (ns * 2 <= std::min(want, cap)) ns *= 2;
+    if (ns == 2 && steps < 16) ns = 1;
+  } else {
+    const int64_t want = (PF_WG_TARGET + mtiles * ntiles - 1) / (mtiles * ntiles);
+    ns = std::min<int64_t>({want, PF_MAX_SPLIT, std::max<int64_t>(1, steps / 4)});
+  }
   if (ns > 1) {
     p.nsplit = (int)ns;
     p.ws = (size_t)ns * T * r * sizeof(float);
@@ -485,8 +500,8 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(PF_KERNEL_SKINNY, dt, b, false, 64, T, X, L->n_in, V, L->n_in, L->nb_in, r / b,
-                  T_lr, r, sp.nsplit,
+    st = dense_nt(PF_KERNEL_SKINNY, dt, b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
+                  r / b, T_lr, r, sp.nsplit,
                   (float *)workspace, s, "T_lr kernel");
     if (st != PF_OK) return st;
   }
@@ -526,8 +541,8 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // S = dY U: dense over N with U read as [k][n].
-    st = dense_nt(PF_KERNEL_SKINNY, dt, b, true, 64, T, dY, L->n_out, U, r, L->nb_out, r / b, S,
-                  r, sp.nsplit,
+    st = dense_nt(PF_KERNEL_SKINNY, dt, b, true, sp.bm, T, dY, L->n_out, U, r, L->nb_out, r / b,
+                  S, r, sp.nsplit,
                   (float *)workspace, s, "S kernel");
     if (st != PF_OK) return st;
   }
