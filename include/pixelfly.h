@@ -125,7 +125,9 @@ pf_status pf_layout_check(const pf_layout *layout);
 /* Diagnostic: work-list statistics, n >= 6 entries written to stats:
  * [0] forward tile rows G, [1] forward tiles, [2] backward-data tile
  * columns G, [3] backward-data tiles, [4] weight-gradient items,
- * [5] kept blocks covered by those items.  Host only. */
+ * [5] kept blocks covered by those items; with n >= 10 also [6..9], the
+ * same four figures of the wide (256-column) tile lists.  n >= 6.  Host
+ * only. */
 pf_status pf_layout_plan_get(const pf_layout *layout, int32_t *stats,
                              int32_t n);
 

@@ -114,28 +114,48 @@ int pow2_group(int gmax, int n) {
   return g;
 }
 
-// NT launch: bf16 tiles 128 columns wide go to the direct-to-LDS kernel
-// family, everything else to the register-staged one.
+// NT launch: bf16 tiles 64 (b <= 64), 128 or 256 columns wide go to the
+// direct-to-LDS kernel family, everything else to the register-staged one.
 #ifndef PF_NTD
 #define PF_NTD 1
 #endif
+// The direct-to-LDS TN kernel (gemm_dma.hip) is parity-tested but slower
+// than the register-staged one at the workload shapes, so it is off.
+#ifndef PF_TND
+#define PF_TND 0
+#endif
+bool ntd_width(int dtype, int blk, int G) {
+  const int w = G * blk;
+  return PF_NTD && dtype == 0 && (w == 128 || w == 256 || (w == 64 && blk <= 64));
+}
+
 hipError_t nt_launch(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm,
                      const pf::NTArgs &a, hipStream_t s) {
   Timed t(kc, s);
-  if (PF_NTD && dtype == 0 && bm == 128 && G * blk == 128) return pf::launch_ntd(blk, G, b_kn, 0, a, s);
+  if (ntd_width(dtype, blk, G)) {
+    // 512-token tiles for 128-column outputs once they still make 512+
+    // workgroups.
+    const bool tall = G * blk == 128 && ((a.M + 511) / 512) * a.ntiles * std::max(1, a.nsplit) >= 512;
+    return pf::launch_ntd(blk, G, b_kn, tall, a, s);
+  }
   return pf::launch_nt(dtype, blk, G, b_kn, bm, a, s);
 }
 
+// Wide (256-column, 256-token) bf16 tiles pay off once there are enough
+// token rows to fill them.
+#ifndef PF_WIDE_MIN_T
+#define PF_WIDE_MIN_T 2048
+#endif
+
 // Dense-mode NT launch: C[M x nblk*b] = A[M x nsteps*b] . B^T (B [n][k]) or
 // A . B (B [k][n]), with M-tile bm; split over K when ws gives room.
-pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, bool b_kn, int bm, int64_t M,
+pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm, int64_t M,
                    const void *A, int64_t lda, const void *B, int64_t ldb, int nsteps, int nblk,
                    void *C, int64_t ldc, int nsplit, float *ws, hipStream_t s, const char *what) {
   pf::NTArgs a{};
   a.A = A; a.lda = lda; a.B = B; a.ldb = ldb;
   a.dense = 1; a.dense_nsteps = nsteps; a.dense_nblk = nblk;
   a.C = C; a.ldc = ldc; a.M = M;
-  const int G = 128 / blk;  // dense tiles are 128 columns wide
   a.ntiles = (nblk + G - 1) / G;
   a.nsplit = nsplit;
   a.partials = ws;
@@ -370,6 +390,12 @@ pf_status pf_layout_check(const pf_layout *L) {
 
 pf_status pf_layout_plan_get(const pf_layout *L, int32_t *stats, int32_t n) {
   if (!L || !stats || n < 6) return fail(PF_ERR_INVALID_ARG, "bad arguments");
+  if (n >= 10) {
+    stats[6] = L->G_fwd_w;
+    stats[7] = (int32_t)L->fwd_tiles_w.size();
+    stats[8] = L->G_bwd_w;
+    stats[9] = (int32_t)L->bwd_tiles_w.size();
+  }
   stats[0] = L->G_fwd;
   stats[1] = (int32_t)L->fwd_tiles.size();
   stats[2] = L->G_bwd;
@@ -390,33 +416,40 @@ pf_status pf_layout_upload(pf_layout *L, void *stream) {
   int dev = -1;
   pf_status st = hip_status(hipGetDevice(&dev), "hipGetDevice");
   if (st != PF_OK) return st;
-  auto bytes = [](size_t n, size_t sz) { return (n * sz + 255) / 256 * 256; };
-  size_t off[11], total = 0;
-  size_t sizes[11] = {
-      bytes(L->fwd_tiles.size(), sizeof(pf::NTTile)), bytes(L->bwd_tiles.size(), sizeof(pf::NTTile)),
-      bytes(L->kcols_fwd.size(), 4), bytes(L->blks_fwd.size(), 4),
-      bytes(L->kcols_bwd.size(), 4), bytes(L->blks_bwd.size(), 4),
-      bytes(L->tn_items.size(), sizeof(pf::TNItem)), bytes(L->row_ptr.size(), 4),
-      bytes(L->col_idx.size(), 4), bytes(L->col_ptr.size(), 4), bytes(L->row_idx.size(), 4)};
-  const void *src[11] = {L->fwd_tiles.data(), L->bwd_tiles.data(), L->kcols_fwd.data(),
-                         L->blks_fwd.data(),  L->kcols_bwd.data(), L->blks_bwd.data(),
-                         L->tn_items.data(),  L->row_ptr.data(),   L->col_idx.data(),
-                         L->col_ptr.data(),   L->row_idx.data()};
-  size_t nbytes[11] = {L->fwd_tiles.size() * sizeof(pf::NTTile), L->bwd_tiles.size() * sizeof(pf::NTTile),
-                       L->kcols_fwd.size() * 4, L->blks_fwd.size() * 4, L->kcols_bwd.size() * 4,
-                       L->blks_bwd.size() * 4, L->tn_items.size() * sizeof(pf::TNItem),
-                       L->row_ptr.size() * 4, L->col_idx.size() * 4, L->col_ptr.size() * 4,
-                       L->row_idx.size() * 4};
-  for (int i = 0; i < 11; ++i) {
+  // Every host array goes into one device allocation, 256-byte aligned
+  // pieces; `dst` receives each piece's device address.
+  struct Piece {
+    const void *src;
+    size_t bytes;
+    const void **dst;
+  };
+  auto vec = [](auto &v, auto &d) {
+    return Piece{v.data(), v.size() * sizeof(v[0]), (const void **)&d};
+  };
+  const Piece pieces[] = {
+      vec(L->fwd_tiles, L->d_fwd_tiles),     vec(L->bwd_tiles, L->d_bwd_tiles),
+      vec(L->kcols_fwd, L->d_kcols_fwd),     vec(L->blks_fwd, L->d_blks_fwd),
+      vec(L->kcols_bwd, L->d_kcols_bwd),     vec(L->blks_bwd, L->d_blks_bwd),
+      vec(L->fwd_tiles_w, L->d_fwd_tiles_w), vec(L->bwd_tiles_w, L->d_bwd_tiles_w),
+      vec(L->kcols_fwd_w, L->d_kcols_fwd_w), vec(L->blks_fwd_w, L->d_blks_fwd_w),
+      vec(L->kcols_bwd_w, L->d_kcols_bwd_w), vec(L->blks_bwd_w, L->d_blks_bwd_w),
+      vec(L->tn_items, L->d_tn_items),       vec(L->row_ptr, L->d_row_ptr),
+      vec(L->col_idx, L->d_col_idx),         vec(L->col_ptr, L->d_col_ptr),
+      vec(L->row_idx, L->d_row_idx)};
+  constexpr int NP = (int)(sizeof(pieces) / sizeof(pieces[0]));
+  size_t off[NP], total = 0;
+  for (int i = 0; i < NP; ++i) {
     off[i] = total;
-    total += sizes[i];
+    total += (pieces[i].bytes + 255) / 256 * 256;
   }
   void *mem = nullptr;
-  if (hipMalloc(&mem, total) != hipSuccess) return fail(PF_ERR_NOMEM, "hipMalloc for layout failed");
+  if (hipMalloc(&mem, std::max<size_t>(total, 256)) != hipSuccess)
+    return fail(PF_ERR_NOMEM, "hipMalloc for layout failed");
   hipStream_t s = (hipStream_t)stream;
-  for (int i = 0; i < 11; ++i)
-    if (nbytes[i]) {
-      hipError_t e = hipMemcpyAsync((char *)mem + off[i], src[i], nbytes[i], hipMemcpyHostToDevice, s);
+  for (int i = 0; i < NP; ++i)
+    if (pieces[i].bytes) {
+      hipError_t e = hipMemcpyAsync((char *)mem + off[i], pieces[i].src, pieces[i].bytes,
+                                    hipMemcpyHostToDevice, s);
       if (e != hipSuccess) {
         (void)hipFree(mem);
         return hip_status(e, "layout upload");
@@ -427,18 +460,7 @@ pf_status pf_layout_upload(pf_layout *L, void *stream) {
     (void)hipFree(mem);
     return hip_status(e, "layout upload sync");
   }
-  char *m = (char *)mem;
-  L->d_fwd_tiles = (const pf::NTTile *)(m + off[0]);
-  L->d_bwd_tiles = (const pf::NTTile *)(m + off[1]);
-  L->d_kcols_fwd = (const int32_t *)(m + off[2]);
-  L->d_blks_fwd = (const int32_t *)(m + off[3]);
-  L->d_kcols_bwd = (const int32_t *)(m + off[4]);
-  L->d_blks_bwd = (const int32_t *)(m + off[5]);
-  L->d_tn_items = (const pf::TNItem *)(m + off[6]);
-  L->d_row_ptr = (const int32_t *)(m + off[7]);
-  L->d_col_idx = (const int32_t *)(m + off[8]);
-  L->d_col_ptr = (const int32_t *)(m + off[9]);
-  L->d_row_idx = (const int32_t *)(m + off[10]);
+  for (int i = 0; i < NP; ++i) *pieces[i].dst = (const char *)mem + off[i];
   L->dev_mem = mem;
   L->device = dev;
   return PF_OK;
@@ -500,7 +522,7 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(PF_KERNEL_SKINNY, dt, b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
+    st = dense_nt(PF_KERNEL_SKINNY, dt, b, 128 / b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
                   r / b, T_lr, r, sp.nsplit,
                   (float *)workspace, s, "T_lr kernel");
     if (st != PF_OK) return st;
@@ -513,10 +535,14 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   a.C2 = epi == PF_EPI_GELU ? Y_pre : nullptr;
   a.epi = (int)epi;
   a.M = T;
-  a.tiles = L->d_fwd_tiles; a.ntiles = (int)L->fwd_tiles.size();
-  a.kcols = L->d_kcols_fwd; a.blks = L->d_blks_fwd;
+  const bool wide = ntd_width(dt, b, L->G_fwd_w) && L->G_fwd_w * b == 256 && T >= PF_WIDE_MIN_T;
+  a.tiles = wide ? L->d_fwd_tiles_w : L->d_fwd_tiles;
+  a.ntiles = (int)(wide ? L->fwd_tiles_w.size() : L->fwd_tiles.size());
+  a.kcols = wide ? L->d_kcols_fwd_w : L->d_kcols_fwd;
+  a.blks = wide ? L->d_blks_fwd_w : L->d_blks_fwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, L->G_fwd, false, 128, a, s), "forward kernel");
+  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, wide ? L->G_fwd_w : L->G_fwd, false, 128, a, s),
+                    "forward kernel");
 }
 
 pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -541,7 +567,7 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // S = dY U: dense over N with U read as [k][n].
-    st = dense_nt(PF_KERNEL_SKINNY, dt, b, true, sp.bm, T, dY, L->n_out, U, r, L->nb_out, r / b,
+    st = dense_nt(PF_KERNEL_SKINNY, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r, L->nb_out, r / b,
                   S, r, sp.nsplit,
                   (float *)workspace, s, "S kernel");
     if (st != PF_OK) return st;
@@ -554,10 +580,13 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.aux = aux;
   a.epi = (int)epi;
   a.M = T;
-  a.tiles = L->d_bwd_tiles; a.ntiles = (int)L->bwd_tiles.size();
-  a.kcols = L->d_kcols_bwd; a.blks = L->d_blks_bwd;
+  const bool wide = ntd_width(dt, b, L->G_bwd_w) && L->G_bwd_w * b == 256 && T >= PF_WIDE_MIN_T;
+  a.tiles = wide ? L->d_bwd_tiles_w : L->d_bwd_tiles;
+  a.ntiles = (int)(wide ? L->bwd_tiles_w.size() : L->bwd_tiles.size());
+  a.kcols = wide ? L->d_kcols_bwd_w : L->d_kcols_bwd;
+  a.blks = wide ? L->d_blks_bwd_w : L->d_blks_bwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, L->G_bwd, true, 128, a, s),
+  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true, 128, a, s),
                     "backward-data kernel");
 }
 
@@ -589,14 +618,17 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   a.chunk = p.chunk;
   a.partials = (float *)workspace;
   hipStream_t s = (hipStream_t)stream;
+  const bool dma = PF_TND && dtype == PF_BF16;
   {
     Timed t(PF_KERNEL_SDDMM, s);
-    if ((st = hip_status(pf::launch_tn((int)dtype, L->b, a, s), "weight-gradient kernel")) != PF_OK)
-      return st;
+    st = hip_status(dma ? pf::launch_tnd(L->b, false, a, s) : pf::launch_tn((int)dtype, L->b, a, s),
+                    "weight-gradient kernel");
+    if (st != PF_OK) return st;
   }
   if (a.nsplit <= 1) return PF_OK;
   Timed t(PF_KERNEL_REDUCE, s);
-  return hip_status(pf::launch_tn_reduce((int)dtype, L->b, a, s), "weight-gradient reduction");
+  return hip_status(dma ? pf::launch_tnd(L->b, true, a, s) : pf::launch_tn_reduce((int)dtype, L->b, a, s),
+                    "weight-gradient reduction");
 }
 
 pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_pre, void *dH_pre,
@@ -686,6 +718,12 @@ size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_
   return tn_plan(items, K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4)).ws;
 }
 
+// Blocks of 64 columns per dense comparator tile: 256-wide bf16 tiles when
+// the shape fills them, else 128.
+static int dense_g(int dt, int64_t M, int64_t N) {
+  return (ntd_width(dt, 64, 4) && N % 256 == 0 && M >= PF_WIDE_MIN_T) ? 4 : 2;
+}
+
 pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K,
                         const void *A, const void *B, void *C, void *workspace, size_t ws_bytes,
                         void *stream) {
@@ -703,11 +741,11 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
   const int dt = (int)dtype;
   switch (op) {
     case PF_OP_NT:
-      return dense_nt(PF_KERNEL_DENSE, dt, 64, false, 128, M, A, K, B, K, (int)(K / 64),
-                      (int)(N / 64), C, N, 1, nullptr, s, "dense NT");
+      return dense_nt(PF_KERNEL_DENSE, dt, 64, dense_g(dt, M, N), false, 128, M, A, K, B, K,
+                      (int)(K / 64), (int)(N / 64), C, N, 1, nullptr, s, "dense NT");
     case PF_OP_NN:
-      return dense_nt(PF_KERNEL_DENSE, dt, 64, true, 128, M, A, K, B, N, (int)(K / 64),
-                      (int)(N / 64), C, N, 1, nullptr, s, "dense NN");
+      return dense_nt(PF_KERNEL_DENSE, dt, 64, dense_g(dt, M, N), true, 128, M, A, K, B, N,
+                      (int)(K / 64), (int)(N / 64), C, N, 1, nullptr, s, "dense NN");
     case PF_OP_TN: {
       pf::TNArgs a{};
       a.n_items = 0;
@@ -719,13 +757,16 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
       a.nsplit = p.nsplit;
       a.chunk = p.chunk;
       a.partials = (float *)workspace;
+      const bool dma = PF_TND && dtype == PF_BF16;
       {
         Timed t(PF_KERNEL_DENSE, s);
-        if ((st = hip_status(pf::launch_tn(dt, 64, a, s), "dense TN")) != PF_OK) return st;
+        st = hip_status(dma ? pf::launch_tnd(64, false, a, s) : pf::launch_tn(dt, 64, a, s), "dense TN");
+        if (st != PF_OK) return st;
       }
       if (a.nsplit <= 1) return PF_OK;
       Timed t(PF_KERNEL_REDUCE, s);
-      return hip_status(pf::launch_tn_reduce(dt, 64, a, s), "dense TN reduction");
+      return hip_status(dma ? pf::launch_tnd(64, true, a, s) : pf::launch_tn_reduce(dt, 64, a, s),
+                        "dense TN reduction");
     }
   }
   return fail(PF_ERR_INVALID_ARG, "bad op");

@@ -153,13 +153,23 @@ __device__ __forceinline__ bf16x8 frag_kn(const uint8_t *region, int n0, int kq,
   return __builtin_bit_cast(bf16x8, v);
 }
 
-template <int BLK, int G, bool BKN, int BM, int BK, int NS, bool DENSE, int EPI, int OCC>
-__global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
+// Pipeline stage I of BYTES bytes: a distinct LDS object per stage, so that
+// the compiler's LDS-DMA dependency tracking can tell the stages apart; only
+// the stages a kernel uses are allocated.
+template <int I, int BYTES>
+__device__ __forceinline__ uint8_t *stage_buf() {
+  __shared__ __attribute__((aligned(1024))) uint8_t buf[BYTES];
+  return buf;
+}
+
+template <int BLK, int G, bool BKN, int BM, int BK, int NS, int NW, bool DENSE, int EPI, int OCC>
+__global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   const NTArgs a = a_arg;
   constexpr int BN = G * BLK;
   constexpr int KW = BK < BLK ? BK : BLK;  // K width of one sub-block
   constexpr int NH = BK / KW;              // sub-blocks per step
-  constexpr int WTM = BM / 2, WTN = BN / 2;
+  // Waves: WGN = BN / 64 along N (64 output columns each), the rest along M.
+  constexpr int WTN = 64, WGN = BN / WTN, WGM = NW / WGN, WTM = BM / WGM;
   constexpr int TM = WTM / 32, TN = WTN / 32;
   // A region: NH sub-blocks of [BM][KW]; B region: G x NH pieces of [BLK][KW]
   // (NT) or [KW][BLK] (B read as [k][n]).
@@ -168,11 +178,12 @@ __global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int PIECE = BLK * KW * 2;
-  constexpr int AWW = A_BYTES / 4096, BWW = B_BYTES / 4096;  // windows per wave
+  constexpr int AWW = A_BYTES / (1024 * NW), BWW = B_BYTES / (1024 * NW);  // windows per wave
   constexpr int WPH = BM / RPWA;                             // A windows per sub-block
   constexpr int WPP = PIECE / 1024;                          // B windows per piece
   constexpr int DPS = AWW + BWW;                             // copies per wave per step
-  static_assert(A_BYTES % 4096 == 0 && B_BYTES % 4096 == 0, "windows");
+  static_assert((NW == 4 || NW == 8) && WGN * WGM == NW && WGM * WTM == BM, "waves");
+  static_assert(A_BYTES % (1024 * NW) == 0 && B_BYTES % (1024 * NW) == 0, "windows");
   static_assert(WPH % AWW == 0, "one sub-block per wave and step");
   static_assert(WPP % BWW == 0 || BWW % WPP == 0, "piece split");
   static_assert(TM >= 1 && TN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
@@ -181,12 +192,9 @@ __global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
   // windows; every wave's first window of a sub-block or piece is even.
   static_assert(AWW % 2 == 0 && BWW % 2 == 0 && WPP % 2 == 0, "window parity");
 
-  __shared__ __attribute__((aligned(1024))) uint8_t st0[STAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t st1[STAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t st2[NS > 2 ? STAGE : 16];
-  __shared__ __attribute__((aligned(1024))) uint8_t st3[NS > 3 ? STAGE : 16];
-  // Each stage is a distinct LDS object so that the compiler's LDS-DMA
-  // dependency tracking can tell the stages apart.
+  uint8_t *const st0 = stage_buf<0, STAGE>(), *const st1 = stage_buf<1, STAGE>();
+  uint8_t *const st2 = NS > 2 ? stage_buf<2, STAGE>() : st0;
+  uint8_t *const st3 = NS > 3 ? stage_buf<3, STAGE>() : st1;
   auto stage = [&](auto j) __attribute__((always_inline)) -> uint8_t * {
     constexpr int J = decltype(j)::value;
     if constexpr (J == 0) return st0;
@@ -202,7 +210,7 @@ __global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / WGN, wn = w % WGN;
   const int ntn = a.ntiles;
   const int mtiles = (int)((a.M + BM - 1) / BM);
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
@@ -408,9 +416,14 @@ __global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
   constexpr int SROW = WTN * 4, SCH = SROW / 16;  // staged row bytes, chunks
   constexpr int SP = 32;                          // rows per pass
   constexpr int LPR = WTN / 8, RPI = 64 / LPR;    // lanes per row, rows per store step
-  static_assert(4 * SP * SROW <= STAGE && (SCH & (SCH - 1)) == 0 && SP % RPI == 0, "staging");
-  const int rem = total % NS;
-  uint8_t *const stg = (rem == 0 ? st0 : rem == 1 ? st1 : rem == 2 ? st2 : st3) + w * (SP * SROW);
+  // Waves per stage buffer; the buffers used are the ones after the stage
+  // read in the last step, so NW / WPS of them must not wrap around to it.
+  constexpr int WPS = STAGE / (SP * SROW) < NW ? STAGE / (SP * SROW) : NW;
+  static_assert(WPS >= 1 && (NW + WPS - 1) / WPS <= NS - 1, "staging room");
+  static_assert((SCH & (SCH - 1)) == 0 && SP % RPI == 0, "staging");
+  const int sidx = (total + w / WPS) % NS;
+  uint8_t *const stg =
+      (sidx == 0 ? st0 : sidx == 1 ? st1 : sidx == 2 ? st2 : st3) + (w % WPS) * (SP * SROW);
   int ob[G];
   sfor<G>([&](auto g) __attribute__((always_inline)) { ob[g] = out_blk(g); });
   bf16_t *C = (bf16_t *)a.C;
@@ -467,7 +480,7 @@ __global__ __launch_bounds__(256, OCC) void ntd_kernel(NTArgs a_arg) {
   });
 }
 
-template <int BLK, int G, bool BKN, int BM, int BK, int NS, bool DENSE, int OCC>
+template <int BLK, int G, bool BKN, int BM, int BK, int NS, int NW, bool DENSE, int OCC>
 hipError_t ntd_go(const NTArgs &a, hipStream_t s) {
   const int64_t mtiles = (a.M + BM - 1) / BM;
   const int64_t grid = mtiles * a.ntiles * std::max(1, a.nsplit);
@@ -475,42 +488,331 @@ hipError_t ntd_go(const NTArgs &a, hipStream_t s) {
   if (!DENSE && a.epi == 1) {
     if constexpr (!DENSE) {
       if constexpr (BKN)
-        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, DENSE, 2, OCC>), dim3((unsigned)grid),
-                           dim3(256), 0, s, a);
+        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 2, OCC>),
+                           dim3((unsigned)grid), dim3(64 * NW), 0, s, a);
       else
-        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, DENSE, 1, OCC>), dim3((unsigned)grid),
-                           dim3(256), 0, s, a);
+        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 1, OCC>),
+                           dim3((unsigned)grid), dim3(64 * NW), 0, s, a);
     }
   } else {
-    hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, DENSE, 0, OCC>), dim3((unsigned)grid),
-                       dim3(256), 0, s, a);
+    hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 0, OCC>), dim3((unsigned)grid),
+                       dim3(64 * NW), 0, s, a);
   }
   return hipGetLastError();
 }
 
-// Tile configurations (output tiles are 128 columns wide): 0 = 128 x 128,
-// K-steps of 64, two stages, two workgroups per CU.
-template <int BLK, bool BKN, bool DENSE>
-hipError_t ntd_cfg(int cfg, const NTArgs &a, hipStream_t s) {
-  constexpr int G = 128 / BLK;
-  if (cfg == 0) return ntd_go<BLK, G, BKN, 128, 64, 2, DENSE, 2>(a, s);
+// Tile configurations, chosen by the output tile width G * BLK:
+//   128: 128 x 128 tiles, 4 waves, two workgroups per CU, or (tall) 512 x
+//        128 tiles, 8 waves of 128 x 64, one workgroup per CU;
+//   256: 256 x 256 tiles, 8 waves of 128 x 64, one workgroup per CU;
+//    64: 256 x  64 tiles, 4 waves, two workgroups per CU.
+// All take K-steps of 64 in two stages.  The 8-wave tiles read half the
+// operand bytes per flop of the 128 x 128 ones and keep two waves per SIMD.
+template <int BLK, int G, bool BKN, bool DENSE>
+hipError_t ntd_cfg(bool tall, const NTArgs &a, hipStream_t s) {
+  constexpr int BN = G * BLK;
+  if constexpr (BN == 128) {
+    if (tall) return ntd_go<BLK, G, BKN, 512, 64, 2, 8, DENSE, 1>(a, s);
+    return ntd_go<BLK, G, BKN, 128, 64, 2, 4, DENSE, 2>(a, s);
+  } else if constexpr (BN == 256) {
+    return ntd_go<BLK, G, BKN, 256, 64, 2, 8, DENSE, 1>(a, s);
+  } else if constexpr (BN == 64) {
+    return ntd_go<BLK, G, BKN, 256, 64, 2, 4, DENSE, 2>(a, s);
+  }
   return hipErrorInvalidValue;
 }
 
 template <int BLK, bool BKN>
-hipError_t ntd_g(int G, int cfg, bool dense, const NTArgs &a, hipStream_t s) {
-  if (G != 128 / BLK) return hipErrorInvalidValue;
-  return dense ? ntd_cfg<BLK, BKN, true>(cfg, a, s) : ntd_cfg<BLK, BKN, false>(cfg, a, s);
+hipError_t ntd_g(int G, bool tall, bool dense, const NTArgs &a, hipStream_t s) {
+  auto go = [&](auto g) {
+    constexpr int GG = decltype(g)::value;
+    return dense ? ntd_cfg<BLK, GG, BKN, true>(tall, a, s) : ntd_cfg<BLK, GG, BKN, false>(tall, a, s);
+  };
+  if (G * BLK == 128) return go(std::integral_constant<int, 128 / BLK>{});
+  if (G * BLK == 256) return go(std::integral_constant<int, 256 / BLK>{});
+  if constexpr (BLK <= 64)
+    if (G * BLK == 64) return go(std::integral_constant<int, 64 / BLK>{});
+  return hipErrorInvalidValue;
+}
+
+
+// ---------------------------------------------------------------------------
+// TN kernel: out[a][b] = sum_t A[t][a] B[t][b] on 128 x 128 work items
+// (weight gradient on kept blocks, dU, dV), same direct-to-LDS pipeline.
+// Both operands are [t][column] tiles (64 tokens x 128 columns, 256-byte
+// rows, chunk index XOR (t & 3) << 2) read with the transpose read; the
+// item's 128 columns gather up to 128 / BLK block columns, so each lane's
+// copy address carries its own block column.
+// ---------------------------------------------------------------------------
+template <int BLK>
+struct TNView {
+  static constexpr int GT = 128 / BLK;
+  bool sparse;
+  const TNItem *it;
+  int na, nb, ag, bg;
+  const bf16_t *Ab, *Bb;
+  int64_t lda, ldb, ldo;
+  bf16_t *dout;
+
+  __device__ __forceinline__ void decode(const TNArgs &a, int item) {
+    const int n0 =
+        a.n_dense > 0 ? ((a.dr[0].na_blk + GT - 1) / GT) * ((a.dr[0].nb_blk + GT - 1) / GT) : 0;
+    sparse = item < a.n_items;
+    it = sparse ? a.items + item : nullptr;
+    ag = bg = 0;
+    dout = nullptr;
+    ldo = 0;
+    if (sparse) {
+      Ab = (const bf16_t *)a.A; lda = a.lda;
+      Bb = (const bf16_t *)a.B; ldb = a.ldb;
+      na = it->na; nb = it->nb;
+    } else {
+      int q = item - a.n_items, r = 0;
+      if (q >= n0) { q -= n0; r = 1; }
+      const TNDense &d = a.dr[r];
+      const int nbg = (d.nb_blk + GT - 1) / GT;
+      ag = q / nbg; bg = q % nbg;
+      Ab = (const bf16_t *)d.A; lda = d.lda;
+      Bb = (const bf16_t *)d.B; ldb = d.ldb;
+      na = min(GT, d.na_blk - ag * GT);
+      nb = min(GT, d.nb_blk - bg * GT);
+      dout = (bf16_t *)d.out;
+      ldo = d.ldo;
+    }
+  }
+  // Block columns of the item (clamped to a valid one past na / nb).
+  __device__ __forceinline__ int acol(int g) const {
+    return sparse ? it->a_col[g] : ag * GT + min(g, na - 1);
+  }
+  __device__ __forceinline__ int bcol(int g) const {
+    return sparse ? it->b_col[g] : bg * GT + min(g, nb - 1);
+  }
+  // Output block of (ga, gb): CSR position (sparse), 0 (dense), -1 if none.
+  __device__ __forceinline__ int oblk(int ga, int gb) const {
+    return sparse ? it->out_blk[ga * kTNMax + gb] : ((ga < na && gb < nb) ? 0 : -1);
+  }
+};
+
+__device__ __forceinline__ int tn_items_total_dev(const TNArgs &a, int GT) {
+  int n = a.n_items;
+  for (int r = 0; r < a.n_dense; ++r)
+    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
+  return n;
+}
+
+template <int BLK>
+__global__ __launch_bounds__(256, 2) void tnd_kernel(TNArgs a_arg) {
+  const TNArgs a = a_arg;
+  constexpr int GT = 128 / BLK;
+  constexpr int BKT = 64;            // tokens per step
+  constexpr int RB = 256;            // LDS bytes per token row (128 columns)
+  constexpr int OPB = BKT * RB;      // one operand tile
+  constexpr int STAGE = 2 * OPB;
+  constexpr int WPW = OPB / 4096;    // windows per wave and operand
+  constexpr int RPW = 1024 / RB;     // token rows per window
+  constexpr int CPB = BLK / 8;       // 16-byte chunks per block row
+  constexpr int TM = 2, TN = 2;      // 4 waves as 2 x 2, 64 x 64 each
+
+  __shared__ __attribute__((aligned(1024))) uint8_t st0[STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t st1[STAGE];
+  auto stage = [&](auto j) __attribute__((always_inline)) -> uint8_t * {
+    if constexpr (decltype(j)::value == 0) return st0;
+    else return st1;
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w >> 1, wn = w & 1;
+  const int items_total = tn_items_total_dev(a, GT);
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = bid / items_total, item = bid % items_total;
+
+  TNView<BLK> v;
+  v.decode(a, item);
+
+  bool live[TN][TM];
+  sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+    sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+      live[tn][tm] = v.oblk((wm * 64 + tm * 32) / BLK, (wn * 64 + tn * 32) / BLK) >= 0;
+    });
+  });
+
+  const int64_t t_begin = (int64_t)split * a.chunk;
+  const int64_t t_end = min(a.T, t_begin + a.chunk);
+  const int total = t_end > t_begin ? (int)((t_end - t_begin + BKT - 1) / BKT) : 0;
+
+  // Copy addresses.  Lane i of a window takes token row i / 16 and LDS chunk
+  // i % 16, which holds the operand's chunk c = (i % 16) ^ ((i / 16) << 2):
+  // block column c / CPB of the item, chunk c % CPB within it.
+  const uint32_t lda_b = (uint32_t)(v.lda * 2), ldb_b = (uint32_t)(v.ldb * 2);
+  uint32_t offA, offB;
+  {
+    const int r = lane >> 4, c = (lane & 15) ^ (r << 2), g = c / CPB, cc = c % CPB;
+    offA = (uint32_t)r * lda_b + (uint32_t)((v.acol(g) * BLK + cc * 8) * 2);
+    offB = (uint32_t)r * ldb_b + (uint32_t)((v.bcol(g) * BLK + cc * 8) * 2);
+  }
+  const bf16_t *const a_base = v.Ab + t_begin * v.lda, *const b_base = v.Bb + t_begin * v.ldb;
+  const int64_t a_bytes = (t_end - t_begin) * v.lda * 2, b_bytes = (t_end - t_begin) * v.ldb * 2;
+
+  auto issue = [&](int t, uint8_t *sb) __attribute__((always_inline)) {
+    const rsrc_t rA = make_rsrc(a_base, a_bytes), rB = make_rsrc(b_base, b_bytes);
+    sfor<WPW>([&](auto i) __attribute__((always_inline)) {
+      const int wi = w * WPW + i;
+      const uint32_t row = (uint32_t)(t * BKT + wi * RPW);
+      dma16(rA, sb + wi * 1024, offA, row * lda_b);
+      dma16(rB, sb + OPB + wi * 1024, offB, row * ldb_b);
+    });
+  };
+
+  f32x16 acc[TN][TM];
+  sfor<TN>([&](auto i) __attribute__((always_inline)) {
+    sfor<TM>([&](auto j) __attribute__((always_inline)) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    });
+  });
+
+  auto compute = [&](const uint8_t *sb) __attribute__((always_inline)) {
+    sfor<BKT / 16>([&](auto ks) __attribute__((always_inline)) {
+      bf16x8 af[TM], bfg[TN];
+      sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+        af[tm] = frag_kn<RB>(sb, wm * 64 + tm * 32, ks, lane);
+      });
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        bfg[tn] = frag_kn<RB>(sb + OPB, wn * 64 + tn * 32, ks, lane);
+      });
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+          if (live[tn][tm])
+            acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfg[tn], af[tm], acc[tn][tm], 0, 0, 0);
+        });
+      });
+    });
+  };
+
+  if (total > 0) issue(0, st0);
+  for (int t0 = 0; t0 < total; t0 += 2) {
+    bool done = false;
+    sfor<2>([&](auto j) __attribute__((always_inline)) {
+      if (done) return;
+      const int t = t0 + j;
+      if (t >= total) {
+        done = true;
+        return;
+      }
+      wait_vm<0>();
+      barrier();
+      if (t + 1 < total) issue(t + 1, stage(std::integral_constant<int, (j + 1) % 2>{}));
+      compute(stage(j));
+    });
+  }
+
+  // Epilogue: as in the NT kernel, lane l of accumulator (tn, tm) holds
+  // output row tm*32 + l%32 (a) and columns tn*32 + q*8 + (l/32)*4 + 0..3
+  // (b); each wave transposes its 64 x 64 tile through the stage buffer not
+  // read in the last step, 32 rows at a time, and stores 8 columns per lane.
+  constexpr int SROW = 64 * 4, SCH = SROW / 16;
+  static_assert(4 * 32 * SROW <= STAGE, "staging");
+  uint8_t *const stg = ((total & 1) ? st1 : st0) + w * (32 * SROW);
+  const int jl = lane & 7, rl = lane >> 3;
+  const int bcl = wn * 64 + jl * 8, gb = bcl / BLK;
+  sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+    {
+      const int r = lane & 31;
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        sfor<4>([&](auto q) __attribute__((always_inline)) {
+          const int c = tn * 8 + q * 2 + (lane >> 5);
+          *(f32x4 *)(stg + r * SROW + ((c ^ (r & (SCH - 1))) << 4)) =
+              f32x4{acc[tn][tm][q * 4 + 0], acc[tn][tm][q * 4 + 1], acc[tn][tm][q * 4 + 2],
+                    acc[tn][tm][q * 4 + 3]};
+        });
+      });
+    }
+    sfor<4>([&](auto it) __attribute__((always_inline)) {
+      const int r = it * 8 + rl;
+      const f32x4 lo = *(const f32x4 *)(stg + r * SROW + (((2 * jl) ^ (r & (SCH - 1))) << 4));
+      const f32x4 hi = *(const f32x4 *)(stg + r * SROW + (((2 * jl + 1) ^ (r & (SCH - 1))) << 4));
+      const int arow = wm * 64 + tm * 32 + r, ga = arow / BLK;
+      const int blk = v.oblk(ga, gb);
+      if (blk < 0) return;
+      if (a.nsplit > 1) {
+        float *P = a.partials + ((int64_t)item * a.nsplit + split) * (128 * 128) + arow * 128 + bcl;
+        *(f32x4 *)P = lo;
+        *(f32x4 *)(P + 4) = hi;
+        return;
+      }
+      bf16_t *dst = v.sparse ? (bf16_t *)a.Wout + (int64_t)blk * (BLK * BLK) + (arow % BLK) * BLK + bcl % BLK
+                             : v.dout + ((int64_t)v.acol(ga) * BLK + arow % BLK) * v.ldo +
+                                   (int64_t)v.bcol(gb) * BLK + bcl % BLK;
+      *(u32x4 *)dst = u32x4{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]),
+                            pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
+    });
+  });
+}
+
+// Sum of the split partials (row-major 128 x 128 per item and split), in
+// split order; workgroup (item, part) covers 1024 of the item's 16384 sums.
+template <int BLK>
+__global__ __launch_bounds__(256) void tnd_reduce_kernel(TNArgs a_arg) {
+  const TNArgs a = a_arg;
+  const int bid = xcd_remap(blockIdx.x, gridDim.x);
+  const int item = bid / 16, part = bid % 16;
+  TNView<BLK> v;
+  v.decode(a, item);
+  const int q = (part * 256 + threadIdx.x) * 4;
+  const int arow = q / 128, bcl = q % 128, ga = arow / BLK, gb = bcl / BLK;
+  const int blk = v.oblk(ga, gb);
+  if (blk < 0) return;
+  const float *P = a.partials + (int64_t)item * a.nsplit * (128 * 128) + q;
+  f32x4 s = *(const f32x4 *)P;
+  for (int sp = 1; sp < a.nsplit; ++sp) s += *(const f32x4 *)(P + (int64_t)sp * (128 * 128));
+  bf16_t *dst = v.sparse ? (bf16_t *)a.Wout + (int64_t)blk * (BLK * BLK) + (arow % BLK) * BLK + bcl % BLK
+                         : v.dout + ((int64_t)v.acol(ga) * BLK + arow % BLK) * v.ldo +
+                               (int64_t)v.bcol(gb) * BLK + bcl % BLK;
+  *(u32x2 *)dst = u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
+}
+
+template <int BLK>
+int tn_items(const TNArgs &a) {
+  constexpr int GT = 128 / BLK;
+  int n = a.n_items;
+  for (int r = 0; r < a.n_dense; ++r)
+    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
+  return n;
+}
+
+template <int BLK>
+hipError_t tnd_go(const TNArgs &a, hipStream_t s, bool reduce) {
+  const int64_t items = tn_items<BLK>(a);
+  if (!reduce) {
+    const int64_t grid = items * a.nsplit;
+    if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((tnd_kernel<BLK>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  } else {
+    if (items <= 0 || items * 16 > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((tnd_reduce_kernel<BLK>), dim3((unsigned)(items * 16)), dim3(256), 0, s, a);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_ntd(int blk, int G, bool b_kn, int cfg, const NTArgs &a, hipStream_t s) {
+hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hipStream_t s) {
   const bool dense = a.dense != 0;
   switch (blk) {
-    case 32: return b_kn ? ntd_g<32, true>(G, cfg, dense, a, s) : ntd_g<32, false>(G, cfg, dense, a, s);
-    case 64: return b_kn ? ntd_g<64, true>(G, cfg, dense, a, s) : ntd_g<64, false>(G, cfg, dense, a, s);
-    case 128: return b_kn ? ntd_g<128, true>(G, cfg, dense, a, s) : ntd_g<128, false>(G, cfg, dense, a, s);
+    case 32: return b_kn ? ntd_g<32, true>(G, tall, dense, a, s) : ntd_g<32, false>(G, tall, dense, a, s);
+    case 64: return b_kn ? ntd_g<64, true>(G, tall, dense, a, s) : ntd_g<64, false>(G, tall, dense, a, s);
+    case 128:
+      return b_kn ? ntd_g<128, true>(G, tall, dense, a, s) : ntd_g<128, false>(G, tall, dense, a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_tnd(int blk, bool reduce, const TNArgs &a, hipStream_t s) {
+  switch (blk) {
+    case 32: return tnd_go<32>(a, s, reduce);
+    case 64: return tnd_go<64>(a, s, reduce);
+    case 128: return tnd_go<128>(a, s, reduce);
   }
   return hipErrorInvalidValue;
 }

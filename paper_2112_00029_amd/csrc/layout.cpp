@@ -29,6 +29,11 @@ int max_group(int32_t b) {
   return std::max(1, std::min(4, PF_MAX_BN / b));
 }
 
+int max_group_wide(int32_t b) {
+  if (b != 32 && b != 64 && b != 128) return 1;
+  return std::max(1, std::min(kMaxG, 256 / b));
+}
+
 static int tn_group(int32_t b) {
   int g = b > 0 ? 128 / b : 1;
   return std::max(1, std::min(kTNMax, g));
@@ -238,6 +243,14 @@ std::string finish_layout(pf_layout &L) {
       L.col_ptr, L.row_idx, gmax,
       [&](int col, int c) { return L.tperm[L.col_ptr[col] + c]; }, L.G_bwd,
       L.bwd_tiles, L.kcols_bwd, L.blks_bwd);
+  build_nt_tiles(
+      L.row_ptr, L.col_idx, max_group_wide(L.b),
+      [&](int row, int c) { return L.row_ptr[row] + c; }, L.G_fwd_w,
+      L.fwd_tiles_w, L.kcols_fwd_w, L.blks_fwd_w);
+  build_nt_tiles(
+      L.col_ptr, L.row_idx, max_group_wide(L.b),
+      [&](int col, int c) { return L.tperm[L.col_ptr[col] + c]; }, L.G_bwd_w,
+      L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w);
   build_tn_items(L);
   return check_layout(L);
 }
@@ -266,8 +279,12 @@ std::string check_layout(const pf_layout &L) {
   };
   std::string e = sweep(L.fwd_tiles, L.kcols_fwd, L.blks_fwd, L.G_fwd, false);
   if (!e.empty()) return "forward: " + e;
+  e = sweep(L.fwd_tiles_w, L.kcols_fwd_w, L.blks_fwd_w, L.G_fwd_w, false);
+  if (!e.empty()) return "forward (wide): " + e;
   e = sweep(L.bwd_tiles, L.kcols_bwd, L.blks_bwd, L.G_bwd, true);
   if (!e.empty()) return "backward-data: " + e;
+  e = sweep(L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w, L.G_bwd_w, true);
+  if (!e.empty()) return "backward-data (wide): " + e;
   std::fill(seen.begin(), seen.end(), 0);
   for (auto &it : L.tn_items)
     for (int a = 0; a < it.na; ++a)

@@ -16,10 +16,12 @@ struct pf_layout {
   // Work lists.  Forward NT tiles cover output block rows (tiles of G_fwd
   // rows with identical column sets); backward-data NT tiles cover block
   // columns (tiles of G_bwd columns with identical row sets); TN items cover
-  // the kept blocks for the weight gradient.
-  int G_fwd = 1, G_bwd = 1;
-  std::vector<pf::NTTile> fwd_tiles, bwd_tiles;
+  // the kept blocks for the weight gradient.  The "_w" lists group up to
+  // 256 / b rows (wide tiles of the bf16 kernels), the others up to 128 / b.
+  int G_fwd = 1, G_bwd = 1, G_fwd_w = 1, G_bwd_w = 1;
+  std::vector<pf::NTTile> fwd_tiles, bwd_tiles, fwd_tiles_w, bwd_tiles_w;
   std::vector<int32_t> kcols_fwd, blks_fwd, kcols_bwd, blks_bwd;
+  std::vector<int32_t> kcols_fwd_w, blks_fwd_w, kcols_bwd_w, blks_bwd_w;
   std::vector<pf::TNItem> tn_items;
 
   // Device copies (valid after pf_layout_upload).
@@ -28,6 +30,9 @@ struct pf_layout {
   const pf::NTTile *d_fwd_tiles = nullptr, *d_bwd_tiles = nullptr;
   const int32_t *d_kcols_fwd = nullptr, *d_blks_fwd = nullptr;
   const int32_t *d_kcols_bwd = nullptr, *d_blks_bwd = nullptr;
+  const pf::NTTile *d_fwd_tiles_w = nullptr, *d_bwd_tiles_w = nullptr;
+  const int32_t *d_kcols_fwd_w = nullptr, *d_blks_fwd_w = nullptr;
+  const int32_t *d_kcols_bwd_w = nullptr, *d_blks_bwd_w = nullptr;
   const pf::TNItem *d_tn_items = nullptr;
   const int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
   const int32_t *d_col_ptr = nullptr, *d_row_idx = nullptr;
@@ -44,6 +49,8 @@ std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, 
 std::string finish_layout(pf_layout &L);
 // Re-verify the work lists against the block-CSR.  Returns "" or an error.
 std::string check_layout(const pf_layout &L);
-// Blocks per NT tile row-group the kernels are instantiated for.
+// Blocks per NT tile row-group the kernels are instantiated for (narrow and
+// wide lists).
 int max_group(int32_t b);
+int max_group_wide(int32_t b);
 }  // namespace pf

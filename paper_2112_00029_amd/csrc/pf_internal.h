@@ -108,8 +108,13 @@ struct AttnArgs {
 hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a,
                      hipStream_t s);
 // bf16 NT family with direct global -> LDS operand copies (gemm_dma.hip).
-// G * blk is 128; cfg 0 = 128-token tiles (two workgroups per CU).
-hipError_t launch_ntd(int blk, int G, bool b_kn, int cfg, const NTArgs &a, hipStream_t s);
+// The output tile is G * blk = 64, 128 or 256 columns wide (the token tile
+// follows: 256, 128 or with `tall` 512, 256).
+hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hipStream_t s);
+// bf16 TN kernel with direct global -> LDS copies (gemm_dma.hip); with
+// reduce = true the pass that sums its split partials (row-major 128 x 128
+// per item and split: a different partial layout from launch_tn's).
+hipError_t launch_tnd(int blk, bool reduce, const TNArgs &a, hipStream_t s);
 // Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
 hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
                               void *C, int64_t ldc, hipStream_t s);

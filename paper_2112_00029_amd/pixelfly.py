@@ -193,9 +193,10 @@ def pf_layout_check(layout: Layout) -> None:
 
 
 def pf_layout_plan_get(layout: Layout) -> dict:
-    st = (_i32 * 6)()
-    _check(_lib.pf_layout_plan_get(layout.handle, st, 6))
-    keys = ["G_fwd", "fwd_tiles", "G_bwd", "bwd_tiles", "tn_items", "tn_kept"]
+    st = (_i32 * 10)()
+    _check(_lib.pf_layout_plan_get(layout.handle, st, 10))
+    keys = ["G_fwd", "fwd_tiles", "G_bwd", "bwd_tiles", "tn_items", "tn_kept",
+            "G_fwd_wide", "fwd_tiles_wide", "G_bwd_wide", "bwd_tiles_wide"]
     return dict(zip(keys, list(st)))
 
 

@@ -64,11 +64,15 @@ def test_tiled_layouts_group_rows():
     # tiles are at most 128 columns wide
     st = pf.pf_layout_plan_get(pf.pf_layout_create(16384, 4096, 128, 32))
     assert st["G_fwd"] == 1 and st["fwd_tiles"] == 128
+    # wide lists: the four tiled copies pair up (256 columns per tile)
+    assert st["G_fwd_wide"] == 2 and st["fwd_tiles_wide"] == 64
     st = pf.pf_layout_plan_get(pf.pf_layout_create(16384, 4096, 64, 32))
     assert st["G_fwd"] == 2 and st["fwd_tiles"] == 128
+    assert st["G_fwd_wide"] == 4 and st["fwd_tiles_wide"] == 64
     # tiled copies along the input dim form 2-column tiles for backward-data
     st = pf.pf_layout_plan_get(pf.pf_layout_create(1024, 4096, 64, 16))
     assert st["G_bwd"] == 2 and st["bwd_tiles"] == 32
+    assert st["G_bwd_wide"] == 4 and st["bwd_tiles_wide"] == 16
 
 
 def test_layout_create_errors():

@@ -10,7 +10,9 @@ pytestmark = pytest.mark.gpu
 
 
 @pytest.mark.parametrize("op", ["NT", "NN", "TN"])
-@pytest.mark.parametrize("M,N,K,dtype", [(4096, 3072, 768, "bf16"), (320, 192, 128, "bf16"),
+@pytest.mark.parametrize("M,N,K,dtype", [(4096, 3072, 768, "bf16"), (2112, 512, 256, "bf16"),
+                                         (8192, 4224, 256, "bf16"),
+                                         (320, 192, 128, "bf16"),
                                          (256, 128, 200, "bf16"), (192, 256, 128, "fp32")])
 def test_dense(op, M, N, K, dtype):
     torch = torch_cuda()

@@ -95,6 +95,13 @@ CASES = [
     pytest.param(3072, 768, 32, 16, 300, 96, "bf16", id="mlp_fc1_ragged300"),
     pytest.param(4096, 1024, 64, 16, 520, 128, "bf16", id="fc1_1024x4096_b64_T520"),
     pytest.param(1024, 4096, 64, 16, 520, 128, "bf16", id="fc2_4096x1024_b64_T520"),
+    # >= 2048 tokens: 256 x 256 tiles where four block rows (columns) share
+    # their kept set, 256 x 64 tiles where none do; ragged last token tile
+    pytest.param(4096, 1024, 64, 16, 2100, 128, "bf16", id="fc1_1024x4096_b64_T2100_wide"),
+    pytest.param(1024, 4096, 64, 16, 2100, 128, "bf16", id="fc2_4096x1024_b64_T2100_wide"),
+    pytest.param(2048, 1024, 128, 8, 2100, 128, "bf16", id="b128_T2100_wide"),
+    # 512-token tiles (128-column outputs with 512+ workgroups)
+    pytest.param(4096, 4096, 128, 32, 8000, 128, "bf16", id="b128_4096sq_T8000_tall"),
     pytest.param(16384, 4096, 128, 32, 200, 256, "bf16", id="large_b128_T200"),
     pytest.param(16384, 4096, 64, 32, 200, 256, "bf16", id="large_b64_T200"),
     pytest.param(16384, 4096, 32, 32, 200, 256, "bf16", id="large_b32_T200"),
