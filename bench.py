@@ -16,8 +16,8 @@ carries the fraction of the bf16 MFMA peak, the speedup over the dense layer
 of the same shape run with the library's own dense MFMA GEMM, and the CPU
 oracle timed on a bounded sample of the workload.  The timed region holds
 only the steps between two events; a second region repeats the steps with
-events between the calls and the library's per-launch events (kernel timing
-hook), which give per_call_ms, per_kernel and the roofline entry of the
+the library's kernel timing hook armed (every dispatch records its own start
+and end events), which gives per_kernel and the roofline entry of the
 dominant kernel.
 """
 from __future__ import annotations
@@ -54,27 +54,6 @@ def parse():
                    help="skip the per-kernel HIP events of the second region (no roofline entry)")
     p.add_argument("--calls-only", default="", help="comma list of calls to loop (profiling aid)")
     return p.parse_args()
-
-
-class Timer:
-    """HIP events on the compute stream between the calls of a step."""
-
-    def __init__(self, torch, names):
-        self.torch = torch
-        self.names = names
-        self.ev = []
-
-    def step_events(self):
-        e = [self.torch.cuda.Event(enable_timing=True) for _ in range(len(self.names) + 1)]
-        self.ev.append(e)
-        return e
-
-    def per_call_ms(self):
-        out = {n: 0.0 for n in self.names}
-        for e in self.ev:
-            for i, n in enumerate(self.names):
-                out[n] += e[i].elapsed_time(e[i + 1])
-        return {n: v / max(1, len(self.ev)) for n, v in out.items()}
 
 
 def dev_bf16(torch, raw):
@@ -397,7 +376,8 @@ def _layer_work(T, K, N, r, w, e):
         "spmm_fwd": (2 * T * (w + r * N), e * (T * K + w + T * r + N * r + T * N)),
         "spmm_bwd_data": (2 * T * (w + r * K), e * (T * N + w + T * r + r * K + T * K)),
         "sddmm": (2 * T * (w + N * r + r * K), e * (T * N + T * K + 2 * T * r + w + N * r + r * K)),
-        "skinny": (2 * T * r * (K + N), e * (T * K + r * K + T * N + N * r + 2 * T * r)),
+        "lowrank_t": (2 * T * K * r, e * (T * K + r * K + T * r)),   # T_lr = X V^T
+        "lowrank_s": (2 * T * N * r, e * (T * N + N * r + T * r)),   # S = dY U
     }
 
 
@@ -457,28 +437,21 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
 
-    # Kernel-timing region: the same K steps again with events between the
-    # calls and the library's per-launch events (pf_timing_begin); event
-    # records add gaps between kernels, so this region only supplies the
-    # per-call and per-kernel durations.
-    timer = Timer(torch, calls)
+    # Kernel-timing region: the same K steps again with the library's
+    # per-launch events (pf_timing_begin: each dispatch records its start and
+    # end), which give per-kernel durations and the roofline entry.
     kernel_timing = not args.no_kernel_timing
     if kernel_timing:
         pf.pf_timing_begin(args.steps * 8)
-    for _ in range(args.steps):
-        ev = timer.step_events()
-        for i, c in enumerate(calls):
-            ev[i].record()
-            R.call(c)
-        ev[-1].record()
-    torch.cuda.synchronize()
-    per_call = timer.per_call_ms()
+        for _ in range(args.steps):
+            for c in calls:
+                R.call(c)
+        torch.cuda.synchronize()
     kt = pf.pf_timing_end() if kernel_timing else {}
     per_kernel = {c: {"launches_per_step": n / args.steps, "avg_ms": avg,
                       "ms_per_step": n * avg / args.steps} for c, (n, avg) in kt.items() if n}
     if args.calls_only:
-        print(json.dumps({"calls_only": calls, "ms_per_step": ms, "per_call_ms": per_call,
-                          "per_kernel": per_kernel}))
+        print(json.dumps({"calls_only": calls, "ms_per_step": ms, "per_kernel": per_kernel}))
         return
 
     sparse, lowrank, dense_fl = R.flops()
@@ -541,7 +514,6 @@ def main():
         "speedup_vs_dense": (dense_ms / ms) if dense_ms else None,
         "dense_tflops": (dense_fl / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
         "torch_dense_ms_per_step": torch_ms,
-        "per_call_ms": per_call,
         "per_kernel": per_kernel,
         "roofline": roof,
         "cpu_baseline": cpu,

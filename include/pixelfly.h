@@ -271,14 +271,15 @@ typedef enum {
   PF_KERNEL_SPMM_FWD = 0,       /* forward block-sparse product (+ low-rank) */
   PF_KERNEL_SPMM_BWD_DATA = 1,  /* backward-data block-sparse product (+ low-rank) */
   PF_KERNEL_SDDMM = 2,          /* weight gradient on the mask, dU, dV */
-  PF_KERNEL_SKINNY = 3,         /* rank-r products T_lr = X V^T, S = dY U */
-  PF_KERNEL_REDUCE = 4,         /* sums of split partial results */
-  PF_KERNEL_GELU_BWD = 5,       /* standalone GELU backward */
-  PF_KERNEL_ATTN_FWD = 6,
-  PF_KERNEL_ATTN_BWD_DQ = 7,    /* dQ (and the row terms delta) */
-  PF_KERNEL_ATTN_BWD_DKV = 8,   /* dK, dV */
-  PF_KERNEL_DENSE = 9,          /* dense comparator GEMM */
-  PF_KERNEL_COUNT = 10
+  PF_KERNEL_LOWRANK_T = 3,      /* rank-r product T_lr = X V^T */
+  PF_KERNEL_LOWRANK_S = 4,      /* rank-r product S = dY U */
+  PF_KERNEL_REDUCE = 5,         /* sums of split partial results */
+  PF_KERNEL_GELU_BWD = 6,       /* standalone GELU backward */
+  PF_KERNEL_ATTN_FWD = 7,
+  PF_KERNEL_ATTN_BWD_DQ = 8,    /* dQ (and the row terms delta) */
+  PF_KERNEL_ATTN_BWD_DKV = 9,   /* dK, dV */
+  PF_KERNEL_DENSE = 10,         /* dense comparator GEMM */
+  PF_KERNEL_COUNT = 11
 } pf_kernel_class;
 
 pf_status pf_timing_begin(int32_t max_launches_per_class);

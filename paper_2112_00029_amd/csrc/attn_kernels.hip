@@ -414,21 +414,21 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
 hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.BH * a.nbq;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(attn_fwd_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
+  launch_kernel(attn_fwd_kernel, dim3((unsigned)grid), dim3(256), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd_dq(const AttnArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.BH * a.nbq;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(attn_bwd_dq_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
+  launch_kernel(attn_bwd_dq_kernel, dim3((unsigned)grid), dim3(256), s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd_dkv(const AttnArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.BH * a.nbq;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(attn_bwd_dkv_kernel, dim3((unsigned)grid), dim3(256), 0, s, a);
+  launch_kernel(attn_bwd_dkv_kernel, dim3((unsigned)grid), dim3(256), s, a);
   return hipGetLastError();
 }
 

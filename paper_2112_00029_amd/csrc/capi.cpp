@@ -15,6 +15,13 @@
 #include "pf_internal.h"
 #include "pixelfly.h"
 
+namespace pf {
+LaunchEvents &next_launch_events() {
+  thread_local LaunchEvents e;
+  return e;
+}
+}  // namespace pf
+
 namespace {
 
 thread_local std::string g_err;
@@ -47,24 +54,27 @@ struct KernelTimer {
 };
 KernelTimer g_kt;
 
-// Scope around one kernel launch: records the start event on entry and the
-// end event on exit when the hook is armed and the class has room.
+// Scope around one kernel launch: when the hook is armed and the class has
+// room, hands the next launch a pair of events (recorded by the dispatch at
+// the kernel's start and end) and counts it if the launch took them.
 class Timed {
  public:
-  Timed(pf_kernel_class k, hipStream_t s) : k_(k), s_(s) {
+  Timed(pf_kernel_class k, hipStream_t) : k_(k) {
     if (!g_kt.armed.load(std::memory_order_acquire) || g_kt.n[k] >= g_kt.cap) return;
-    on_ = hipEventRecord(g_kt.ev[k][2 * g_kt.n[k]], s) == hipSuccess;
+    pf::next_launch_events() = {g_kt.ev[k][2 * g_kt.n[k]], g_kt.ev[k][2 * g_kt.n[k] + 1]};
+    on_ = true;
   }
   ~Timed() {
     if (!on_) return;
-    if (hipEventRecord(g_kt.ev[k_][2 * g_kt.n[k_] + 1], s_) == hipSuccess) g_kt.n[k_]++;
+    pf::LaunchEvents &e = pf::next_launch_events();
+    if (!e.start) g_kt.n[k_]++;  // consumed by a launch
+    e.start = e.stop = nullptr;
   }
   Timed(const Timed &) = delete;
   Timed &operator=(const Timed &) = delete;
 
  private:
   pf_kernel_class k_;
-  hipStream_t s_;
   bool on_ = false;
 };
 
@@ -115,15 +125,12 @@ int pow2_group(int gmax, int n) {
 }
 
 // NT launch: bf16 tiles 64 (b <= 64), 128 or 256 columns wide go to the
-// direct-to-LDS kernel family, everything else to the register-staged one.
+// direct-to-LDS kernel family; fp32 and 32-column bf16 tiles go to the
+// register-staged one (faster for single 32-wide block columns).
 #ifndef PF_NTD
 #define PF_NTD 1
 #endif
-// The direct-to-LDS TN kernel (gemm_dma.hip) is parity-tested but slower
-// than the register-staged one at the workload shapes, so it is off.
-#ifndef PF_TND
-#define PF_TND 0
-#endif
+
 bool ntd_width(int dtype, int blk, int G) {
   const int w = G * blk;
   return PF_NTD && dtype == 0 && (w == 128 || w == 256 || (w == 64 && blk <= 64));
@@ -209,30 +216,36 @@ SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   return p;
 }
 
-// Split-token plan of the TN kernel.
+// Split-token plan of the TN kernel: aim for about 4096 workgroups (token
+// splits also shorten each workgroup's serial chain and its L2 footprint),
+// power-of-two splits of at least 512 tokens, at most PF_TN_MAX_SPLIT; and
+// enough splits that one split's rows stay below 2^31 bytes (32-bit buffer
+// offsets).
+#ifndef PF_TN_MAX_SPLIT
+#define PF_TN_MAX_SPLIT 8
+#endif
 struct TNPlan {
   int nsplit;
   int64_t chunk;
   size_t ws;
 };
 
-// row_bytes: the largest operand row stride in bytes; one split's token
-// range must stay below 2^31 bytes of rows (32-bit buffer offsets).
+// row_bytes: the largest operand row stride in bytes.
 TNPlan tn_plan(int items, int64_t T, int64_t row_bytes) {
   TNPlan p{1, ((T + 63) / 64) * 64, 0};
   const int64_t min_split = (T * row_bytes + 0x7fffffffLL - 1) / 0x7fffffffLL;
-  if (items < PF_WG_TARGET || min_split > 1) {
-    int64_t want = (PF_WG_TARGET + items - 1) / items;
-    int64_t maxs = std::max<int64_t>(1, T / 256);
-    int64_t ns = std::max(min_split, std::min<int64_t>({want, maxs, PF_MAX_SPLIT}));
+  int64_t ns = 1;
+  const int64_t want = std::max<int64_t>(1, 4096 / std::max(1, items));
+  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(PF_TN_MAX_SPLIT, T / 512));
+  while (ns * 2 <= std::min(want, cap)) ns *= 2;
+  ns = std::max(ns, min_split);
+  if (ns > 1) {
+    const int64_t chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
+    ns = (T + chunk - 1) / chunk;
     if (ns > 1) {
-      int64_t chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
-      ns = (T + chunk - 1) / chunk;
-      if (ns > 1) {
-        p.nsplit = (int)ns;
-        p.chunk = chunk;
-        p.ws = (size_t)items * ns * 128 * 128 * sizeof(float);
-      }
+      p.nsplit = (int)ns;
+      p.chunk = chunk;
+      p.ws = (size_t)items * ns * 128 * 128 * sizeof(float);
     }
   }
   return p;
@@ -522,7 +535,7 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(PF_KERNEL_SKINNY, dt, b, 128 / b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
+    st = dense_nt(PF_KERNEL_LOWRANK_T, dt, b, 128 / b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
                   r / b, T_lr, r, sp.nsplit,
                   (float *)workspace, s, "T_lr kernel");
     if (st != PF_OK) return st;
@@ -567,7 +580,7 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   const int dt = (int)dtype, b = L->b;
   if (r > 0) {
     // S = dY U: dense over N with U read as [k][n].
-    st = dense_nt(PF_KERNEL_SKINNY, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r, L->nb_out, r / b,
+    st = dense_nt(PF_KERNEL_LOWRANK_S, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r, L->nb_out, r / b,
                   S, r, sp.nsplit,
                   (float *)workspace, s, "S kernel");
     if (st != PF_OK) return st;
@@ -618,17 +631,14 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   a.chunk = p.chunk;
   a.partials = (float *)workspace;
   hipStream_t s = (hipStream_t)stream;
-  const bool dma = PF_TND && dtype == PF_BF16;
   {
     Timed t(PF_KERNEL_SDDMM, s);
-    st = hip_status(dma ? pf::launch_tnd(L->b, false, a, s) : pf::launch_tn((int)dtype, L->b, a, s),
-                    "weight-gradient kernel");
+    st = hip_status(pf::launch_tn((int)dtype, L->b, a, s), "weight-gradient kernel");
     if (st != PF_OK) return st;
   }
   if (a.nsplit <= 1) return PF_OK;
   Timed t(PF_KERNEL_REDUCE, s);
-  return hip_status(dma ? pf::launch_tnd(L->b, true, a, s) : pf::launch_tn_reduce((int)dtype, L->b, a, s),
-                    "weight-gradient reduction");
+  return hip_status(pf::launch_tn_reduce((int)dtype, L->b, a, s), "weight-gradient reduction");
 }
 
 pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_pre, void *dH_pre,
@@ -757,16 +767,14 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
       a.nsplit = p.nsplit;
       a.chunk = p.chunk;
       a.partials = (float *)workspace;
-      const bool dma = PF_TND && dtype == PF_BF16;
       {
         Timed t(PF_KERNEL_DENSE, s);
-        st = hip_status(dma ? pf::launch_tnd(64, false, a, s) : pf::launch_tn(dt, 64, a, s), "dense TN");
+        st = hip_status(pf::launch_tn(dt, 64, a, s), "dense TN");
         if (st != PF_OK) return st;
       }
       if (a.nsplit <= 1) return PF_OK;
       Timed t(PF_KERNEL_REDUCE, s);
-      return hip_status(dma ? pf::launch_tnd(64, true, a, s) : pf::launch_tn_reduce(dt, 64, a, s),
-                        "dense TN reduction");
+      return hip_status(pf::launch_tn_reduce(dt, 64, a, s), "dense TN reduction");
     }
   }
   return fail(PF_ERR_INVALID_ARG, "bad op");

@@ -190,7 +190,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   static_assert(NS >= 2 && NS <= 4 && DPS * (NS - 2) < 64, "stages");
   // The lane swizzle of 8-chunk rows alternates between even and odd
   // windows; every wave's first window of a sub-block or piece is even.
-  static_assert(AWW % 2 == 0 && BWW % 2 == 0 && WPP % 2 == 0, "window parity");
+  static_assert(RBA != 128 || AWW % 2 == 0, "window parity (A)");
+  static_assert(BKN || RBB != 128 || (BWW % 2 == 0 && WPP % 2 == 0), "window parity (B)");
 
   uint8_t *const st0 = stage_buf<0, STAGE>(), *const st1 = stage_buf<1, STAGE>();
   uint8_t *const st2 = NS > 2 ? stage_buf<2, STAGE>() : st0;
@@ -488,15 +489,15 @@ hipError_t ntd_go(const NTArgs &a, hipStream_t s) {
   if (!DENSE && a.epi == 1) {
     if constexpr (!DENSE) {
       if constexpr (BKN)
-        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 2, OCC>),
-                           dim3((unsigned)grid), dim3(64 * NW), 0, s, a);
+        launch_kernel(ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 2, OCC>,
+                      dim3((unsigned)grid), dim3(64 * NW), s, a);
       else
-        hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 1, OCC>),
-                           dim3((unsigned)grid), dim3(64 * NW), 0, s, a);
+        launch_kernel(ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 1, OCC>,
+                      dim3((unsigned)grid), dim3(64 * NW), s, a);
     }
   } else {
-    hipLaunchKernelGGL((ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 0, OCC>), dim3((unsigned)grid),
-                       dim3(64 * NW), 0, s, a);
+    launch_kernel(ntd_kernel<BLK, G, BKN, BM, BK, NS, NW, DENSE, 0, OCC>,
+                  dim3((unsigned)grid), dim3(64 * NW), s, a);
   }
   return hipGetLastError();
 }
@@ -536,265 +537,6 @@ hipError_t ntd_g(int G, bool tall, bool dense, const NTArgs &a, hipStream_t s) {
 }
 
 
-// ---------------------------------------------------------------------------
-// TN kernel: out[a][b] = sum_t A[t][a] B[t][b] on 128 x 128 work items
-// (weight gradient on kept blocks, dU, dV), same direct-to-LDS pipeline.
-// Both operands are [t][column] tiles (64 tokens x 128 columns, 256-byte
-// rows, chunk index XOR (t & 3) << 2) read with the transpose read; the
-// item's 128 columns gather up to 128 / BLK block columns, so each lane's
-// copy address carries its own block column.
-// ---------------------------------------------------------------------------
-template <int BLK>
-struct TNView {
-  static constexpr int GT = 128 / BLK;
-  bool sparse;
-  const TNItem *it;
-  int na, nb, ag, bg;
-  const bf16_t *Ab, *Bb;
-  int64_t lda, ldb, ldo;
-  bf16_t *dout;
-
-  __device__ __forceinline__ void decode(const TNArgs &a, int item) {
-    const int n0 =
-        a.n_dense > 0 ? ((a.dr[0].na_blk + GT - 1) / GT) * ((a.dr[0].nb_blk + GT - 1) / GT) : 0;
-    sparse = item < a.n_items;
-    it = sparse ? a.items + item : nullptr;
-    ag = bg = 0;
-    dout = nullptr;
-    ldo = 0;
-    if (sparse) {
-      Ab = (const bf16_t *)a.A; lda = a.lda;
-      Bb = (const bf16_t *)a.B; ldb = a.ldb;
-      na = it->na; nb = it->nb;
-    } else {
-      int q = item - a.n_items, r = 0;
-      if (q >= n0) { q -= n0; r = 1; }
-      const TNDense &d = a.dr[r];
-      const int nbg = (d.nb_blk + GT - 1) / GT;
-      ag = q / nbg; bg = q % nbg;
-      Ab = (const bf16_t *)d.A; lda = d.lda;
-      Bb = (const bf16_t *)d.B; ldb = d.ldb;
-      na = min(GT, d.na_blk - ag * GT);
-      nb = min(GT, d.nb_blk - bg * GT);
-      dout = (bf16_t *)d.out;
-      ldo = d.ldo;
-    }
-  }
-  // Block columns of the item (clamped to a valid one past na / nb).
-  __device__ __forceinline__ int acol(int g) const {
-    return sparse ? it->a_col[g] : ag * GT + min(g, na - 1);
-  }
-  __device__ __forceinline__ int bcol(int g) const {
-    return sparse ? it->b_col[g] : bg * GT + min(g, nb - 1);
-  }
-  // Output block of (ga, gb): CSR position (sparse), 0 (dense), -1 if none.
-  __device__ __forceinline__ int oblk(int ga, int gb) const {
-    return sparse ? it->out_blk[ga * kTNMax + gb] : ((ga < na && gb < nb) ? 0 : -1);
-  }
-};
-
-__device__ __forceinline__ int tn_items_total_dev(const TNArgs &a, int GT) {
-  int n = a.n_items;
-  for (int r = 0; r < a.n_dense; ++r)
-    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
-  return n;
-}
-
-template <int BLK>
-__global__ __launch_bounds__(256, 2) void tnd_kernel(TNArgs a_arg) {
-  const TNArgs a = a_arg;
-  constexpr int GT = 128 / BLK;
-  constexpr int BKT = 64;            // tokens per step
-  constexpr int RB = 256;            // LDS bytes per token row (128 columns)
-  constexpr int OPB = BKT * RB;      // one operand tile
-  constexpr int STAGE = 2 * OPB;
-  constexpr int WPW = OPB / 4096;    // windows per wave and operand
-  constexpr int RPW = 1024 / RB;     // token rows per window
-  constexpr int CPB = BLK / 8;       // 16-byte chunks per block row
-  constexpr int TM = 2, TN = 2;      // 4 waves as 2 x 2, 64 x 64 each
-
-  __shared__ __attribute__((aligned(1024))) uint8_t st0[STAGE];
-  __shared__ __attribute__((aligned(1024))) uint8_t st1[STAGE];
-  auto stage = [&](auto j) __attribute__((always_inline)) -> uint8_t * {
-    if constexpr (decltype(j)::value == 0) return st0;
-    else return st1;
-  };
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = w >> 1, wn = w & 1;
-  const int items_total = tn_items_total_dev(a, GT);
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int split = bid / items_total, item = bid % items_total;
-
-  TNView<BLK> v;
-  v.decode(a, item);
-
-  bool live[TN][TM];
-  sfor<TN>([&](auto tn) __attribute__((always_inline)) {
-    sfor<TM>([&](auto tm) __attribute__((always_inline)) {
-      live[tn][tm] = v.oblk((wm * 64 + tm * 32) / BLK, (wn * 64 + tn * 32) / BLK) >= 0;
-    });
-  });
-
-  const int64_t t_begin = (int64_t)split * a.chunk;
-  const int64_t t_end = min(a.T, t_begin + a.chunk);
-  const int total = t_end > t_begin ? (int)((t_end - t_begin + BKT - 1) / BKT) : 0;
-
-  // Copy addresses.  Lane i of a window takes token row i / 16 and LDS chunk
-  // i % 16, which holds the operand's chunk c = (i % 16) ^ ((i / 16) << 2):
-  // block column c / CPB of the item, chunk c % CPB within it.
-  const uint32_t lda_b = (uint32_t)(v.lda * 2), ldb_b = (uint32_t)(v.ldb * 2);
-  uint32_t offA, offB;
-  {
-    const int r = lane >> 4, c = (lane & 15) ^ (r << 2), g = c / CPB, cc = c % CPB;
-    offA = (uint32_t)r * lda_b + (uint32_t)((v.acol(g) * BLK + cc * 8) * 2);
-    offB = (uint32_t)r * ldb_b + (uint32_t)((v.bcol(g) * BLK + cc * 8) * 2);
-  }
-  const bf16_t *const a_base = v.Ab + t_begin * v.lda, *const b_base = v.Bb + t_begin * v.ldb;
-  const int64_t a_bytes = (t_end - t_begin) * v.lda * 2, b_bytes = (t_end - t_begin) * v.ldb * 2;
-
-  auto issue = [&](int t, uint8_t *sb) __attribute__((always_inline)) {
-    const rsrc_t rA = make_rsrc(a_base, a_bytes), rB = make_rsrc(b_base, b_bytes);
-    sfor<WPW>([&](auto i) __attribute__((always_inline)) {
-      const int wi = w * WPW + i;
-      const uint32_t row = (uint32_t)(t * BKT + wi * RPW);
-      dma16(rA, sb + wi * 1024, offA, row * lda_b);
-      dma16(rB, sb + OPB + wi * 1024, offB, row * ldb_b);
-    });
-  };
-
-  f32x16 acc[TN][TM];
-  sfor<TN>([&](auto i) __attribute__((always_inline)) {
-    sfor<TM>([&](auto j) __attribute__((always_inline)) {
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-    });
-  });
-
-  auto compute = [&](const uint8_t *sb) __attribute__((always_inline)) {
-    sfor<BKT / 16>([&](auto ks) __attribute__((always_inline)) {
-      bf16x8 af[TM], bfg[TN];
-      sfor<TM>([&](auto tm) __attribute__((always_inline)) {
-        af[tm] = frag_kn<RB>(sb, wm * 64 + tm * 32, ks, lane);
-      });
-      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
-        bfg[tn] = frag_kn<RB>(sb + OPB, wn * 64 + tn * 32, ks, lane);
-      });
-      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
-        sfor<TM>([&](auto tm) __attribute__((always_inline)) {
-          if (live[tn][tm])
-            acc[tn][tm] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bfg[tn], af[tm], acc[tn][tm], 0, 0, 0);
-        });
-      });
-    });
-  };
-
-  if (total > 0) issue(0, st0);
-  for (int t0 = 0; t0 < total; t0 += 2) {
-    bool done = false;
-    sfor<2>([&](auto j) __attribute__((always_inline)) {
-      if (done) return;
-      const int t = t0 + j;
-      if (t >= total) {
-        done = true;
-        return;
-      }
-      wait_vm<0>();
-      barrier();
-      if (t + 1 < total) issue(t + 1, stage(std::integral_constant<int, (j + 1) % 2>{}));
-      compute(stage(j));
-    });
-  }
-
-  // Epilogue: as in the NT kernel, lane l of accumulator (tn, tm) holds
-  // output row tm*32 + l%32 (a) and columns tn*32 + q*8 + (l/32)*4 + 0..3
-  // (b); each wave transposes its 64 x 64 tile through the stage buffer not
-  // read in the last step, 32 rows at a time, and stores 8 columns per lane.
-  constexpr int SROW = 64 * 4, SCH = SROW / 16;
-  static_assert(4 * 32 * SROW <= STAGE, "staging");
-  uint8_t *const stg = ((total & 1) ? st1 : st0) + w * (32 * SROW);
-  const int jl = lane & 7, rl = lane >> 3;
-  const int bcl = wn * 64 + jl * 8, gb = bcl / BLK;
-  sfor<TM>([&](auto tm) __attribute__((always_inline)) {
-    {
-      const int r = lane & 31;
-      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
-        sfor<4>([&](auto q) __attribute__((always_inline)) {
-          const int c = tn * 8 + q * 2 + (lane >> 5);
-          *(f32x4 *)(stg + r * SROW + ((c ^ (r & (SCH - 1))) << 4)) =
-              f32x4{acc[tn][tm][q * 4 + 0], acc[tn][tm][q * 4 + 1], acc[tn][tm][q * 4 + 2],
-                    acc[tn][tm][q * 4 + 3]};
-        });
-      });
-    }
-    sfor<4>([&](auto it) __attribute__((always_inline)) {
-      const int r = it * 8 + rl;
-      const f32x4 lo = *(const f32x4 *)(stg + r * SROW + (((2 * jl) ^ (r & (SCH - 1))) << 4));
-      const f32x4 hi = *(const f32x4 *)(stg + r * SROW + (((2 * jl + 1) ^ (r & (SCH - 1))) << 4));
-      const int arow = wm * 64 + tm * 32 + r, ga = arow / BLK;
-      const int blk = v.oblk(ga, gb);
-      if (blk < 0) return;
-      if (a.nsplit > 1) {
-        float *P = a.partials + ((int64_t)item * a.nsplit + split) * (128 * 128) + arow * 128 + bcl;
-        *(f32x4 *)P = lo;
-        *(f32x4 *)(P + 4) = hi;
-        return;
-      }
-      bf16_t *dst = v.sparse ? (bf16_t *)a.Wout + (int64_t)blk * (BLK * BLK) + (arow % BLK) * BLK + bcl % BLK
-                             : v.dout + ((int64_t)v.acol(ga) * BLK + arow % BLK) * v.ldo +
-                                   (int64_t)v.bcol(gb) * BLK + bcl % BLK;
-      *(u32x4 *)dst = u32x4{pack_bf16x2(lo[0], lo[1]), pack_bf16x2(lo[2], lo[3]),
-                            pack_bf16x2(hi[0], hi[1]), pack_bf16x2(hi[2], hi[3])};
-    });
-  });
-}
-
-// Sum of the split partials (row-major 128 x 128 per item and split), in
-// split order; workgroup (item, part) covers 1024 of the item's 16384 sums.
-template <int BLK>
-__global__ __launch_bounds__(256) void tnd_reduce_kernel(TNArgs a_arg) {
-  const TNArgs a = a_arg;
-  const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int item = bid / 16, part = bid % 16;
-  TNView<BLK> v;
-  v.decode(a, item);
-  const int q = (part * 256 + threadIdx.x) * 4;
-  const int arow = q / 128, bcl = q % 128, ga = arow / BLK, gb = bcl / BLK;
-  const int blk = v.oblk(ga, gb);
-  if (blk < 0) return;
-  const float *P = a.partials + (int64_t)item * a.nsplit * (128 * 128) + q;
-  f32x4 s = *(const f32x4 *)P;
-  for (int sp = 1; sp < a.nsplit; ++sp) s += *(const f32x4 *)(P + (int64_t)sp * (128 * 128));
-  bf16_t *dst = v.sparse ? (bf16_t *)a.Wout + (int64_t)blk * (BLK * BLK) + (arow % BLK) * BLK + bcl % BLK
-                         : v.dout + ((int64_t)v.acol(ga) * BLK + arow % BLK) * v.ldo +
-                               (int64_t)v.bcol(gb) * BLK + bcl % BLK;
-  *(u32x2 *)dst = u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
-}
-
-template <int BLK>
-int tn_items(const TNArgs &a) {
-  constexpr int GT = 128 / BLK;
-  int n = a.n_items;
-  for (int r = 0; r < a.n_dense; ++r)
-    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
-  return n;
-}
-
-template <int BLK>
-hipError_t tnd_go(const TNArgs &a, hipStream_t s, bool reduce) {
-  const int64_t items = tn_items<BLK>(a);
-  if (!reduce) {
-    const int64_t grid = items * a.nsplit;
-    if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((tnd_kernel<BLK>), dim3((unsigned)grid), dim3(256), 0, s, a);
-  } else {
-    if (items <= 0 || items * 16 > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((tnd_reduce_kernel<BLK>), dim3((unsigned)(items * 16)), dim3(256), 0, s, a);
-  }
-  return hipGetLastError();
-}
-
 }  // namespace
 
 hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hipStream_t s) {
@@ -804,15 +546,6 @@ hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hip
     case 64: return b_kn ? ntd_g<64, true>(G, tall, dense, a, s) : ntd_g<64, false>(G, tall, dense, a, s);
     case 128:
       return b_kn ? ntd_g<128, true>(G, tall, dense, a, s) : ntd_g<128, false>(G, tall, dense, a, s);
-  }
-  return hipErrorInvalidValue;
-}
-
-hipError_t launch_tnd(int blk, bool reduce, const TNArgs &a, hipStream_t s) {
-  switch (blk) {
-    case 32: return tnd_go<32>(a, s, reduce);
-    case 64: return tnd_go<64>(a, s, reduce);
-    case 128: return tnd_go<128>(a, s, reduce);
   }
   return hipErrorInvalidValue;
 }

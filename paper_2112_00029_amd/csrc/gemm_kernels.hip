@@ -787,11 +787,13 @@ static hipError_t nt_go(const NTArgs &a, hipStream_t s) {
   // backward-data (B read as [k][n]) the GELU-backward one.
   if (!DENSE && a.epi == 1) {
     if constexpr (!DENSE) {
-      if constexpr (BKN) hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN, BM, DENSE, 2>), dim3((unsigned)grid), dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN, BM, DENSE, 1>), dim3((unsigned)grid), dim3(256), 0, s, a);
+      if constexpr (BKN) launch_kernel(nt_kernel<T, BLK, G, BKN, BM, DENSE, 2>,
+                                       dim3((unsigned)grid), dim3(256), s, a);
+      else launch_kernel(nt_kernel<T, BLK, G, BKN, BM, DENSE, 1>,
+                         dim3((unsigned)grid), dim3(256), s, a);
     }
   } else {
-    hipLaunchKernelGGL((nt_kernel<T, BLK, G, BKN, BM, DENSE, 0>), dim3((unsigned)grid), dim3(256), 0, s, a);
+    launch_kernel(nt_kernel<T, BLK, G, BKN, BM, DENSE, 0>, dim3((unsigned)grid), dim3(256), s, a);
   }
   return hipGetLastError();
 }
@@ -839,11 +841,11 @@ hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, 
   const int64_t n4 = M * ncols / 4;
   const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n4 + 255) / 256, 4096));
   if (dtype == 0)
-    hipLaunchKernelGGL((reduce_rows_kernel<bf16_t>), dim3((unsigned)blocks), dim3(256), 0, s, nsplit, P,
-                       M, ncols, (bf16_t *)C, ldc);
+    launch_kernel(reduce_rows_kernel<bf16_t>,
+                  dim3((unsigned)blocks), dim3(256), s, nsplit, P, M, ncols, (bf16_t *)C, ldc);
   else
-    hipLaunchKernelGGL((reduce_rows_kernel<float>), dim3((unsigned)blocks), dim3(256), 0, s, nsplit, P,
-                       M, ncols, (float *)C, ldc);
+    launch_kernel(reduce_rows_kernel<float>,
+                  dim3((unsigned)blocks), dim3(256), s, nsplit, P, M, ncols, (float *)C, ldc);
   return hipGetLastError();
 }
 
@@ -859,7 +861,7 @@ template <typename T, int BLK>
 static hipError_t tn_go(const TNArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)tn_items_total(a, BLK) * a.nsplit;
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((tn_kernel<T, BLK>), dim3((unsigned)grid), dim3(256), 0, s, a);
+  launch_kernel(tn_kernel<T, BLK>, dim3((unsigned)grid), dim3(256), s, a);
   return hipGetLastError();
 }
 
@@ -867,7 +869,7 @@ template <typename T, int BLK>
 static hipError_t tn_reduce_go(const TNArgs &a, hipStream_t s) {
   const int64_t items = tn_items_total(a, BLK);
   if (items <= 0 || items * 16 > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((tn_reduce_kernel<T, BLK>), dim3((unsigned)(items * 16)), dim3(256), 0, s, a);
+  launch_kernel(tn_reduce_kernel<T, BLK>, dim3((unsigned)(items * 16)), dim3(256), s, a);
   return hipGetLastError();
 }
 
@@ -909,11 +911,13 @@ hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH, const void *Hpr
   if (n <= 0) return hipSuccess;
   int64_t blocks = std::min<int64_t>((n + 255) / 256, 256 * 64);
   if (dtype == 0)
-    hipLaunchKernelGGL((gelu_bwd_kernel<bf16_t>), dim3((unsigned)blocks), dim3(256), 0, s, n,
-                       (const bf16_t *)dH, (const bf16_t *)Hpre, (bf16_t *)out);
+    launch_kernel(gelu_bwd_kernel<bf16_t>,
+                  dim3((unsigned)blocks), dim3(256), s, n, (const bf16_t *)dH,
+                  (const bf16_t *)Hpre, (bf16_t *)out);
   else
-    hipLaunchKernelGGL((gelu_bwd_kernel<float>), dim3((unsigned)blocks), dim3(256), 0, s, n,
-                       (const float *)dH, (const float *)Hpre, (float *)out);
+    launch_kernel(gelu_bwd_kernel<float>,
+                  dim3((unsigned)blocks), dim3(256), s, n, (const float *)dH, (const float *)Hpre,
+                  (float *)out);
   return hipGetLastError();
 }
 

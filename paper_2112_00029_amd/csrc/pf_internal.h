@@ -2,10 +2,31 @@
 // Not part of the public ABI (see include/pixelfly.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace pf {
+
+// Events the next kernel launch of the calling thread records its start and
+// end into (set by the C ABI's kernel timing hook; null when it is off).
+// The timestamps come from the dispatch itself, so they bracket exactly the
+// kernel's execution.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents &next_launch_events();
+
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  LaunchEvents &e = next_launch_events();
+  if (e.start) {
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e.start, e.stop, 0, args...);
+    e.start = e.stop = nullptr;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+  }
+}
 
 // Maximum block rows one NT output tile covers, and blocks per side of a TN
 // (weight-gradient) tile.
@@ -111,10 +132,6 @@ hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs 
 // The output tile is G * blk = 64, 128 or 256 columns wide (the token tile
 // follows: 256, 128 or with `tall` 512, 256).
 hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hipStream_t s);
-// bf16 TN kernel with direct global -> LDS copies (gemm_dma.hip); with
-// reduce = true the pass that sums its split partials (row-major 128 x 128
-// per item and split: a different partial layout from launch_tn's).
-hipError_t launch_tnd(int blk, bool reduce, const TNArgs &a, hipStream_t s);
 // Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
 hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
                               void *C, int64_t ldc, hipStream_t s);

@@ -26,8 +26,8 @@ PF_BF16, PF_FP32 = 0, 1
 PF_EPI_NONE, PF_EPI_GELU = 0, 1
 PF_OP_NT, PF_OP_NN, PF_OP_TN = 0, 1, 2
 # Kernel classes of the timing hook (pf_kernel_class).
-KERNEL_CLASSES = ["spmm_fwd", "spmm_bwd_data", "sddmm", "skinny", "reduce", "gelu_bwd",
-                  "attn_fwd", "attn_bwd_dq", "attn_bwd_dkv", "dense"]
+KERNEL_CLASSES = ["spmm_fwd", "spmm_bwd_data", "sddmm", "lowrank_t", "lowrank_s", "reduce",
+                  "gelu_bwd", "attn_fwd", "attn_bwd_dq", "attn_bwd_dkv", "dense"]
 PF_KERNEL_COUNT = len(KERNEL_CLASSES)
 
 

@@ -185,4 +185,4 @@ def test_timing_hook_errors_before_any_hip_call():
     with pytest.raises(pf.PixelflyError) as e:
         pf.pf_timing_end()
     assert e.value.status == pf.PF_ERR_STATE
-    assert len(pf.KERNEL_CLASSES) == pf.PF_KERNEL_COUNT == 10
+    assert len(pf.KERNEL_CLASSES) == pf.PF_KERNEL_COUNT == 11
