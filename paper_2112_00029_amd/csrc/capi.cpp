@@ -136,14 +136,23 @@ bool ntd_width(int dtype, int blk, int G) {
   return PF_NTD && dtype == 0 && (w == 128 || w == 256 || (w == 64 && blk <= 64));
 }
 
-hipError_t nt_launch(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm,
+// kmax: the most K-blocks (kept + low-rank) of any tile of the launch.
+hipError_t nt_launch(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm, int kmax,
                      const pf::NTArgs &a, hipStream_t s) {
   Timed t(kc, s);
   if (ntd_width(dtype, blk, G)) {
-    // 512-token tiles for 128-column outputs once they still make 512+
-    // workgroups.
-    const bool tall = G * blk == 128 && ((a.M + 511) / 512) * a.ntiles * std::max(1, a.nsplit) >= 512;
-    return pf::launch_ntd(blk, G, b_kn, tall, a, s);
+    // 128-column outputs: 512-token tiles once they still make 512+
+    // workgroups; for block-sparse tiles, short K-steps with three
+    // workgroups per CU when every tile has at most 8 steps of 64 and one
+    // round of workgroups covers them.
+    int variant = pf::NTD_DEFAULT;
+    if (G * blk == 128) {
+      const int64_t wg = ((a.M + 127) / 128) * a.ntiles * std::max(1, a.nsplit);
+      const int64_t steps = ((int64_t)kmax * blk + 63) / 64;
+      if (((a.M + 511) / 512) * a.ntiles * std::max(1, a.nsplit) >= 512) variant = pf::NTD_TALL;
+      else if (!a.dense && steps <= 8 && wg <= 768) variant = pf::NTD_SHORT_K;
+    }
+    return pf::launch_ntd(blk, G, b_kn, variant, a, s);
   }
   return pf::launch_nt(dtype, blk, G, b_kn, bm, a, s);
 }
@@ -167,7 +176,8 @@ pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int
   a.nsplit = nsplit;
   a.partials = ws;
   a.ldp = (int64_t)nblk * blk;
-  pf_status st = hip_status(nt_launch(kc, dtype, blk, G, b_kn, bm, a, s), what);
+  const int per_split = (nsteps + std::max(1, nsplit) - 1) / std::max(1, nsplit);
+  pf_status st = hip_status(nt_launch(kc, dtype, blk, G, b_kn, bm, per_split, a, s), what);
   if (st != PF_OK || nsplit <= 1) return st;
   Timed t(PF_KERNEL_REDUCE, s);
   return hip_status(pf::launch_reduce_rows(dtype, nsplit, ws, M, (int64_t)nblk * blk, C, ldc, s), what);
@@ -554,7 +564,8 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   a.kcols = wide ? L->d_kcols_fwd_w : L->d_kcols_fwd;
   a.blks = wide ? L->d_blks_fwd_w : L->d_blks_fwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, wide ? L->G_fwd_w : L->G_fwd, false, 128, a, s),
+  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, wide ? L->G_fwd_w : L->G_fwd, false, 128,
+                              L->kmax_fwd + r / b, a, s),
                     "forward kernel");
 }
 
@@ -599,7 +610,8 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.kcols = wide ? L->d_kcols_bwd_w : L->d_kcols_bwd;
   a.blks = wide ? L->d_blks_bwd_w : L->d_blks_bwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true, 128, a, s),
+  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true, 128,
+                              L->kmax_bwd + r / b, a, s),
                     "backward-data kernel");
 }
 

@@ -503,17 +503,22 @@ hipError_t ntd_go(const NTArgs &a, hipStream_t s) {
 }
 
 // Tile configurations, chosen by the output tile width G * BLK:
-//   128: 128 x 128 tiles, 4 waves, two workgroups per CU, or (tall) 512 x
-//        128 tiles, 8 waves of 128 x 64, one workgroup per CU;
+//   128: 128 x 128 tiles, 4 waves, two workgroups per CU; or (tall) 512 x
+//        128 tiles, 8 waves of 128 x 64, one workgroup per CU; or (short K
+//        lists) 128 x 128 tiles with K-steps of 32 in three stages, three
+//        workgroups per CU;
 //   256: 256 x 256 tiles, 8 waves of 128 x 64, one workgroup per CU;
 //    64: 256 x  64 tiles, 4 waves, two workgroups per CU.
-// All take K-steps of 64 in two stages.  The 8-wave tiles read half the
-// operand bytes per flop of the 128 x 128 ones and keep two waves per SIMD.
+// The others take K-steps of 64 in two stages.  The 8-wave tiles read half
+// the operand bytes per flop of the 128 x 128 ones and keep two waves per
+// SIMD; the short-K variant keeps more workgroups per CU in flight when each
+// has only a few steps.
 template <int BLK, int G, bool BKN, bool DENSE>
-hipError_t ntd_cfg(bool tall, const NTArgs &a, hipStream_t s) {
+hipError_t ntd_cfg(int variant, const NTArgs &a, hipStream_t s) {
   constexpr int BN = G * BLK;
   if constexpr (BN == 128) {
-    if (tall) return ntd_go<BLK, G, BKN, 512, 64, 2, 8, DENSE, 1>(a, s);
+    if (variant == NTD_TALL) return ntd_go<BLK, G, BKN, 512, 64, 2, 8, DENSE, 1>(a, s);
+    if (variant == NTD_SHORT_K) return ntd_go<BLK, G, BKN, 128, 32, 3, 4, DENSE, 3>(a, s);
     return ntd_go<BLK, G, BKN, 128, 64, 2, 4, DENSE, 2>(a, s);
   } else if constexpr (BN == 256) {
     return ntd_go<BLK, G, BKN, 256, 64, 2, 8, DENSE, 1>(a, s);
@@ -524,10 +529,11 @@ hipError_t ntd_cfg(bool tall, const NTArgs &a, hipStream_t s) {
 }
 
 template <int BLK, bool BKN>
-hipError_t ntd_g(int G, bool tall, bool dense, const NTArgs &a, hipStream_t s) {
+hipError_t ntd_g(int G, int variant, bool dense, const NTArgs &a, hipStream_t s) {
   auto go = [&](auto g) {
     constexpr int GG = decltype(g)::value;
-    return dense ? ntd_cfg<BLK, GG, BKN, true>(tall, a, s) : ntd_cfg<BLK, GG, BKN, false>(tall, a, s);
+    return dense ? ntd_cfg<BLK, GG, BKN, true>(variant, a, s)
+                 : ntd_cfg<BLK, GG, BKN, false>(variant, a, s);
   };
   if (G * BLK == 128) return go(std::integral_constant<int, 128 / BLK>{});
   if (G * BLK == 256) return go(std::integral_constant<int, 256 / BLK>{});
@@ -539,13 +545,16 @@ hipError_t ntd_g(int G, bool tall, bool dense, const NTArgs &a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hipStream_t s) {
+hipError_t launch_ntd(int blk, int G, bool b_kn, int variant, const NTArgs &a, hipStream_t s) {
   const bool dense = a.dense != 0;
   switch (blk) {
-    case 32: return b_kn ? ntd_g<32, true>(G, tall, dense, a, s) : ntd_g<32, false>(G, tall, dense, a, s);
-    case 64: return b_kn ? ntd_g<64, true>(G, tall, dense, a, s) : ntd_g<64, false>(G, tall, dense, a, s);
+    case 32:
+      return b_kn ? ntd_g<32, true>(G, variant, dense, a, s) : ntd_g<32, false>(G, variant, dense, a, s);
+    case 64:
+      return b_kn ? ntd_g<64, true>(G, variant, dense, a, s) : ntd_g<64, false>(G, variant, dense, a, s);
     case 128:
-      return b_kn ? ntd_g<128, true>(G, tall, dense, a, s) : ntd_g<128, false>(G, tall, dense, a, s);
+      return b_kn ? ntd_g<128, true>(G, variant, dense, a, s)
+                  : ntd_g<128, false>(G, variant, dense, a, s);
   }
   return hipErrorInvalidValue;
 }

@@ -252,6 +252,9 @@ std::string finish_layout(pf_layout &L) {
       [&](int col, int c) { return L.tperm[L.col_ptr[col] + c]; }, L.G_bwd_w,
       L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w);
   build_tn_items(L);
+  L.kmax_fwd = L.kmax_bwd = 0;
+  for (auto &t : L.fwd_tiles) L.kmax_fwd = std::max(L.kmax_fwd, (int)t.nsteps);
+  for (auto &t : L.bwd_tiles) L.kmax_bwd = std::max(L.kmax_bwd, (int)t.nsteps);
   return check_layout(L);
 }
 

@@ -19,6 +19,7 @@ struct pf_layout {
   // the kept blocks for the weight gradient.  The "_w" lists group up to
   // 256 / b rows (wide tiles of the bf16 kernels), the others up to 128 / b.
   int G_fwd = 1, G_bwd = 1, G_fwd_w = 1, G_bwd_w = 1;
+  int kmax_fwd = 0, kmax_bwd = 0;  // most kept K-blocks of any forward / backward-data tile
   std::vector<pf::NTTile> fwd_tiles, bwd_tiles, fwd_tiles_w, bwd_tiles_w;
   std::vector<int32_t> kcols_fwd, blks_fwd, kcols_bwd, blks_bwd;
   std::vector<int32_t> kcols_fwd_w, blks_fwd_w, kcols_bwd_w, blks_bwd_w;

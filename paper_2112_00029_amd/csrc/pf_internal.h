@@ -130,8 +130,11 @@ hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs 
                      hipStream_t s);
 // bf16 NT family with direct global -> LDS operand copies (gemm_dma.hip).
 // The output tile is G * blk = 64, 128 or 256 columns wide (the token tile
-// follows: 256, 128 or with `tall` 512, 256).
-hipError_t launch_ntd(int blk, int G, bool b_kn, bool tall, const NTArgs &a, hipStream_t s);
+// follows: 256, 128, 256).  For 128-column tiles `variant` picks 512-token
+// tiles (NTD_TALL) or short K-steps with more workgroups per CU
+// (NTD_SHORT_K).
+enum { NTD_DEFAULT = 0, NTD_TALL = 1, NTD_SHORT_K = 2 };
+hipError_t launch_ntd(int blk, int G, bool b_kn, int variant, const NTArgs &a, hipStream_t s);
 // Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
 hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
                               void *C, int64_t ldc, hipStream_t s);
