@@ -33,6 +33,13 @@
 
 #include "pf_internal.h"
 
+// Token rows per group of the workgroup order (a group covers the token
+// tiles of PF_GROUP_ROWS rows x a run of output tiles, so both operands are
+// re-used from L2).
+#ifndef PF_GROUP_ROWS
+#define PF_GROUP_ROWS 512
+#endif
+
 namespace pf {
 namespace {
 
@@ -215,7 +222,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   const int ntn = a.ntiles;
   const int mtiles = (int)((a.M + BM - 1) / BM);
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  constexpr int GM = 8;  // grouped order: GM m-tiles x a run of n-tiles
+  constexpr int GM = PF_GROUP_ROWS / BM > 0 ? PF_GROUP_ROWS / BM : 1;  // token tiles per group
   const int split = bid / (mtiles * ntn);
   const int lin = bid % (mtiles * ntn);
   const int first_m = (lin / (GM * ntn)) * GM;
