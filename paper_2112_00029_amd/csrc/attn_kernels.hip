@@ -38,6 +38,11 @@ constexpr int LDV = D + 16;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+// 2^x on the hardware exponential unit (v_exp_f32): results below 2^-126
+// flush toward zero, which a softmax probability can afford; saves the
+// range-reduction sequence the library exp2f adds for denormal outputs.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ float bf2f_a(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 __device__ __forceinline__ bf16_t f2bf_a(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
@@ -156,25 +161,31 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
       for (int j = 0; j < 4; ++j) bmax = fmaxf(bmax, s[mt][j]);
     bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-    const float m_new = fmaxf(m_run, bmax * c);
-    const float alpha = exp2f(m_run - m_new);
+    // The softmax reference m_run moves only when some row's maximum grew by
+    // more than 8 (log2 units): until then the probabilities stay below 2^8
+    // and the rescale of O and l, a wave-uniform branch, is skipped.
+    const float m_cand = fmaxf(m_run, bmax * c);
+    if (__builtin_amdgcn_ballot_w64(m_cand > m_run + 8.0f)) {
+      const float alpha = fast_exp2(m_run - m_cand);
+      m_run = m_cand;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[dt][j] *= alpha;
+    }
     float rs = 0.f;
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        float e = exp2f(s[mt][j] * c - m_new);
+        float e = fast_exp2(s[mt][j] * c - m_run);
         s[mt][j] = e;
         rs += e;
       }
     rs += __shfl_xor(rs, 16);
     rs += __shfl_xor(rs, 32);
-    l_run = l_run * alpha + rs;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) o[dt][j] *= alpha;
+    l_run += rs;
     // O^T[dim][query] += V^T[dim][key] P^T[key][query]
     const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
 #pragma unroll
@@ -280,7 +291,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        float pr = exp2f(s[mt][j] * c - lse2);
+        float pr = fast_exp2(s[mt][j] * c - lse2);
         s[mt][j] = pr * (dp[mt][j] - delta);  // dS^T
       }
     const bf16x8 d0 = pack_perm(s[0], s[1]), d1 = pack_perm(s[2], s[3]);
@@ -378,7 +389,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int qi = mt * 16 + (lane >> 4) * 4 + j;
-        const float pr = exp2f(s[mt][j] * c - ls[cur][qi]);
+        const float pr = fast_exp2(s[mt][j] * c - ls[cur][qi]);
         s[mt][j] = pr;
         dp[mt][j] = pr * (dp[mt][j] - ds[cur][qi]);  // dS
       }
