@@ -22,6 +22,13 @@ ARCH = "gfx950"
 
 SOURCES = ["layout.cpp", "capi.cpp", "gemm_kernels.hip", "gemm_dma.hip", "attn_kernels.hip"]
 
+# Per-source extra flags.  The attention kernels feed MFMA results straight
+# into VALU softmax arithmetic: asking for the VGPR form of MFMA keeps those
+# results out of AGPRs (no accvgpr copies) and lowers register use.
+SOURCE_FLAGS = {
+    "attn_kernels.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
 FLAGS = [
     "-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
     # keep the compiler from forming packed-fp32 VALU ops
@@ -33,7 +40,7 @@ FLAGS = [
 
 def _compile(src: str, build_dir: str = BUILD, defines=()) -> str:
     obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines]]
+    cmd = [HIPCC, *FLAGS, *SOURCE_FLAGS.get(src, []), *[f"-D{d}" for d in defines]]
     if src.endswith(".cpp"):
         cmd += ["-x", "hip"]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
