@@ -569,10 +569,14 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
                     "forward kernel");
 }
 
-pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
-                             const void *dY, const void *Wblk, const void *U, const void *V,
-                             void *S, void *dX, pf_epilogue epi, const void *aux,
-                             void *workspace, size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the backward calls (everything before any enqueue).
+pf_status check_bwd_data_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                              const void *dY, const void *Wblk, const void *U, const void *V,
+                              const void *S, const void *dX, pf_epilogue epi, const void *aux) {
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
@@ -584,18 +588,38 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
     return st;
   if (epi != PF_EPI_NONE && epi != PF_EPI_GELU) return fail(PF_ERR_INVALID_ARG, "bad epilogue");
   if (epi == PF_EPI_GELU && (st = need_ptr(aux, "aux")) != PF_OK) return st;
-  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
-  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
-  if ((st = check_state(L)) != PF_OK) return st;
-  hipStream_t s = (hipStream_t)stream;
-  const int dt = (int)dtype, b = L->b;
-  if (r > 0) {
-    // S = dY U: dense over N with U read as [k][n].
-    st = dense_nt(PF_KERNEL_LOWRANK_S, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r, L->nb_out, r / b,
-                  S, r, sp.nsplit,
-                  (float *)workspace, s, "S kernel");
-    if (st != PF_OK) return st;
-  }
+  return PF_OK;
+}
+
+pf_status check_bwd_weight_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                                const void *dY, const void *X, const void *T_lr, const void *S,
+                                const void *dWblk, const void *dU, const void *dV) {
+  pf_status st = check_layout_arg(L);
+  if (st != PF_OK) return st;
+  if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = need_ptr(dY, "dY")) != PF_OK || (st = need_ptr(X, "X")) != PF_OK ||
+      (st = need_ptr(dWblk, "dWblk")) != PF_OK)
+    return st;
+  if (r > 0 && ((st = need_ptr(T_lr, "T_lr")) != PF_OK || (st = need_ptr(S, "S")) != PF_OK ||
+                (st = need_ptr(dU, "dU")) != PF_OK || (st = need_ptr(dV, "dV")) != PF_OK))
+    return st;
+  return PF_OK;
+}
+
+// S = dY U (rank-r product, dense over N with U read as [k][n]).
+pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
+                    const void *U, void *S, const SkinnyPlan &sp, float *ws, hipStream_t s) {
+  if (r <= 0) return PF_OK;
+  const int b = L->b;
+  return dense_nt(PF_KERNEL_LOWRANK_S, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r,
+                  L->nb_out, r / b, S, r, sp.nsplit, ws, s, "S kernel");
+}
+
+// dX = dY (M o W) + S V (optionally times gelu'(aux)).
+pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
+                     const void *Wblk, const void *S, const void *V, void *dX, pf_epilogue epi,
+                     const void *aux, hipStream_t s) {
+  const int b = L->b;
   pf::NTArgs a{};
   a.A = dY; a.lda = L->n_out;
   a.B = Wblk;
@@ -610,25 +634,15 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.kcols = wide ? L->d_kcols_bwd_w : L->d_kcols_bwd;
   a.blks = wide ? L->d_blks_bwd_w : L->d_blks_bwd;
   a.nsplit = 1;
-  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true, 128,
-                              L->kmax_bwd + r / b, a, s),
+  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true,
+                              128, L->kmax_bwd + r / b, a, s),
                     "backward-data kernel");
 }
 
-pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
-                               const void *dY, const void *X, const void *T_lr, const void *S,
-                               void *dWblk, void *dU, void *dV, void *workspace, size_t ws_bytes,
-                               void *stream) {
-  pf_status st = check_layout_arg(L);
-  if (st != PF_OK) return st;
-  if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
-  if ((st = need_ptr(dY, "dY")) != PF_OK || (st = need_ptr(X, "X")) != PF_OK ||
-      (st = need_ptr(dWblk, "dWblk")) != PF_OK)
-    return st;
-  if (r > 0 && ((st = need_ptr(T_lr, "T_lr")) != PF_OK || (st = need_ptr(S, "S")) != PF_OK ||
-                (st = need_ptr(dU, "dU")) != PF_OK || (st = need_ptr(dV, "dV")) != PF_OK))
-    return st;
-  if ((st = check_state(L)) != PF_OK) return st;
+// Weight-gradient work list and its token split.
+pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *dY,
+                   const void *X, const void *T_lr, const void *S, void *dWblk, void *dU,
+                   void *dV, TNPlan *plan) {
   pf::TNArgs a{};
   a.A = dY; a.lda = L->n_out;
   a.B = X; a.ldb = L->n_in;
@@ -636,21 +650,55 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
   a.T = T;
-  TNPlan p = tn_plan(pf::tn_items_total(a, L->b), T,
-                     std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
-  if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
-  a.nsplit = p.nsplit;
-  a.chunk = p.chunk;
-  a.partials = (float *)workspace;
-  hipStream_t s = (hipStream_t)stream;
+  *plan = tn_plan(pf::tn_items_total(a, L->b), T,
+                  std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
+  a.nsplit = plan->nsplit;
+  a.chunk = plan->chunk;
+  return a;
+}
+
+// dW on the mask, dU, dV (and the pass over split partials).
+pf_status enqueue_tn(const pf_layout *L, int dt, pf::TNArgs a, float *ws, hipStream_t s) {
+  a.partials = ws;
   {
     Timed t(PF_KERNEL_SDDMM, s);
-    st = hip_status(pf::launch_tn((int)dtype, L->b, a, s), "weight-gradient kernel");
+    pf_status st = hip_status(pf::launch_tn(dt, L->b, a, s), "weight-gradient kernel");
     if (st != PF_OK) return st;
   }
   if (a.nsplit <= 1) return PF_OK;
   Timed t(PF_KERNEL_REDUCE, s);
-  return hip_status(pf::launch_tn_reduce((int)dtype, L->b, a, s), "weight-gradient reduction");
+  return hip_status(pf::launch_tn_reduce(dt, L->b, a, s), "weight-gradient reduction");
+}
+
+}  // namespace
+
+extern "C" {
+
+pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                             const void *dY, const void *Wblk, const void *U, const void *V,
+                             void *S, void *dX, pf_epilogue epi, const void *aux,
+                             void *workspace, size_t ws_bytes, void *stream) {
+  pf_status st = check_bwd_data_args(L, dtype, T, r, dY, Wblk, U, V, S, dX, epi, aux);
+  if (st != PF_OK) return st;
+  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
+  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = enqueue_s(L, (int)dtype, T, r, dY, U, S, sp, (float *)workspace, s)) != PF_OK) return st;
+  return enqueue_dx(L, (int)dtype, T, r, dY, Wblk, S, V, dX, epi, aux, s);
+}
+
+pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                               const void *dY, const void *X, const void *T_lr, const void *S,
+                               void *dWblk, void *dU, void *dV, void *workspace, size_t ws_bytes,
+                               void *stream) {
+  pf_status st = check_bwd_weight_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV);
+  if (st != PF_OK) return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  TNPlan p;
+  const pf::TNArgs a = tn_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, &p);
+  if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
+  return enqueue_tn(L, (int)dtype, a, (float *)workspace, (hipStream_t)stream);
 }
 
 pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_pre, void *dH_pre,
