@@ -53,7 +53,53 @@ def parse():
     p.add_argument("--no-kernel-timing", action="store_true",
                    help="skip the per-kernel HIP events of the second region (no roofline entry)")
     p.add_argument("--calls-only", default="", help="comma list of calls to loop (profiling aid)")
+    p.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                   help="before the steps, copy MIB MiB device to device three times: a plain "
+                        "copy of known size that calibrates HBM byte counters (profiling aid)")
     return p.parse_args()
+
+
+def library_source_hash():
+    """sha256 over the library's sources (csrc/ and the public header): HBM
+    traffic taken with counters is only reported while it still matches."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2112_00029_amd", "csrc")
+    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)) + [os.path.join(ROOT, "include", "pixelfly.h")]
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of a kernel class from the committed counter
+    summaries (profiles/*traffic*.md lines of the form
+    `traffic workload=W kernel=C bytes=B fetch=F write=X source=H`), or
+    (None, reason) when none matches the current sources."""
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None, "no counter summary"
+    cur = library_source_hash()
+    stale = False
+    for f in sorted(os.listdir(pdir)):
+        if "traffic" not in f:
+            continue
+        with open(os.path.join(pdir, f)) as fh:
+            for line in fh:
+                line = line.strip().strip("`")
+                if not line.startswith("traffic "):
+                    continue
+                kv = dict(x.split("=", 1) for x in line.split()[1:] if "=" in x)
+                if kv.get("workload") != workload or kv.get("kernel") != kernel:
+                    continue
+                if kv.get("source") != cur:
+                    stale = True
+                    continue
+                return {"bytes": float(kv["bytes"]), "fetch": float(kv["fetch"]),
+                        "write": float(kv["write"]), "file": f}, None
+    return None, ("kernel sources changed since the counters were taken" if stale else "no counter summary")
 
 
 def dev_bf16(torch, raw):
@@ -417,6 +463,16 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention}[wl.kind](torch, pf, wl)
 
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     calls = [c for c in args.calls_only.split(",") if c] or R.calls
     if "dense" in calls:  # profiling aid: the dense comparator step as one call
         R.dense_setup()
@@ -487,7 +543,13 @@ def main():
             else:
                 roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
         roof["frac"] = roof["achieved"] / roof["peak"]
-        roof["traffic"] = None
+        tr, why = measured_traffic(wl.name, dom)
+        roof["traffic"] = tr["bytes"] if tr else None
+        if tr:
+            roof["traffic_detail"] = {"fetch_bytes": tr["fetch"], "write_bytes": tr["write"],
+                                      "over_algorithmic": tr["bytes"] / by, "source": "profiles/" + tr["file"]}
+        else:
+            roof["traffic_detail"] = why
         roof.update({"kernel": dom, "avg_launch_ms": cand[dom]["avg_ms"], "launches_per_step": lps,
                      "algorithmic_bytes_per_launch": by, "flops_per_launch": fl,
                      "flop_per_byte": ai,
