@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libpixelfly.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["layout.cpp", "capi.cpp", "gemm_kernels.hip", "gemm_dma.hip", "attn_kernels.hip"]
+SOURCES = ["layout.cpp", "capi.cpp", "gemm_kernels.hip", "gemm_dma.hip", "skinny.hip", "attn_kernels.hip"]
 
 # Per-source extra flags.  The attention kernels feed MFMA results straight
 # into VALU softmax arithmetic: asking for the VGPR form of MFMA keeps those

@@ -183,6 +183,28 @@ pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int
   return hip_status(pf::launch_reduce_rows(dtype, nsplit, ws, M, (int64_t)nblk * blk, C, ldc, s), what);
 }
 
+// The bf16 rank-r kernel (32-token x 64-column workgroups, no split) runs a
+// product when 128 x 128 tiles would cover less than a quarter of the CUs
+// (those then need a deep K split, fp32 partials and a reduction pass).
+// With more tiles the tile kernel re-reads the small operand far less and
+// measured faster (4096 tokens, r = 96: rank-r kernel; 8192 tokens,
+// r = 128: tiles).
+bool use_skinny(int dtype, int64_t T, int r) {
+  return dtype == 0 && r > 0 && ((T + 127) / 128) * ((r + 127) / 128) < 64;
+}
+
+// bf16 rank-r product C[M x r] = A[M x K] . op(B) on the rank-r kernel
+// (B [n][k] for V, [k][n] for U); one launch, no workspace.
+pf_status skinny_bf16(pf_kernel_class kc, bool b_kn, int64_t M, const void *A, int64_t lda,
+                      const void *B, int64_t ldb, int K, int r, void *C, hipStream_t s,
+                      const char *what) {
+  pf::SkinnyArgs a{};
+  a.A = A; a.lda = lda; a.B = B; a.ldb = ldb; a.C = C; a.ldc = r;
+  a.M = M; a.K = K; a.ncols = r;
+  Timed t(kc, s);
+  return hip_status(pf::launch_skinny(b_kn, a, s), what);
+}
+
 // Workgroups a launch aims for (2 per CU on 256 CUs) before splitting K.
 #ifndef PF_WG_TARGET
 #define PF_WG_TARGET 512
@@ -205,7 +227,7 @@ struct SkinnyPlan {
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0};
-  if (r <= 0) return p;
+  if (r <= 0 || use_skinny(dtype, T, r)) return p;  // the rank-r kernel needs no split
   const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + 127) / 128;
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
   int64_t ns;
@@ -543,7 +565,11 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   const int dt = (int)dtype, b = L->b;
-  if (r > 0) {
+  if (use_skinny(dt, T, r)) {
+    st = skinny_bf16(PF_KERNEL_LOWRANK_T, false, T, X, L->n_in, V, L->n_in, (int)L->n_in, r, T_lr,
+                     s, "T_lr kernel");
+    if (st != PF_OK) return st;
+  } else if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
     st = dense_nt(PF_KERNEL_LOWRANK_T, dt, b, 128 / b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
                   r / b, T_lr, r, sp.nsplit,
@@ -610,6 +636,9 @@ pf_status check_bwd_weight_args(const pf_layout *L, pf_dtype dtype, int64_t T, i
 pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
                     const void *U, void *S, const SkinnyPlan &sp, float *ws, hipStream_t s) {
   if (r <= 0) return PF_OK;
+  if (use_skinny(dt, T, r))
+    return skinny_bf16(PF_KERNEL_LOWRANK_S, true, T, dY, L->n_out, U, r, (int)L->n_out, r, S, s,
+                       "S kernel");
   const int b = L->b;
   return dense_nt(PF_KERNEL_LOWRANK_S, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r,
                   L->nb_out, r / b, S, r, sp.nsplit, ws, s, "S kernel");

@@ -99,6 +99,17 @@ __device__ __forceinline__ void dma16(rsrc_t r, uint8_t *lds, uint32_t voff, uin
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, (int)voff, (int)soff, 0, 0);
 }
 
+// Load of work-list metadata (tile lists, column and block indices) through
+// the constant address space: these arrays do not change while a kernel
+// runs, and such loads always use the scalar unit.  A generic load of them
+// after an operand copy becomes a vector load (the copy counts as a
+// possible writer), and its vmcnt wait then also waits for every copy in
+// flight: the A copies of a step would land before its B copies issue.
+template <typename T>
+__device__ __forceinline__ T ld_meta(const T *p) {
+  return *(const __attribute__((address_space(4))) T *)p;
+}
+
 // Wait until at most VM vector-memory operations of this wave are in flight
 // and all of its LDS reads have returned.
 template <int VM>
@@ -237,14 +248,14 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     g_valid = min(G, a.dense_nblk - nt * G);
     nsteps = a.dense_nsteps;
   } else {
-    g_valid = tile->g;
-    nsteps = tile->nsteps;
-    kcol_off = tile->kcol_off;
-    blk_off = tile->blk_off;
+    g_valid = ld_meta(&tile->g);
+    nsteps = ld_meta(&tile->nsteps);
+    kcol_off = ld_meta(&tile->kcol_off);
+    blk_off = ld_meta(&tile->blk_off);
   }
   auto out_blk = [&](int g) __attribute__((always_inline)) -> int {
     if constexpr (DENSE) return nt * G + min(g, g_valid - 1);
-    else return tile->out_blk[g];
+    else return ld_meta(&tile->out_blk[g]);
   };
   const int vblocks = nsteps + a.nlr;
   const int total_all = (vblocks * BLK + BK - 1) / BK;
@@ -264,7 +275,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
                    uint32_t &colb) __attribute__((always_inline)) {
     const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
     const bool sp = c < nsteps;
-    const int kcol = DENSE ? c : a.kcols[kcol_off + min(c, nsteps - 1)];
+    const int kcol = DENSE ? c : ld_meta(&a.kcols[kcol_off + min(c, nsteps - 1)]);
     base = sp ? a_base : l_base;
     bytes = sp ? a_bytes : (c < vblocks ? l_bytes : 0);
     ldb = (uint32_t)((sp ? a.lda : a.ldl) * 2);
@@ -282,7 +293,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       bytes = c < nsteps ? BIG : 0;
     } else {
       const bool sp = c < nsteps;
-      const int64_t blk = a.blks[blk_off + min(c, nsteps - 1) * G + g];
+      const int64_t blk = ld_meta(&a.blks[blk_off + min(c, nsteps - 1) * G + g]);
       const int cr = c - nsteps;
       const bf16_t *sp_base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
       const bf16_t *lr_base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
@@ -320,7 +331,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   auto issue = [&](int t, uint8_t *sb) __attribute__((always_inline)) {
     {
       const int wa0 = w * AWW;
-      const int h = wa0 / WPH, wr0 = wa0 % WPH;
+      const int h = __builtin_amdgcn_readfirstlane(wa0 / WPH), wr0 = wa0 % WPH;
       const bf16_t *base;
       int64_t bytes;
       uint32_t ldb, colb;
@@ -337,7 +348,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     constexpr int WIN = BWW > WPP ? WPP : BWW;      // windows per piece and wave
     sfor<PPW>([&](auto pi) __attribute__((always_inline)) {
       const int wb0 = w * BWW + pi * WIN;
-      const int piece = wb0 / WPP, wi0 = wb0 % WPP;
+      // Uniform; readfirstlane lets the block lookups stay scalar loads.
+      const int piece = __builtin_amdgcn_readfirstlane(wb0 / WPP), wi0 = wb0 % WPP;
       const bf16_t *base;
       int64_t bytes;
       uint32_t ldb;

@@ -96,6 +96,20 @@ __device__ __forceinline__ bf16x8 frag_kmajor(const bf16_t *base, int ld,
   return cat8(tr16(p), tr16(p + 4 * ld));
 }
 
+// Same fragment from an unpadded [k][128] tile (256-byte k rows) whose
+// 16-byte chunks are XOR-swizzled by k: chunk c of k row k sits at chunk
+// c ^ ((k & 3) << 2).  The four k rows one 16-lane group reads then fall in
+// four different 64-byte bank groups (no LDS bank conflicts).
+__device__ __forceinline__ int swz128(int k, int col) {
+  return k * 128 + ((((col >> 3) ^ ((k & 3) << 2)) << 3) | (col & 7));
+}
+__device__ __forceinline__ bf16x8 frag_kmajor_swz(const bf16_t *base, int ks, int row0, int lane) {
+  const int g16 = lane >> 4, i = lane & 15;
+  const int k = ks * 16 + (g16 >> 1) * 8 + (i >> 2);
+  const int col = row0 + (g16 & 1) * 16 + (i & 3) * 4;
+  return cat8(tr16(base + swz128(k, col)), tr16(base + swz128(k + 4, col)));
+}
+
 // MFMA (32x32x16) fragment of a 32-row operand stored [row][k] in LDS.
 __device__ __forceinline__ bf16x8 frag_rmajor(const bf16_t *base, int ld,
                                               int ks, int row0, int lane) {
@@ -196,7 +210,10 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
   constexpr int NH = BK / KW;                // sub-blocks per step (2: bf16, b = 32)
   constexpr int PADA = BF ? 8 : 4;
   constexpr int LDA_S = BK + PADA;
-  constexpr int LDB_S = BKN ? (BN + (BF ? 16 : 4)) : (BK + PADA);
+  // B read as [k][n]: a 32-column bf16 tile keeps unpadded 64-byte k rows
+  // (the four k rows of each 16-lane transpose read, and the two 16-lane
+  // groups of a half-wave, then cover distinct banks); wider tiles pad.
+  constexpr int LDB_S = BKN ? (BN + (BF ? (BN == 32 ? 0 : 16) : 4)) : (BK + PADA);
   constexpr int A_ELEMS = BM * LDA_S;
   constexpr int B_ELEMS = BKN ? BK * LDB_S : BN * LDB_S;
   constexpr int WNN = BN == 32 ? 1 : 2;      // waves along N
@@ -565,14 +582,19 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
   constexpr int GT = 128 / BLK;  // blocks per tile side
   constexpr int BKT = BF ? 64 : 32, TILE = 128;
   constexpr int VEC = 16 / (int)sizeof(T);
-  constexpr int LDS_S = TILE + (BF ? 16 : 4);
+  constexpr int LDS_S = TILE + (BF ? 0 : 4);  // bf16: unpadded, chunk-swizzled rows
   constexpr int OP_ELEMS = BKT * LDS_S;
   constexpr int CPB = BKT * BLK / VEC;  // chunks of one block column slab
   constexpr int CH = GT * CPB, LD = CH / 256;
   constexpr int TM = 2, TN = 2;  // 4 waves as 2 x 2, 64 x 64 each
   static_assert(CPB % 256 == 0 && LD <= 8, "chunking");
 
-  __shared__ __attribute__((aligned(16))) T smem[2 * 2 * OP_ELEMS];
+  // Two stages of both operands; the fp32 epilogue tile (128 x 132) reuses
+  // the same memory.
+  constexpr int SMEM_ELEMS = 2 * 2 * OP_ELEMS > TILE * (TILE + 4) * 4 / (int)sizeof(T)
+                                 ? 2 * 2 * OP_ELEMS
+                                 : TILE * (TILE + 4) * 4 / (int)sizeof(T);
+  __shared__ __attribute__((aligned(16))) T smem[SMEM_ELEMS];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -624,8 +646,9 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
       constexpr int g = (i * 256) / CPB;
       const int r = (tid + i * 256) % CPB;
       const int t = r / (BLK / VEC), c = g * BLK + (r % (BLK / VEC)) * VEC;
-      *(u32x4 *)(As + t * LDS_S + c) = ra.template at<i>();
-      *(u32x4 *)(Bs + t * LDS_S + c) = rb.template at<i>();
+      const int o = BF ? swz128(t, c) : t * LDS_S + c;
+      *(u32x4 *)(As + o) = ra.template at<i>();
+      *(u32x4 *)(Bs + o) = rb.template at<i>();
     });
   };
 
@@ -644,10 +667,10 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
       static_for<BKT / 16>([&](auto ks) __attribute__((always_inline)) {
         bf16x8 af[TM], bfg[TN];
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
-          af[tm] = frag_kmajor((const bf16_t *)As, LDS_S, ks, wm * 64 + tm * 32, lane);
+          af[tm] = frag_kmajor_swz((const bf16_t *)As, ks, wm * 64 + tm * 32, lane);
         });
         static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-          bfg[tn] = frag_kmajor((const bf16_t *)Bs, LDS_S, ks, wn * 64 + tn * 32, lane);
+          bfg[tn] = frag_kmajor_swz((const bf16_t *)Bs, ks, wn * 64 + tn * 32, lane);
         });
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {

@@ -113,6 +113,19 @@ struct TNArgs {
   float *partials;      // [items_total][nsplit][128*128] when nsplit > 1
 };
 
+// Rank-r product C[M x ncols] = A[M x K] . op(B) (bf16, skinny.hip):
+// B is ncols x K ([n][k], V) or K x ncols ([k][n], U), row stride ldb.
+struct SkinnyArgs {
+  const void *A;
+  int64_t lda;
+  const void *B;
+  int64_t ldb;
+  void *C;
+  int64_t ldc;
+  int64_t M;
+  int K, ncols;
+};
+
 struct AttnArgs {
   const void *Q, *K, *V, *O, *dO;
   void *Oout, *dQ, *dK, *dV;
@@ -142,6 +155,7 @@ hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, 
 hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
 hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s);
 int tn_items_total(const TNArgs &a, int blk);
+hipError_t launch_skinny(bool b_kn, const SkinnyArgs &a, hipStream_t s);
 hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
                            const void *Hpre, void *out, hipStream_t s);
 hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s);

@@ -105,6 +105,9 @@ CASES = [
     pytest.param(16384, 4096, 128, 32, 200, 256, "bf16", id="large_b128_T200"),
     pytest.param(16384, 4096, 64, 32, 200, 256, "bf16", id="large_b64_T200"),
     pytest.param(16384, 4096, 32, 32, 200, 256, "bf16", id="large_b32_T200"),
+    # rank-r kernel edges: r = 32 (half of a 64-column tile past r), K and N
+    # = 32 mod 64 (the last 64-wide step half outside), 3 steps for 4 waves
+    pytest.param(480, 160, 32, 4, 70, 32, "bf16", id="rank32_K160_N480_T70"),
     pytest.param(512, 512, 32, 1, 130, 0, "bf16", id="blockdiag_r0"),
     pytest.param(128, 128, 64, 2, 1, 64, "bf16", id="dense_mask_T1"),
     pytest.param(384, 640, 64, 1024, 77, 64, "bf16", id="clamped_stride_rect"),
