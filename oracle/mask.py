@@ -132,3 +132,33 @@ def layout(n_out: int, n_in: int, b: int, max_stride: int):
     assert n_out % b == 0 and n_in % b == 0
     M = stretch_block_mask(n_out // b, n_in // b, max_stride)
     return M, block_csr(M)
+
+
+def global_block_mask(nb: int, global_blocks: int) -> np.ndarray:
+    """The "global" component of the attention mask (appendix on method
+    details, low-rank in attention), in block units: a horizontal stripe (the
+    first `global_blocks` block rows: those queries attend to every key) and
+    a vertical stripe (the first `global_blocks` block columns: every query
+    attends to those keys).  With stripe width w = global_blocks * b, any
+    matrix supported on it is the sum of one supported on w rows and one on
+    w columns, so its rank is at most 2w: the restricted low-rank term.
+    Reading: the stripes sit at the start of the sequence."""
+    assert 0 <= global_blocks <= nb
+    G = np.zeros((nb, nb), dtype=bool)
+    G[:global_blocks, :] = True
+    G[:, :global_blocks] = True
+    return G
+
+
+def attention_block_mask(nb: int, max_stride: int, global_blocks: int = 0) -> np.ndarray:
+    """Attention score mask: flat block butterfly (square, nb x nb block
+    units) plus the global stripes, as a union of supports (the paper adds
+    the sparse and the low-rank parts)."""
+    return square_block_mask(nb, max_stride) | global_block_mask(nb, global_blocks)
+
+
+def attention_layout(seq: int, b: int, max_stride: int, global_blocks: int = 0):
+    """Block mask and block-CSR of the attention mask for sequence length seq."""
+    assert seq % b == 0
+    M = attention_block_mask(seq // b, max_stride, global_blocks)
+    return M, block_csr(M)
