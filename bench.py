@@ -344,7 +344,7 @@ class Attention:
     def __init__(self, torch, pf, wl, seed=0):
         self.torch, self.pf, self.wl, self.dtype = torch, pf, wl, "bf16"
         B, H, S, d = wl.B, wl.H, wl.S, wl.d
-        self.L = pf.pf_layout_create(S, S, wl.b, wl.max_stride)
+        self.L = pf.pf_layout_create_attention(S, wl.b, wl.max_stride, wl.global_blocks)
         pf.pf_layout_upload(self.L)
         self.nnzb = pf.pf_layout_info_get(self.L)["nnzb"]
         dr = lambda s: dev_bf16(torch, synth.draw((B, H, S, d), 1.0, seed, s, "bf16")[1])
@@ -400,7 +400,7 @@ class Attention:
         from oracle import attention as oa
         from oracle import mask as om
         wl = self.wl
-        M, _ = om.layout(wl.S, wl.S, wl.b, wl.max_stride)
+        M, _ = om.attention_layout(wl.S, wl.b, wl.max_stride, wl.global_blocks)
         Mel = om.element_mask(M, wl.b)
         g = lambda s: synth.draw((1, 1, wl.S, wl.d), 1.0, 0, s, "bf16")[0][0, 0]
         Q, K, V, dO = g(11), g(12), g(13), g(14)
@@ -562,7 +562,8 @@ def main():
 
     cfg = {"workload": wl.name}
     if wl.kind == "attention":
-        cfg.update(B=wl.B, H=wl.H, S=wl.S, d=wl.d, b=wl.b, max_stride=wl.max_stride)
+        cfg.update(B=wl.B, H=wl.H, S=wl.S, d=wl.d, b=wl.b, max_stride=wl.max_stride,
+                   global_blocks=wl.global_blocks)
     else:
         cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=wl.max_stride, r=wl.r)
     out = {

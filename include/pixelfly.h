@@ -113,6 +113,23 @@ pf_status pf_layout_create(int64_t n_out, int64_t n_in, int32_t b,
 pf_status pf_layout_create_from_mask(int32_t nb_out, int32_t nb_in, int32_t b,
                                      const uint8_t *block_mask, pf_layout **out);
 
+/*
+ * Attention score layout for a sequence of seq tokens, block size b: the
+ * square flat block butterfly of side seq / b (as pf_layout_create with
+ * n_out = n_in = seq) plus the "global" component of the appendix on method
+ * details (low-rank in attention): block rows and block columns
+ * 0 .. global_blocks-1 are kept whole, i.e. the first global_blocks * b
+ * queries attend to every key and every query attends to the first
+ * global_blocks * b keys (stripes of width w = global_blocks * b, a term of
+ * rank at most 2w).  global_blocks = 0 gives the plain butterfly mask.  The
+ * layout serves pf_attn_fwd / pf_attn_bwd (which need b = 64).
+ * Requires b >= 1 dividing seq, seq / b <= 16384, max_stride a power of two
+ * >= 1, 0 <= global_blocks <= seq / b.  Host only; *out receives a new
+ * layout (free with pf_layout_destroy).  Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_layout_create_attention(int64_t seq, int32_t b, int32_t max_stride,
+                                     int32_t global_blocks, pf_layout **out);
+
 /* Fill *out with host views of the layout.  Errors: INVALID_ARG. */
 pf_status pf_layout_info_get(const pf_layout *layout, pf_layout_info *out);
 

@@ -107,6 +107,21 @@ struct Tile64 {
 };
 
 // ---------------------------------------------------------------------------
+// Work order: (head, block) of logical id L.  Block rows (or, for dK/dV,
+// block columns) below nlong are the global stripes of the mask, which keep
+// every block of the other side: they go first, over all heads, so that the
+// long workgroups do not trail the launch; the rest follow head by head.
+__device__ __forceinline__ void attn_order(int L, int BH, int nb, int nlong, int &bh, int &blk) {
+  if (L < nlong * BH) {
+    blk = L / BH;
+    bh = L % BH;
+  } else {
+    const int r = L - nlong * BH, m = nb - nlong;
+    bh = r / m;
+    blk = nlong + r % m;
+  }
+}
+
 // Forward
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
@@ -115,7 +130,8 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
-  const int bh = bid / a.nbq, qb = bid % a.nbq;
+  int bh, qb;
+  attn_order(bid, a.BH, a.nbq, a.nlong, bh, qb);
   const int64_t head = (int64_t)bh * a.S * D;
   const bf16_t *Q = (const bf16_t *)a.Q + head;
   const bf16_t *K = (const bf16_t *)a.K + head;
@@ -222,7 +238,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
-  const int bh = bid / a.nbq, qb = bid % a.nbq;
+  int bh, qb;
+  attn_order(bid, a.BH, a.nbq, a.nlong, bh, qb);
   const int64_t head = (int64_t)bh * a.S * D;
   const bf16_t *Q = (const bf16_t *)a.Q + head;
   const bf16_t *K = (const bf16_t *)a.K + head;
@@ -327,7 +344,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
-  const int bh = bid / a.nbq, kb = bid % a.nbq;
+  int bh, kb;
+  attn_order(bid, a.BH, a.nbq, a.nlong, bh, kb);
   const int64_t head = (int64_t)bh * a.S * D;
   const bf16_t *Q = (const bf16_t *)a.Q + head;
   const bf16_t *K = (const bf16_t *)a.K + head;

@@ -407,6 +407,30 @@ pf_status pf_layout_create_from_mask(int32_t nb_out, int32_t nb_in, int32_t b,
   return PF_OK;
 }
 
+pf_status pf_layout_create_attention(int64_t seq, int32_t b, int32_t max_stride,
+                                     int32_t global_blocks, pf_layout **out) {
+  if (!out) return fail(PF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  pf_layout *L = new (std::nothrow) pf_layout();
+  if (!L) return fail(PF_ERR_NOMEM, "host allocation failed");
+  std::string e;
+  try {
+    e = pf::build_attention_layout(*L, seq, b, max_stride, global_blocks);
+  } catch (const std::bad_alloc &) {
+    delete L;
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  } catch (...) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, "layout build failed");
+  }
+  if (!e.empty()) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, e);
+  }
+  *out = L;
+  return PF_OK;
+}
+
 pf_status pf_layout_info_get(const pf_layout *L, pf_layout_info *o) {
   if (!L || !o) return fail(PF_ERR_INVALID_ARG, "NULL argument");
   o->n_out = L->n_out;
@@ -767,6 +791,7 @@ pf_status pf_attn_fwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
   pf::AttnArgs a{};
   a.Q = Q; a.K = K; a.V = V; a.Oout = O; a.lse = lse;
   a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
+  a.nlong = L->global_blocks;
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
   Timed t(PF_KERNEL_ATTN_FWD, (hipStream_t)stream);
@@ -799,6 +824,7 @@ pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
   a.dQ = dQ; a.dK = dK; a.dV = dV;
   a.lse_in = lse; a.delta = (float *)workspace;
   a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
+  a.nlong = L->global_blocks;
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
   hipStream_t s = (hipStream_t)stream;

@@ -188,6 +188,34 @@ std::string build_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
   return finish_layout(L);
 }
 
+// Attention score layout: the square flat block butterfly of the sequence
+// (block units nb = seq / b) plus the global component of the appendix on
+// method details (low-rank in attention): the first global_blocks block rows
+// (queries that attend to every key) and block columns (keys every query
+// attends to), as a union of supports.
+std::string build_attention_layout(pf_layout &L, int64_t seq, int32_t b, int32_t max_stride,
+                                   int32_t global_blocks) {
+  if (b < 1 || seq < 1 || seq % b) return "seq must be a positive multiple of b";
+  if (seq / b > 16384) return "seq / b must be <= 16384";
+  const int32_t nb = (int32_t)(seq / b);
+  if (global_blocks < 0 || global_blocks > nb) return "global_blocks must be in [0, seq / b]";
+  pf_layout sq;
+  std::string e = build_layout(sq, seq, seq, b, max_stride);
+  if (!e.empty()) return e;
+  std::vector<uint8_t> m((size_t)nb * nb, 0);
+  for (int32_t i = 0; i < nb; ++i) {
+    for (int32_t p = sq.row_ptr[i]; p < sq.row_ptr[i + 1]; ++p) m[(size_t)i * nb + sq.col_idx[p]] = 1;
+    for (int32_t j = 0; j < nb; ++j)
+      if (i < global_blocks || j < global_blocks) m[(size_t)i * nb + j] = 1;
+  }
+  e = build_layout_from_mask(L, nb, nb, b, m.data());
+  if (!e.empty()) return e;
+  L.max_stride = sq.max_stride;
+  L.eff_stride = sq.eff_stride;
+  L.global_blocks = global_blocks;
+  return "";
+}
+
 std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, int32_t b,
                                    const uint8_t *mask) {
   if (b < 1) return "block size b must be >= 1";

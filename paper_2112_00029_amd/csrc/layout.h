@@ -10,6 +10,7 @@
 struct pf_layout {
   int64_t n_out = 0, n_in = 0;
   int32_t b = 0, max_stride = 0, eff_stride = 0, s = 0, nb_out = 0, nb_in = 0;
+  int32_t global_blocks = 0;  // attention layouts: width of the global stripes (blocks)
   int64_t nnzb = 0;
   std::vector<int32_t> row_ptr, col_idx, col_ptr, row_idx, tperm;
 
@@ -47,6 +48,10 @@ std::string build_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
 // kept); every block row must keep at least one block.
 std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, int32_t b,
                                    const uint8_t *mask);
+// Attention layout: square flat block butterfly of side seq / b plus the
+// first global_blocks block rows and columns.
+std::string build_attention_layout(pf_layout &L, int64_t seq, int32_t b, int32_t max_stride,
+                                   int32_t global_blocks);
 std::string finish_layout(pf_layout &L);
 // Re-verify the work lists against the block-CSR.  Returns "" or an error.
 std::string check_layout(const pf_layout &L);

@@ -133,6 +133,7 @@ struct AttnArgs {
   const float *lse_in;
   float *delta;
   int BH, S, nbq;
+  int nlong;            // leading block rows / columns kept whole (global stripes)
   float scale;
   const int32_t *row_ptr, *col_idx, *col_ptr, *row_idx;
 };

@@ -67,6 +67,7 @@ class pf_layout_info(ctypes.Structure):
 _SIGS = {
     "pf_layout_create": (_i32, [_i64, _i64, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_create_from_mask": (_i32, [_i32, _i32, _i32, _p, ctypes.POINTER(_p)]),
+    "pf_layout_create_attention": (_i32, [_i64, _i32, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_info_get": (_i32, [_p, ctypes.POINTER(pf_layout_info)]),
     "pf_layout_check": (_i32, [_p]),
     "pf_layout_plan_get": (_i32, [_p, ctypes.POINTER(_i32), _i32]),
@@ -170,6 +171,12 @@ def pf_layout_create_from_mask(nb_out: int, nb_in: int, b: int, block_mask) -> L
         raise ValueError(f"block_mask shape {m.shape} != ({nb_out}, {nb_in})")
     h = _p()
     _check(_lib.pf_layout_create_from_mask(nb_out, nb_in, b, m.ctypes.data_as(_p), ctypes.byref(h)))
+    return Layout(h.value)
+
+
+def pf_layout_create_attention(seq: int, b: int, max_stride: int, global_blocks: int = 0) -> Layout:
+    h = _p()
+    _check(_lib.pf_layout_create_attention(seq, b, max_stride, global_blocks, ctypes.byref(h)))
     return Layout(h.value)
 
 

@@ -72,6 +72,7 @@ class Workload:
     H: int = 0                # attention heads
     S: int = 0                # attention sequence length
     d: int = 0                # attention head dim
+    global_blocks: int = 0    # attention: width of the global stripes, in blocks
     seed: int = 0
 
 
@@ -96,6 +97,11 @@ WORKLOADS = {
     "attn_8x12x4096x64": Workload(
         "attn_8x12x4096x64", "attention", "bf16", B=8, H=12, S=4096, d=64,
         b=64, max_stride=64, std_x=1.0, std_dy=1.0),
+    # The same attention with the global component: the first 64 queries
+    # attend to every key and every query attends to the first 64 keys.
+    "attn_global_8x12x4096x64": Workload(
+        "attn_global_8x12x4096x64", "attention", "bf16", B=8, H=12, S=4096, d=64,
+        b=64, max_stride=64, std_x=1.0, std_dy=1.0, global_blocks=1),
     # Large layer 4096 -> 16384, 16384 tokens, 128x128 blocks, strides < 32.
     "linear_16384x4096_b128": Workload(
         "linear_16384x4096_b128", "linear", "bf16", T=16384, K=4096, N=16384,

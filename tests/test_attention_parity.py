@@ -11,17 +11,17 @@ from tests._gpu_util import TOL, empty, rel_fro, to_dev, to_host, torch_cuda
 pytestmark = pytest.mark.gpu
 
 
-def _run(B, H, S, ms, heads, seed=0, check_bwd=True):
+def _run(B, H, S, ms, heads, seed=0, check_bwd=True, g=0):
     torch = torch_cuda()
     from paper_2112_00029_amd import pixelfly as pf
     d, b = 64, 64
-    print(f"[attn] B={B} H={H} S={S} ms={ms}", flush=True)
+    print(f"[attn] B={B} H={H} S={S} ms={ms} global_blocks={g}", flush=True)
     Q, Qr = synth.draw((B, H, S, d), 1.0, seed, 11, "bf16")
     K, Kr = synth.draw((B, H, S, d), 1.0, seed, 12, "bf16")
     V, Vr = synth.draw((B, H, S, d), 1.0, seed, 13, "bf16")
     dO, dOr = synth.draw((B, H, S, d), 1.0, seed, 14, "bf16")
     scale = 1.0 / np.sqrt(d)
-    L = pf.pf_layout_create(S, S, b, ms)
+    L = pf.pf_layout_create_attention(S, b, ms, g)
     pf.pf_layout_upload(L)
     q, k, v, do = to_dev(Qr), to_dev(Kr), to_dev(Vr), to_dev(dOr)
     O = empty((B, H, S, d), "bf16")
@@ -32,7 +32,7 @@ def _run(B, H, S, ms, heads, seed=0, check_bwd=True):
     ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
     pf.pf_attn_bwd(L, B, H, S, d, scale, q, k, v, O, lse, do, dQ, dK, dV, ws, wsb)
     torch.cuda.synchronize()
-    M, _ = om.layout(S, S, b, ms)
+    M, _ = om.attention_layout(S, b, ms, g)
     Mel = om.element_mask(M, b)
     Og, lg = to_host(O), lse.cpu().numpy().astype(np.float64)
     dQg, dKg, dVg = to_host(dQ), to_host(dK), to_host(dV)
@@ -70,3 +70,19 @@ def test_attention_block_diagonal():
 
 def test_attention_small_stride():
     _run(2, 2, 1024, 4, heads=[(0, 1), (1, 0)])
+
+
+def test_attention_global_component_full_sequence():
+    """Butterfly + one 64-wide global stripe (appendix on method details,
+    low-rank in attention): the first query block attends to all 64 key
+    blocks, every query to the first key block; sequence 4096."""
+    _run(2, 3, 4096, 64, heads=[(0, 0), (1, 2)], g=1)
+
+
+def test_attention_global_workload_shape():
+    """The attn_global_8x12x4096x64 benchmark configuration, sampled heads."""
+    _run(8, 12, 4096, 64, heads=[(3, 5)], g=1)
+
+
+def test_attention_global_wide_stripes_small_stride():
+    _run(1, 2, 1024, 4, heads=[(0, 0), (0, 1)], g=3)

@@ -186,3 +186,24 @@ def test_timing_hook_errors_before_any_hip_call():
         pf.pf_timing_end()
     assert e.value.status == pf.PF_ERR_STATE
     assert len(pf.KERNEL_CLASSES) == pf.PF_KERNEL_COUNT == 11
+
+
+@pytest.mark.parametrize("seq,b,ms,g", [(4096, 64, 64, 1), (4096, 64, 64, 2), (512, 64, 8, 1),
+                                        (1536, 64, 16, 3), (256, 32, 4, 0), (640, 64, 1024, 10)])
+def test_attention_layout_bit_exact_vs_oracle(seq, b, ms, g):
+    """Flat butterfly + global stripes: the C++ builder against the oracle's
+    independently built union of supports."""
+    L = pf.pf_layout_create_attention(seq, b, ms, g)
+    info = pf.pf_layout_info_get(L)
+    M, ref = om.attention_layout(seq, b, ms, g)
+    for name, r in zip(["row_ptr", "col_idx", "col_ptr", "row_idx", "tperm"], ref):
+        assert np.array_equal(info[name], r), name
+    assert info["nnzb"] == M.sum()
+    pf.pf_layout_check(L)
+
+
+def test_attention_layout_errors():
+    for args in [(4096, 64, 64, -1), (4096, 64, 64, 65), (4000, 64, 64, 1), (4096, 64, 3, 1),
+                 (64 * 20000, 64, 64, 1)]:
+        with pytest.raises(pf.PixelflyError):
+            pf.pf_layout_create_attention(*args)
