@@ -130,6 +130,27 @@ pf_status pf_layout_create_from_mask(int32_t nb_out, int32_t nb_in, int32_t b,
 pf_status pf_layout_create_attention(int64_t seq, int32_t b, int32_t max_stride,
                                      int32_t global_blocks, pf_layout **out);
 
+/*
+ * Mask selection for one layer from a compute budget (Section 3.3, step 2):
+ * a share lowrank_share of the budget (the paper's rule of thumb: one
+ * quarter to one third) goes to the low-rank part, whose rank is the largest
+ * multiple of the block size b within that share (and at most min(n_out,
+ * n_in)); the rest selects the maximum stride of the flat block butterfly:
+ * the largest power of two whose kept entries plus the low-rank entries
+ * stay within the budget ("fill up the budget"), at least 1 (block
+ * diagonal), at most the next power of two of s = min(n_out, n_in) / b.
+ * Cost unit: weight entries, kept b x b blocks plus r (n_out + n_in),
+ * against budget * n_out * n_in (per-token FLOPs are twice the entries).
+ * budget in (0, 1], lowrank_share in [0, 1]; b >= 1 must divide n_out and
+ * n_in.  Outputs: *r_out (rank), *max_stride_out, and (if not NULL)
+ * *params_out, the entries of the chosen configuration (which exceed the
+ * budget only when even the block diagonal does).  Host only.
+ * Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_select_mask(int64_t n_out, int64_t n_in, int32_t b, double budget,
+                         double lowrank_share, int32_t *r_out, int32_t *max_stride_out,
+                         int64_t *params_out);
+
 /* Fill *out with host views of the layout.  Errors: INVALID_ARG. */
 pf_status pf_layout_info_get(const pf_layout *layout, pf_layout_info *out);
 

@@ -17,9 +17,11 @@ Modules
              (Section 3.3 parameterisation; gradient Lemma in the appendix on
              gradient computation, sparse training algorithm).
   attention  block-sparse softmax attention forward/backward, dense masked.
+  select     rank and maximum stride from a compute budget (Section 3.3,
+             mask selection step).
 
 Parity pins: every function here is pinned by a CPU test against a hand-made
 fixture, a closed form, a special case that reduces to a library routine or
 finite differences; none is "parity unpinned".
 """
-from . import mask, butterfly, linear, attention  # noqa: F401
+from . import mask, butterfly, linear, attention, select  # noqa: F401

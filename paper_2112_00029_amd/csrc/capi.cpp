@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <cstdio>
 #include <cstring>
@@ -428,6 +429,48 @@ pf_status pf_layout_create_attention(int64_t seq, int32_t b, int32_t max_stride,
     return fail(PF_ERR_INVALID_ARG, e);
   }
   *out = L;
+  return PF_OK;
+}
+
+pf_status pf_select_mask(int64_t n_out, int64_t n_in, int32_t b, double budget,
+                         double lowrank_share, int32_t *r_out, int32_t *max_stride_out,
+                         int64_t *params_out) {
+  if (!r_out || !max_stride_out) return fail(PF_ERR_INVALID_ARG, "NULL output");
+  if (b < 1 || n_out < b || n_in < b || n_out % b || n_in % b)
+    return fail(PF_ERR_INVALID_ARG, "b must be >= 1 and divide n_out and n_in");
+  if (!(budget > 0.0 && budget <= 1.0)) return fail(PF_ERR_INVALID_ARG, "budget must be in (0, 1]");
+  if (!(lowrank_share >= 0.0 && lowrank_share <= 1.0))
+    return fail(PF_ERR_INVALID_ARG, "lowrank_share must be in [0, 1]");
+  // Cost of a configuration: kept weight entries plus low-rank entries (the
+  // per-token FLOPs are twice this), against budget * n_out * n_in.
+  const double dense = (double)n_out * (double)n_in, total = budget * dense;
+  const int64_t per_rank = n_out + n_in;
+  const int64_t rmax = std::min(n_out, n_in) / b * b;
+  int64_t r = (int64_t)std::floor(lowrank_share * total / (double)per_rank);
+  r = std::max<int64_t>(0, std::min(rmax, r / b * b));
+  const int64_t s = std::min(n_out, n_in) / b;
+  int64_t top = 1;
+  while (top < s) top *= 2;  // strides past the next power of two of s change nothing
+  int32_t best = 1;
+  int64_t best_params = -1;
+  try {
+    for (int64_t ms = 1; ms <= top; ms *= 2) {
+      pf_layout L;
+      std::string e = pf::build_layout(L, n_out, n_in, b, (int32_t)ms);
+      if (!e.empty()) return fail(PF_ERR_INVALID_ARG, e);
+      const int64_t params = L.nnzb * (int64_t)b * b + r * per_rank;
+      if (ms == 1 || (double)params <= total) {
+        best = (int32_t)ms;
+        best_params = params;
+      }
+      if ((double)params > total) break;
+    }
+  } catch (const std::bad_alloc &) {
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  }
+  *r_out = (int32_t)r;
+  *max_stride_out = best;
+  if (params_out) *params_out = best_params;
   return PF_OK;
 }
 

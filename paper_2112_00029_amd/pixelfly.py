@@ -68,6 +68,8 @@ _SIGS = {
     "pf_layout_create": (_i32, [_i64, _i64, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_create_from_mask": (_i32, [_i32, _i32, _i32, _p, ctypes.POINTER(_p)]),
     "pf_layout_create_attention": (_i32, [_i64, _i32, _i32, _i32, ctypes.POINTER(_p)]),
+    "pf_select_mask": (_i32, [_i64, _i64, _i32, ctypes.c_double, ctypes.c_double,
+                              ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "pf_layout_info_get": (_i32, [_p, ctypes.POINTER(pf_layout_info)]),
     "pf_layout_check": (_i32, [_p]),
     "pf_layout_plan_get": (_i32, [_p, ctypes.POINTER(_i32), _i32]),
@@ -178,6 +180,15 @@ def pf_layout_create_attention(seq: int, b: int, max_stride: int, global_blocks:
     h = _p()
     _check(_lib.pf_layout_create_attention(seq, b, max_stride, global_blocks, ctypes.byref(h)))
     return Layout(h.value)
+
+
+def pf_select_mask(n_out: int, n_in: int, b: int, budget: float, lowrank_share: float = 0.25) -> dict:
+    """Rank and maximum stride for a layer from a compute budget; returns
+    dict(r=..., max_stride=..., params=...)."""
+    r, ms, pr = _i32(), _i32(), _i64()
+    _check(_lib.pf_select_mask(n_out, n_in, b, budget, lowrank_share, ctypes.byref(r),
+                               ctypes.byref(ms), ctypes.byref(pr)))
+    return dict(r=r.value, max_stride=ms.value, params=pr.value)
 
 
 def pf_layout_info_get(layout: Layout) -> dict:

@@ -207,3 +207,21 @@ def test_attention_layout_errors():
                  (64 * 20000, 64, 64, 1)]:
         with pytest.raises(pf.PixelflyError):
             pf.pf_layout_create_attention(*args)
+
+
+@pytest.mark.parametrize("n_out,n_in,b", [(3072, 768, 32), (4096, 1024, 64), (16384, 4096, 128),
+                                          (1024, 1024, 32), (768, 768, 32), (96, 160, 32)])
+def test_select_mask_matches_oracle(n_out, n_in, b):
+    from oracle import select as osel
+    for k in range(1, 21):
+        for share in (0.0, 0.25, 1 / 3):
+            got = pf.pf_select_mask(n_out, n_in, b, k / 20, share)
+            r, ms, entries = osel.select(n_out, n_in, b, k / 20, share)
+            assert (got["r"], got["max_stride"], got["params"]) == (r, ms, entries), (k, share)
+
+
+def test_select_mask_errors():
+    for args in [(1024, 1024, 32, 0.0, 0.25), (1024, 1024, 32, 1.5, 0.25), (1024, 1024, 32, 0.5, -0.1),
+                 (1000, 1024, 32, 0.5, 0.25), (1024, 1024, 0, 0.5, 0.25)]:
+        with pytest.raises(pf.PixelflyError):
+            pf.pf_select_mask(*args)
