@@ -110,3 +110,43 @@ def mlp_pair_backward(X, W1d, M1, U1, V1, W2d, M2, U2, V2, dY, fwd=None):
     dH_pre = g2["dX"] * gelu_grad(fwd["H_pre"])
     g1 = backward(X, W1d, M1, dH_pre, U1, V1)
     return {"l2": g2, "l1": g1, "dH": g2["dX"], "dH_pre": dH_pre}
+
+
+def mixed_weight(Wd, U, V, gamma):
+    """The layer's weight with the learnable mixing weight of Section 3.3
+    (model sparsification): gamma B + (1 - gamma) (low-rank product), with B
+    the masked sparse matrix Wd (N x K) and the low-rank product U V (U: N x r,
+    V: r x K; the paper's U V^T with its V transposed)."""
+    return gamma * Wd + (1.0 - gamma) * (U @ V)
+
+
+def forward_mixed(X, Wd, U, V, gamma):
+    """Y = X W^T for the mixed weight, evaluated as the method does it:
+    gamma X Wd^T + (1 - gamma) (X V^T) U^T.  Returns (Y, T_lr)."""
+    T_lr = X @ V.T
+    return gamma * (X @ Wd.T) + (1.0 - gamma) * (T_lr @ U.T), T_lr
+
+
+def backward_mixed(X, Wd, Mel, dY, U, V, gamma):
+    """Gradients of L = <dY, Y> for forward_mixed: with respect to X, the
+    sparse blocks (restricted to the mask, gradient Lemma of the appendix on
+    gradient computation), U, V and gamma.
+
+        dX     = gamma dY Wd + (1 - gamma) (dY U) V
+        dW     = gamma (dY^T X) o M
+        dU     = (1 - gamma) dY^T (X V^T)
+        dV     = (1 - gamma) (dY U)^T X
+        dgamma = <dY, X Wd^T> - <dY, (X V^T) U^T>
+               = <(dY^T X) o M, Wd> - <dY U, X V^T>
+    (S = dY U and T_lr = X V^T are the unscaled intermediates.)"""
+    S = dY @ U
+    T_lr = X @ V.T
+    G = dY.T @ X
+    return {
+        "dX": gamma * (dY @ Wd) + (1.0 - gamma) * (S @ V),
+        "dW": gamma * G * Mel,
+        "dU": (1.0 - gamma) * (dY.T @ T_lr),
+        "dV": (1.0 - gamma) * (S.T @ X),
+        "dgamma": float(np.sum(dY * (X @ Wd.T)) - np.sum(dY * (T_lr @ U.T))),
+        "S": S,
+    }
