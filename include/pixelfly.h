@@ -236,6 +236,48 @@ pf_status pf_linear_bwd_weight(const pf_layout *layout, pf_dtype dtype,
                                void *dWblk, void *dU, void *dV,
                                void *workspace, size_t ws_bytes, void *stream);
 
+/*
+ * The layer with the learnable mixing weight of Section 3.3 (model
+ * sparsification): W = gamma B + (1 - gamma) (low-rank product), B the
+ * block-sparse matrix on the mask, evaluated as the method does it:
+ *
+ *   pf_linear_fwd_mixed:       Y  = gamma X B^T + (1 - gamma) T_lr U^T,
+ *                              T_lr = X V^T (stored unscaled);
+ *   pf_linear_bwd_data_mixed:  dX = gamma dY B + (1 - gamma) S V,
+ *                              S = dY U (stored unscaled);
+ *   pf_linear_bwd_weight_mixed:
+ *                              dW = gamma (dY^T X) o M (packed),
+ *                              dU = (1 - gamma) dY^T T_lr,
+ *                              dV = (1 - gamma) S^T X,
+ *                              *dgamma = <(dY^T X) o M, B> - <S, T_lr>
+ *                              = <dY, X B^T - T_lr U^T> (one fp32 scalar,
+ *                              device memory, 4-byte aligned; summed in a
+ *                              fixed order, so repeat calls agree bitwise).
+ *
+ * Arguments, layouts, epilogues, workspace and errors as the unmixed calls;
+ * gamma must be finite (INVALID_ARG otherwise).  The kept-block sums are
+ * scaled once in fp32 before the low-rank K-blocks join the same
+ * accumulator, so each output is rounded once.  gamma = 1 skips the
+ * low-rank K-blocks of the forward and backward-data products (T_lr and S
+ * are still produced, dgamma needs them).  pf_linear_bwd_weight_mixed also
+ * reads Wblk (the dgamma term) and needs pf_workspace_bytes of workspace
+ * (it always includes room for the dgamma partials).
+ */
+pf_status pf_linear_fwd_mixed(const pf_layout *layout, pf_dtype dtype, int64_t T, int32_t r,
+                              float gamma, const void *X, const void *Wblk, const void *U,
+                              const void *V, void *Y, void *T_lr, pf_epilogue epi, void *Y_pre,
+                              void *workspace, size_t ws_bytes, void *stream);
+pf_status pf_linear_bwd_data_mixed(const pf_layout *layout, pf_dtype dtype, int64_t T, int32_t r,
+                                   float gamma, const void *dY, const void *Wblk, const void *U,
+                                   const void *V, void *S, void *dX, pf_epilogue epi,
+                                   const void *aux, void *workspace, size_t ws_bytes,
+                                   void *stream);
+pf_status pf_linear_bwd_weight_mixed(const pf_layout *layout, pf_dtype dtype, int64_t T,
+                                     int32_t r, float gamma, const void *dY, const void *X,
+                                     const void *Wblk, const void *T_lr, const void *S,
+                                     void *dWblk, void *dU, void *dV, float *dgamma,
+                                     void *workspace, size_t ws_bytes, void *stream);
+
 /* dH_pre = dH * gelu'(H_pre), n elements (exact erf GELU).  Standalone form
  * of the GELU epilogue.  Errors: INVALID_ARG, UNSUPPORTED, HIP. */
 pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH,

@@ -284,6 +284,14 @@ TNPlan tn_plan(int items, int64_t T, int64_t row_bytes) {
   return p;
 }
 
+// Workspace the mixed weight-gradient call adds after the split partials:
+// the kept-block dot partials (one per item, or 16 per item after a split)
+// and the S.T_lr partials, 256-byte aligned.
+size_t mix_dgamma_bytes(int items) {
+  return ((size_t)items * 16 + pf::kMixDotParts) * sizeof(float) + 256;
+}
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
 void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
                      const void *X, const void *T_lr, const void *S, void *dU, void *dV) {
   a.n_dense = 0;
@@ -597,10 +605,11 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
   a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
   const int64_t es = dtype == PF_BF16 ? 2 : 4;
-  const size_t tn = tn_plan(pf::tn_items_total(a, L->b), T, std::max(L->n_out, L->n_in) * es).ws;
+  const int items = pf::tn_items_total(a, L->b);
+  const size_t tn = tn_plan(items, T, std::max(L->n_out, L->n_in) * es).ws;
   const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
   const size_t bwd = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
-  return std::max({tn, fwd, bwd});
+  return std::max({tn, fwd, bwd}) + mix_dgamma_bytes(items);
 }
 
 // Checks a caller workspace against a need of `need` bytes.
@@ -611,10 +620,42 @@ static pf_status need_ws(size_t need, const void *ws, size_t ws_bytes) {
   return need_ptr(ws, "workspace");
 }
 
-pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *X,
-                        const void *Wblk, const void *U, const void *V, void *Y, void *T_lr,
-                        pf_epilogue epi, void *Y_pre, void *workspace, size_t ws_bytes,
-                        void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Mixing weight of the mixed calls: alpha on the block-sparse part, beta on
+// the low-rank part (alpha = gamma, beta = 1 - gamma).
+struct Mix {
+  bool on;
+  float alpha, beta;
+};
+constexpr Mix kNoMix{false, 1.f, 1.f};
+
+pf_status check_gamma(float gamma) {
+  if (!std::isfinite(gamma)) return fail(PF_ERR_INVALID_ARG, "gamma must be finite");
+  return PF_OK;
+}
+
+// The NT arguments' mixing fields for low-rank blocks nlr (0: none, or
+// skipped because beta is 0).
+void set_mix(pf::NTArgs &a, const Mix &m) {
+  if (!m.on) return;
+  a.mix = 1;
+  if (a.nlr > 0 && m.beta != 0.f) {
+    a.mix_ratio = m.alpha / m.beta;
+    a.mix_out = m.beta;
+  } else {
+    a.nlr = 0;
+    a.mix_ratio = 1.f;
+    a.mix_out = m.alpha;
+  }
+}
+
+pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const Mix &mix,
+                     const void *X, const void *Wblk, const void *U, const void *V, void *Y,
+                     void *T_lr, pf_epilogue epi, void *Y_pre, void *workspace, size_t ws_bytes,
+                     void *stream) {
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
@@ -657,9 +698,32 @@ pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r
   a.kcols = wide ? L->d_kcols_fwd_w : L->d_kcols_fwd;
   a.blks = wide ? L->d_blks_fwd_w : L->d_blks_fwd;
   a.nsplit = 1;
+  set_mix(a, mix);
   return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, wide ? L->G_fwd_w : L->G_fwd, false, 128,
-                              L->kmax_fwd + r / b, a, s),
+                              L->kmax_fwd + a.nlr, a, s),
                     "forward kernel");
+}
+
+}  // namespace
+
+extern "C" {
+
+pf_status pf_linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *X,
+                        const void *Wblk, const void *U, const void *V, void *Y, void *T_lr,
+                        pf_epilogue epi, void *Y_pre, void *workspace, size_t ws_bytes,
+                        void *stream) {
+  return linear_fwd(L, dtype, T, r, kNoMix, X, Wblk, U, V, Y, T_lr, epi, Y_pre, workspace,
+                    ws_bytes, stream);
+}
+
+pf_status pf_linear_fwd_mixed(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                              float gamma, const void *X, const void *Wblk, const void *U,
+                              const void *V, void *Y, void *T_lr, pf_epilogue epi, void *Y_pre,
+                              void *workspace, size_t ws_bytes, void *stream) {
+  pf_status st = check_gamma(gamma);
+  if (st != PF_OK) return st;
+  return linear_fwd(L, dtype, T, r, Mix{true, gamma, 1.f - gamma}, X, Wblk, U, V, Y, T_lr, epi,
+                    Y_pre, workspace, ws_bytes, stream);
 }
 
 }  // extern "C"
@@ -714,7 +778,7 @@ pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void
 // dX = dY (M o W) + S V (optionally times gelu'(aux)).
 pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
                      const void *Wblk, const void *S, const void *V, void *dX, pf_epilogue epi,
-                     const void *aux, hipStream_t s) {
+                     const void *aux, hipStream_t s, const Mix &mix = kNoMix) {
   const int b = L->b;
   pf::NTArgs a{};
   a.A = dY; a.lda = L->n_out;
@@ -730,8 +794,9 @@ pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const voi
   a.kcols = wide ? L->d_kcols_bwd_w : L->d_kcols_bwd;
   a.blks = wide ? L->d_blks_bwd_w : L->d_blks_bwd;
   a.nsplit = 1;
+  set_mix(a, mix);
   return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true,
-                              128, L->kmax_bwd + r / b, a, s),
+                              128, L->kmax_bwd + a.nlr, a, s),
                     "backward-data kernel");
 }
 
@@ -746,6 +811,7 @@ pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, con
   a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
   a.T = T;
+  a.scale_w = a.scale_lr = 1.f;
   *plan = tn_plan(pf::tn_items_total(a, L->b), T,
                   std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
   a.nsplit = plan->nsplit;
@@ -795,6 +861,54 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   const pf::TNArgs a = tn_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, &p);
   if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
   return enqueue_tn(L, (int)dtype, a, (float *)workspace, (hipStream_t)stream);
+}
+
+pf_status pf_linear_bwd_data_mixed(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                                   float gamma, const void *dY, const void *Wblk, const void *U,
+                                   const void *V, void *S, void *dX, pf_epilogue epi,
+                                   const void *aux, void *workspace, size_t ws_bytes,
+                                   void *stream) {
+  pf_status st = check_gamma(gamma);
+  if (st != PF_OK) return st;
+  if ((st = check_bwd_data_args(L, dtype, T, r, dY, Wblk, U, V, S, dX, epi, aux)) != PF_OK) return st;
+  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
+  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = enqueue_s(L, (int)dtype, T, r, dY, U, S, sp, (float *)workspace, s)) != PF_OK) return st;
+  return enqueue_dx(L, (int)dtype, T, r, dY, Wblk, S, V, dX, epi, aux, s,
+                    Mix{true, gamma, 1.f - gamma});
+}
+
+pf_status pf_linear_bwd_weight_mixed(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                                     float gamma, const void *dY, const void *X,
+                                     const void *Wblk, const void *T_lr, const void *S,
+                                     void *dWblk, void *dU, void *dV, float *dgamma,
+                                     void *workspace, size_t ws_bytes, void *stream) {
+  pf_status st = check_gamma(gamma);
+  if (st != PF_OK) return st;
+  if ((st = check_bwd_weight_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV)) != PF_OK) return st;
+  if ((st = need_ptr(Wblk, "Wblk")) != PF_OK) return st;
+  if (!dgamma || ((uintptr_t)dgamma & 3)) return fail(PF_ERR_INVALID_ARG, "dgamma NULL or misaligned");
+  if ((st = check_state(L)) != PF_OK) return st;
+  TNPlan p;
+  pf::TNArgs a = tn_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, &p);
+  const int items = pf::tn_items_total(a, L->b);
+  const size_t off = align256(p.ws);
+  const size_t need = off + mix_dgamma_bytes(items);
+  if ((st = need_ws(need, workspace, ws_bytes)) != PF_OK) return st;
+  a.scale_w = gamma;
+  a.scale_lr = 1.f - gamma;
+  a.wdot = Wblk;
+  float *wparts = (float *)((char *)workspace + off);
+  float *sparts = wparts + (size_t)items * 16;
+  a.wdot_out = wparts;
+  hipStream_t s = (hipStream_t)stream;
+  if ((st = enqueue_tn(L, (int)dtype, a, (float *)workspace, s)) != PF_OK) return st;
+  Timed t(PF_KERNEL_REDUCE, s);
+  return hip_status(pf::launch_mix_dgamma((int)dtype, S, T_lr, r > 0 ? T * r : 0, wparts,
+                                          a.nsplit > 1 ? items * 16 : items, sparts, dgamma, s),
+                    "dgamma kernels");
 }
 
 pf_status pf_gelu_bwd(pf_dtype dtype, int64_t n, const void *dH, const void *H_pre, void *dH_pre,
@@ -917,6 +1031,7 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
     case PF_OP_TN: {
       pf::TNArgs a{};
       a.n_items = 0;
+      a.scale_w = a.scale_lr = 1.f;
       a.dr[0] = pf::TNDense{A, M, B, N, C, N, (int)(M / 64), (int)(N / 64)};
       a.n_dense = 1;
       a.T = K;

@@ -371,9 +371,20 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     });
   });
 
-  auto compute = [&](const uint8_t *sb) __attribute__((always_inline)) {
+  // Mixing weight: scale the kept-block sums once, at the first low-rank
+  // K-block (virtual K index nsteps * BLK).
+  const int kswitch = nsteps * BLK;
+  auto compute = [&](const uint8_t *sb, int t) __attribute__((always_inline)) {
     sfor<BK / 16>([&](auto ks) __attribute__((always_inline)) {
       constexpr int h = (ks * 16) / KW, kq = ks % (KW / 16);
+      if (a.mix && (s_begin + t) * BK + ks * 16 == kswitch) {
+        sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+          sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[tn][tm][e] *= a.mix_ratio;
+          });
+        });
+      }
       bf16x8 xf[TM], wf[TN];
       sfor<TM>([&](auto tm) __attribute__((always_inline)) {
         xf[tm] = frag_rows<RBA>(sb + h * (BM * RBA), wm * WTM + tm * 32, kq, lane);
@@ -421,7 +432,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       }
       barrier();
       if (t + NS - 1 < total) issue(t + NS - 1, stage(std::integral_constant<int, (j + NS - 1) % NS>{}));
-      compute(stage(j));
+      compute(stage(j), t);
     });
   }
 
@@ -479,6 +490,10 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
         *(f32x4 *)P = lo;
         *(f32x4 *)(P + 4) = hi;
         return;
+      }
+      if (a.mix) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] *= a.mix_out;
       }
       const int64_t o = gm * a.ldc + col;
       if constexpr (EPI == 1) {  // forward GELU: keep the pre-activation

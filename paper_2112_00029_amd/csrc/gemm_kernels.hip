@@ -152,7 +152,7 @@ struct Stage8 {
 
 // Double-buffered pipeline driver: load(s, ra, rb) issues the global loads
 // of step s into a register stage, store(ra, rb, buf) writes a register stage
-// to LDS buffer buf, compute(buf) runs the MFMAs of the step held in buf.
+// to LDS buffer buf, compute(buf, s) runs the MFMAs of step s held in buf.
 // Register stage 0 carries even steps, stage 1 odd steps; step s lives in
 // LDS buffer s % 2.  The loads of step s+2 are in flight while step s is
 // computed.
@@ -167,12 +167,12 @@ __device__ __forceinline__ void pipeline(int total, Stage8 &ra0, Stage8 &rb0, St
   __syncthreads();
   for (int s = 0; s < total; s += 2) {
     if (s + 2 < total) load(s + 2, ra0, rb0);
-    compute(0);
+    compute(0, s);
     if (s + 1 < total) store(ra1, rb1, 1);
     __syncthreads();
     if (s + 1 < total) {
       if (s + 3 < total) load(s + 3, ra1, rb1);
-      compute(1);
+      compute(1, s + 1);
       if (s + 2 < total) store(ra0, rb0, 0);
       __syncthreads();
     }
@@ -380,11 +380,25 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
     });
   });
 
-  auto compute = [&](int buf) __attribute__((always_inline)) {
+  // Mixing weight: scale the kept-block sums once, at the first low-rank
+  // K-block (the virtual K index nsteps * BLK).
+  const int kswitch = nsteps * BLK;
+  auto mix_switch = [&](int k) __attribute__((always_inline)) {
+    if (a.mix && k == kswitch) {
+      static_for<TM>([&](auto tm) __attribute__((always_inline)) {
+        static_for<TN>([&](auto tn) __attribute__((always_inline)) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[tm][tn][e] *= a.mix_ratio;
+        });
+      });
+    }
+  };
+  auto compute = [&](int buf, int s) __attribute__((always_inline)) {
     const T *As = smem + buf * (A_ELEMS + B_ELEMS);
     const T *Bs = As + A_ELEMS;
     if constexpr (BF) {
       static_for<BK / 16>([&](auto ks) __attribute__((always_inline)) {
+        mix_switch((s_begin + s) * BK + ks * 16);
         bf16x8 af[TM], bfg[TN];
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           af[tm] = frag_rmajor((const bf16_t *)As, LDA_S, ks, wm * WTM + tm * 32, lane);
@@ -401,6 +415,7 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
       });
     } else {
       static_for<BK / 2>([&](auto ks) __attribute__((always_inline)) {
+        mix_switch((s_begin + s) * BK + ks * 2);
         float af[TM], bfg[TN];
         const int kq = ks * 2 + (lane >> 5);
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
@@ -460,6 +475,10 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
         *(f32x4 *)(P + 4) = hi;
         return;
       }
+      if (a.mix) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] *= a.mix_out;
+      }
       const int64_t o = gm * a.ldc + col;
       if constexpr (EPI == 1) {  // forward GELU: keep the pre-activation
         if constexpr (BF) {
@@ -469,8 +488,8 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
             w[e] = (uint32_t)f2bf(v[2 * e]) | ((uint32_t)f2bf(v[2 * e + 1]) << 16);
           *(u32x4 *)((T *)a.C2 + o) = w;
         } else {
-          *(f32x4 *)((T *)a.C2 + o) = lo;
-          *(f32x4 *)((T *)a.C2 + o + 4) = hi;
+          *(f32x4 *)((T *)a.C2 + o) = f32x4{v[0], v[1], v[2], v[3]};
+          *(f32x4 *)((T *)a.C2 + o + 4) = f32x4{v[4], v[5], v[6], v[7]};
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = gelu_f(v[e]);
@@ -570,6 +589,18 @@ __device__ __forceinline__ int tn_items_total_dev(const TNArgs &a, int GT) {
   return n;
 }
 
+// Sum of one float per thread over a 256-thread workgroup in a fixed order
+// (wave butterflies, then the four wave sums in wave order); every thread
+// must call it.  red: 4 floats of LDS.
+__device__ __forceinline__ float block_sum256(float x, float *red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = x;
+  __syncthreads();
+  return ((red[0] + red[1]) + red[2]) + red[3];
+}
+
 // Partial-sum index of (wave, tm, tn, j, lane): lane-contiguous.
 __device__ __forceinline__ int tn_pidx(int wave, int tm, int tn, int j, int lane) {
   return (((wave * 2 + tm) * 2 + tn) * 16 + j) * 64 + lane;
@@ -660,7 +691,7 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
     });
   });
 
-  auto compute = [&](int buf) __attribute__((always_inline)) {
+  auto compute = [&](int buf, int) __attribute__((always_inline)) {
     const T *As = smem + buf * 2 * OP_ELEMS;
     const T *Bs = As + OP_ELEMS;
     if constexpr (BF) {
@@ -730,6 +761,8 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
   });
   __syncthreads();
   constexpr int RCH = BLK / 8;  // 8-column chunks per block row
+  const float sc = v.sparse ? a.scale_w : a.scale_lr;
+  float wd = 0.f;  // mixing weight: sum of (unscaled sum) x W over stored kept elements
   static_for<GT * GT>([&](auto q) __attribute__((always_inline)) {
     constexpr int ga = q / GT, gb = q % GT;
     const int blk = v.oblk(ga, gb);
@@ -737,7 +770,14 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
       for (int c = tid; c < BLK * RCH; c += 256) {
         const int rl = c / RCH, c8 = (c % RCH) * 8;
         const float *src = Cs + (ga * BLK + rl) * CS + gb * BLK + c8;
-        const f32x4 lo = *(const f32x4 *)src, hi = *(const f32x4 *)(src + 4);
+        f32x4 lo = *(const f32x4 *)src, hi = *(const f32x4 *)(src + 4);
+        if (a.wdot && v.sparse) {
+          const T *wp = (const T *)a.wdot + (int64_t)blk * (BLK * BLK) + rl * BLK + c8;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) wd += lo[e] * to_f<T>(wp[e]) + hi[e] * to_f<T>(wp[4 + e]);
+        }
+        lo *= sc;
+        hi *= sc;
         T *dst = v.sparse ? (T *)a.Wout + (int64_t)blk * (BLK * BLK) + rl * BLK + c8
                           : v.dout + ((int64_t)v.acol(ga) * BLK + rl) * v.ldo + (int64_t)v.bcol(gb) * BLK + c8;
         if constexpr (BF) {
@@ -754,6 +794,11 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
       }
     }
   });
+  if (a.wdot) {
+    __shared__ float red[4];
+    const float tot = block_sum256(wd, red);
+    if (tid == 0) a.wdot_out[item] = tot;
+  }
 }
 
 // Second pass of a split TN product: sum the split partials in split order
@@ -773,20 +818,77 @@ __global__ __launch_bounds__(256) void tn_reduce_kernel(TNArgs a_arg) {
   const int cl = (wave & 1) * 64 + tn * 32 + (lane & 31);
   const int ga = rl / BLK, gb = cl / BLK;
   const int blk = v.oblk(ga, gb);
-  if (blk < 0) return;
-  const float *part_p = a.partials + (int64_t)item * a.nsplit * (128 * 128) + q;
-  f32x4 acc = *(const f32x4 *)part_p;
-  for (int sp = 1; sp < a.nsplit; ++sp) acc += *(const f32x4 *)(part_p + (int64_t)sp * (128 * 128));
-  T *dst = v.sparse ? (T *)a.Wout + (int64_t)blk * (BLK * BLK) + (rl % BLK) * BLK + (cl % BLK)
-                    : v.dout + ((int64_t)v.acol(ga) * BLK + (rl % BLK)) * v.ldo + (int64_t)v.bcol(gb) * BLK + (cl % BLK);
-  if constexpr (std::is_same<T, bf16_t>::value) {
-    uint2 w;
-    w.x = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
-    w.y = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
-    *(uint2 *)dst = w;
-  } else {
-    *(f32x4 *)dst = acc;
+  float wd = 0.f;
+  if (blk >= 0) {
+    const float *part_p = a.partials + (int64_t)item * a.nsplit * (128 * 128) + q;
+    f32x4 acc = *(const f32x4 *)part_p;
+    for (int sp = 1; sp < a.nsplit; ++sp) acc += *(const f32x4 *)(part_p + (int64_t)sp * (128 * 128));
+    const int64_t po = (int64_t)blk * (BLK * BLK) + (rl % BLK) * BLK + (cl % BLK);
+    if (a.wdot && v.sparse) {
+      const T *wp = (const T *)a.wdot + po;
+      wd = ((acc[0] * to_f<T>(wp[0]) + acc[1] * to_f<T>(wp[1])) + acc[2] * to_f<T>(wp[2])) +
+           acc[3] * to_f<T>(wp[3]);
+    }
+    acc *= v.sparse ? a.scale_w : a.scale_lr;
+    T *dst = v.sparse ? (T *)a.Wout + po
+                      : v.dout + ((int64_t)v.acol(ga) * BLK + (rl % BLK)) * v.ldo + (int64_t)v.bcol(gb) * BLK + (cl % BLK);
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      uint2 w;
+      w.x = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
+      w.y = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
+      *(uint2 *)dst = w;
+    } else {
+      *(f32x4 *)dst = acc;
+    }
   }
+  if (a.wdot) {
+    __shared__ float red[4];
+    const float tot = block_sum256(wd, red);
+    if (threadIdx.x == 0) a.wdot_out[item * 16 + part] = tot;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dgamma of the mixing weight: <S, T_lr> in kMixDotParts fixed partials, then
+// one workgroup: sum of the kept-block dot partials minus the S.T_lr ones.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void mix_dot_kernel(const T *__restrict__ S,
+                                                      const T *__restrict__ Tl, int64_t n,
+                                                      float *__restrict__ out) {
+  float x = 0.f;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)kMixDotParts * 256)
+    x += to_f<T>(S[i]) * to_f<T>(Tl[i]);
+  __shared__ float red[4];
+  const float tot = block_sum256(x, red);
+  if (threadIdx.x == 0) out[blockIdx.x] = tot;
+}
+
+__global__ __launch_bounds__(256) void mix_final_kernel(const float *__restrict__ wparts, int nw,
+                                                        const float *__restrict__ sparts, int ns,
+                                                        float *__restrict__ dgamma) {
+  float x = 0.f;
+  for (int i = threadIdx.x; i < nw; i += 256) x += wparts[i];
+  for (int i = threadIdx.x; i < ns; i += 256) x -= sparts[i];
+  __shared__ float red[4];
+  const float tot = block_sum256(x, red);
+  if (threadIdx.x == 0) *dgamma = tot;
+}
+
+hipError_t launch_mix_dgamma(int dtype, const void *S, const void *T_lr, int64_t n,
+                             const float *wparts, int nw, float *sparts, float *dgamma,
+                             hipStream_t s) {
+  if (n > 0) {
+    if (dtype == 0)
+      launch_kernel(mix_dot_kernel<bf16_t>, dim3(kMixDotParts), dim3(256), s, (const bf16_t *)S,
+                    (const bf16_t *)T_lr, n, sparts);
+    else
+      launch_kernel(mix_dot_kernel<float>, dim3(kMixDotParts), dim3(256), s, (const float *)S,
+                    (const float *)T_lr, n, sparts);
+  }
+  launch_kernel(mix_final_kernel, dim3(1), dim3(256), s, wparts, nw, (const float *)sparts,
+                n > 0 ? kMixDotParts : 0, dgamma);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------

@@ -83,6 +83,13 @@ struct NTArgs {
   int nsplit;
   float *partials;
   int64_t ldp;
+  // Mixing weight (block-sparse mode, nsplit 1): when mix is set the kept
+  // blocks accumulate first, the accumulator is multiplied by mix_ratio at
+  // the first low-rank K-block and the result by mix_out, giving
+  // alpha * sparse + beta * low-rank with mix_ratio = alpha / beta and
+  // mix_out = beta (or mix_out = alpha with no low-rank blocks).
+  int mix;
+  float mix_ratio, mix_out;
 };
 
 // A dense region of the TN kernel: out[a][b] = sum_t A[t][a] B[t][b] over
@@ -111,6 +118,15 @@ struct TNArgs {
   int nsplit;
   int64_t chunk;        // tokens per split (multiple of 64)
   float *partials;      // [items_total][nsplit][128*128] when nsplit > 1
+  // Mixing weight: stores scale the kept-block sums by scale_w and the dense
+  // regions by scale_lr (1 and 1 otherwise).  With wdot set, every workgroup
+  // that stores kept blocks also writes the sum over its stored elements of
+  // (unscaled fp32 sum) x (the same element of the packed matrix wdot) to
+  // wdot_out[item] (nsplit 1) or wdot_out[item * 16 + part] (the split
+  // reduction), zero where it stores none.
+  float scale_w, scale_lr;
+  const void *wdot;
+  float *wdot_out;
 };
 
 // Rank-r product C[M x ncols] = A[M x K] . op(B) (bf16, skinny.hip):
@@ -157,6 +173,14 @@ hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
 hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s);
 int tn_items_total(const TNArgs &a, int blk);
 hipError_t launch_skinny(bool b_kn, const SkinnyArgs &a, hipStream_t s);
+// dgamma of the mixing weight: partial sums of <S, T_lr> (n elements,
+// kMixDotParts workgroups), then one workgroup adds the kernel-stored partial
+// dot products wparts[0 .. nw) and subtracts the S.T_lr partials, in a fixed
+// order, into *dgamma.
+constexpr int kMixDotParts = 256;
+hipError_t launch_mix_dgamma(int dtype, const void *S, const void *T_lr, int64_t n,
+                             const float *wparts, int nw, float *sparts, float *dgamma,
+                             hipStream_t s);
 hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
                            const void *Hpre, void *out, hipStream_t s);
 hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s);

@@ -80,6 +80,12 @@ _SIGS = {
     "pf_linear_bwd_data": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _i32, _p, _p, _sz,
                                   _p]),
     "pf_linear_bwd_weight": (_i32, [_p, _i32, _i64, _i32, _p, _p, _p, _p, _p, _p, _p, _p, _sz, _p]),
+    "pf_linear_fwd_mixed": (_i32, [_p, _i32, _i64, _i32, _f32, _p, _p, _p, _p, _p, _p, _i32, _p, _p,
+                                   _sz, _p]),
+    "pf_linear_bwd_data_mixed": (_i32, [_p, _i32, _i64, _i32, _f32, _p, _p, _p, _p, _p, _p, _i32,
+                                        _p, _p, _sz, _p]),
+    "pf_linear_bwd_weight_mixed": (_i32, [_p, _i32, _i64, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
+                                          _p, _p, _p, _sz, _p]),
     "pf_gelu_bwd": (_i32, [_i32, _i64, _p, _p, _p, _p]),
     "pf_attn_fwd": (_i32, [_p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p]),
     "pf_attn_bwd": (_i32, [_p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p,
@@ -251,6 +257,29 @@ def pf_linear_bwd_weight(layout, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, wor
     _check(_lib.pf_linear_bwd_weight(layout.handle, _dt(dtype), T, r, _ptr(dY), _ptr(X),
                                      _ptr(T_lr), _ptr(S), _ptr(dWblk), _ptr(dU), _ptr(dV),
                                      _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pf_linear_fwd_mixed(layout, dtype, T, r, gamma, X, Wblk, U, V, Y, T_lr, epi=PF_EPI_NONE,
+                        Y_pre=None, workspace=None, ws_bytes=0, stream=None) -> None:
+    _check(_lib.pf_linear_fwd_mixed(layout.handle, _dt(dtype), T, r, float(gamma), _ptr(X),
+                                    _ptr(Wblk), _ptr(U), _ptr(V), _ptr(Y), _ptr(T_lr), epi,
+                                    _ptr(Y_pre), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pf_linear_bwd_data_mixed(layout, dtype, T, r, gamma, dY, Wblk, U, V, S, dX, epi=PF_EPI_NONE,
+                             aux=None, workspace=None, ws_bytes=0, stream=None) -> None:
+    _check(_lib.pf_linear_bwd_data_mixed(layout.handle, _dt(dtype), T, r, float(gamma), _ptr(dY),
+                                         _ptr(Wblk), _ptr(U), _ptr(V), _ptr(S), _ptr(dX), epi,
+                                         _ptr(aux), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pf_linear_bwd_weight_mixed(layout, dtype, T, r, gamma, dY, X, Wblk, T_lr, S, dWblk, dU, dV,
+                               dgamma, workspace, ws_bytes, stream=None) -> None:
+    """dgamma: device buffer of one float32."""
+    _check(_lib.pf_linear_bwd_weight_mixed(layout.handle, _dt(dtype), T, r, float(gamma),
+                                           _ptr(dY), _ptr(X), _ptr(Wblk), _ptr(T_lr), _ptr(S),
+                                           _ptr(dWblk), _ptr(dU), _ptr(dV), _ptr(dgamma),
+                                           _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def pf_gelu_bwd(dtype, n, dH, H_pre, dH_pre, stream=None) -> None:
