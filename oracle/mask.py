@@ -162,3 +162,29 @@ def attention_layout(seq: int, b: int, max_stride: int, global_blocks: int = 0):
     assert seq % b == 0
     M = attention_block_mask(seq // b, max_stride, global_blocks)
     return M, block_csr(M)
+
+
+def block_cover(M: np.ndarray, b1: int, b2: int) -> np.ndarray:
+    """(b1, b2)-block cover of a 0/1 mask (definition in the appendix on the
+    cost model: the block-aligned mask with the fewest nonzeros that
+    contains M): every b1 x b2 block that holds a nonzero becomes all ones.
+    The shape must be a multiple of (b1, b2)."""
+    m, n = M.shape
+    assert m % b1 == 0 and n % b2 == 0
+    C = np.zeros_like(M, dtype=bool)
+    for i in range(0, m, b1):
+        for j in range(0, n, b2):
+            if M[i:i + b1, j:j + b2].any():
+                C[i:i + b1, j:j + b2] = True
+    return C
+
+
+def random_block_mask(n_out: int, n_in: int, p: int, density: float, seed: int) -> np.ndarray:
+    """Random sparsity pattern of the appendix on microbenchmarking: the
+    n_out x n_in matrix is split into p x p blocks and each block is kept
+    independently with probability `density` (the expected density).  The
+    seeded draw is the pattern's definition here (numpy PCG64, stream 101)."""
+    assert n_out % p == 0 and n_in % p == 0
+    rng = np.random.Generator(np.random.PCG64([seed, 101]))
+    keep = rng.random((n_out // p, n_in // p)) < density
+    return np.kron(keep.astype(np.int8), np.ones((p, p), np.int8)).astype(bool)
