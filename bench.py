@@ -415,6 +415,111 @@ class Attention:
         return fl / el / 1e12, f"oracle fwd+bwd (fp64, dense masked) on {reps} heads of {wl.B * wl.H}, {el:.1f} s"
 
 
+# ---------------------------------------------------------------------------
+# Pattern microbenchmark
+# ---------------------------------------------------------------------------
+class Patterns:
+    """Forward block-sparse product of an N x N weight over T tokens for the
+    flat block butterfly + low-rank layer selected for a 10% budget (the
+    timed step) and, measured beside it, random p x p block patterns of 10%
+    expected density run on their 32 x 32 block cover (appendix on
+    microbenchmarking): the kernels touch every kept cover block, so a fine
+    random pattern costs close to the dense product."""
+    calls = ["pixelfly"]
+    BLOCKS = (1, 2, 4, 8, 16, 32)
+    DENSITY = 0.10
+
+    def __init__(self, torch, pf, wl, seed=0):
+        self.torch, self.pf, self.wl, self.dtype = torch, pf, wl, "bf16"
+        T, n, b = wl.T, wl.N, wl.b
+        sel = pf.pf_select_mask(n, n, b, self.DENSITY, 0.25)
+        self.r, self.ms = sel["r"], sel["max_stride"]
+        dr = lambda shape, s: dev_bf16(torch, synth.draw(shape, 0.02, seed, s, "bf16")[1])
+        e = lambda *sh: torch.empty(*sh, dtype=torch.bfloat16, device="cuda")
+        self.X, self.Y = dr((T, n), 1), e(T, n)
+        self.cases = []
+        L = pf.pf_layout_create(n, n, b, self.ms)
+        pf.pf_layout_upload(L)
+        nnzb = pf.pf_layout_info_get(L)["nnzb"]
+        self.nnzb = nnzb
+        self.cases.append(dict(name="pixelfly", block=b, L=L, nnzb=nnzb, r=self.r,
+                               W=dr((nnzb, b, b), 2), U=dr((n, self.r), 3), V=dr((self.r, n), 4),
+                               Tl=e(T, max(self.r, 1)),
+                               expected_density=(nnzb * b * b + 2 * n * self.r) / (n * n)))
+        for p in self.BLOCKS:
+            E = synth.random_block_mask(n, n, p, self.DENSITY, seed)
+            Lr = pf.pf_layout_create_from_element_mask(n, n, b, E)
+            pf.pf_layout_upload(Lr)
+            nz = pf.pf_layout_info_get(Lr)["nnzb"]
+            self.cases.append(dict(name=f"random_{p}x{p}", block=p, L=Lr, nnzb=nz, r=0,
+                                   W=dr((nz, b, b), 2), U=None, V=None, Tl=None,
+                                   expected_density=float(E.mean())))
+        self.wsb = max(pf.pf_workspace_bytes(c["L"], T, c["r"], "bf16") for c in self.cases)
+        self.ws = torch.empty(max(self.wsb, 256), dtype=torch.uint8, device="cuda")
+
+    def _fwd(self, c):
+        self.pf.pf_linear_fwd(c["L"], "bf16", self.wl.T, c["r"], self.X, c["W"], c["U"], c["V"],
+                              self.Y, c["Tl"] if c["r"] else None, workspace=self.ws,
+                              ws_bytes=self.wsb)
+
+    def call(self, name):
+        self._fwd(next(c for c in self.cases if c["name"] == name))
+
+    def flops(self):
+        wl = self.wl
+        return (2 * wl.T * self.nnzb * wl.b * wl.b, 2 * wl.T * self.r * 2 * wl.N,
+                2 * wl.T * wl.N * wl.K)
+
+    def kernel_work(self):
+        wl = self.wl
+        w = _layer_work(wl.T, wl.K, wl.N, self.r, self.nnzb * wl.b * wl.b, 2)
+        return {k: w[k] for k in ("spmm_fwd", "lowrank_t")}
+
+    def extra(self):
+        """Latency of each pattern's forward (events around 20 launches)."""
+        wl, rows = self.wl, []
+        for c in self.cases:
+            ms = timed(self.torch, lambda c=c: self._fwd(c), 20, 3)
+            kept = 2 * wl.T * c["nnzb"] * wl.b * wl.b
+            rows.append({"pattern": c["name"], "block": c["block"],
+                         "expected_density": c["expected_density"],
+                         "actual_density": c["nnzb"] * wl.b * wl.b / (wl.N * wl.K),
+                         "ms": ms, "tflops_on_cover": kept / (ms * 1e-3) / 1e12})
+        return {"patterns": rows, "pass": "forward"}
+
+    def dense_setup(self):
+        torch, wl = self.torch, self.wl
+        self.Wd = torch.randn(wl.N, wl.K, dtype=torch.bfloat16, device="cuda") * 0.02
+
+    def dense_step(self):
+        wl = self.wl
+        self.pf.pf_dense_gemm("bf16", self.pf.PF_OP_NT, wl.T, wl.N, wl.K, self.X, self.Wd, self.Y)
+
+    def torch_dense_step(self):
+        self.torch.matmul(self.X, self.Wd.t(), out=self.Y)
+
+    def cpu_baseline(self, budget_s=12.0):
+        from oracle import linear as ol
+        from oracle import mask as om
+        wl = self.wl
+        M, (row_ptr, col_idx, *_x) = om.layout(wl.N, wl.K, wl.b, self.ms)
+        Ts = 512
+        X = synth.draw((Ts, wl.K), 0.02, 0, 1, "bf16")[0]
+        W = synth.draw((int(M.sum()), wl.b, wl.b), 0.02, 0, 2, "bf16")[0]
+        U = synth.draw((wl.N, self.r), 0.02, 0, 3, "bf16")[0]
+        V = synth.draw((self.r, wl.K), 0.02, 0, 4, "bf16")[0]
+        Wd = ol.unpack(W, row_ptr, col_idx, wl.N // wl.b, wl.K // wl.b, wl.b)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            ol.forward(X, Wd, U, V)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 1000:
+                break
+        fl = 2 * Ts * int(M.sum()) * wl.b * wl.b * reps
+        return fl / el / 1e12, f"oracle forward (fp64, dense masked) on {Ts} of {wl.T} tokens x {reps} reps, {el:.1f} s"
+
+
 def _layer_work(T, K, N, r, w, e):
     """(flops, bytes) per step of the kernel classes of one K -> N layer with
     w kept weight elements, r-rank factors and e-byte elements."""
@@ -461,7 +566,8 @@ def main():
     from paper_2112_00029_amd import pixelfly as pf
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     wl = synth.WORKLOADS[args.workload]
-    R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention}[wl.kind](torch, pf, wl)
+    R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention,
+         "patterns": Patterns}[wl.kind](torch, pf, wl)
 
     if args.copy_probe:
         n = args.copy_probe << 20
@@ -520,6 +626,7 @@ def main():
         dense_ms = timed(torch, R.dense_step, max(5, args.steps // 4), 3)
         if wl.kind != "attention":
             torch_ms = timed(torch, R.torch_dense_step, max(5, args.steps // 4), 3)
+    extra = R.extra() if hasattr(R, "extra") else {}
 
     # Roofline of the dominant kernel: the kernel class with the most time
     # per step, its algorithmic work per launch over its mean launch time
@@ -564,6 +671,8 @@ def main():
     if wl.kind == "attention":
         cfg.update(B=wl.B, H=wl.H, S=wl.S, d=wl.d, b=wl.b, max_stride=wl.max_stride,
                    global_blocks=wl.global_blocks)
+    elif wl.kind == "patterns":
+        cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=R.ms, r=R.r, budget=Patterns.DENSITY)
     else:
         cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=wl.max_stride, r=wl.r)
     out = {
@@ -581,6 +690,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    out.update(extra)
     print(json.dumps(out))
 
 

@@ -131,6 +131,22 @@ pf_status pf_layout_create_attention(int64_t seq, int32_t b, int32_t max_stride,
                                      int32_t global_blocks, pf_layout **out);
 
 /*
+ * Layout of the (b, b)-block cover of an arbitrary element mask (appendix on
+ * the cost model: the block cover is the block-aligned mask with the fewest
+ * nonzeros containing the mask; the kernels touch exactly its blocks, so
+ * its density is the "actual density" of the appendix on
+ * microbenchmarking).  elem_mask: n_out x n_in bytes, row-major host
+ * memory, nonzero = kept element, read during the call only.  Block (i, j)
+ * is kept iff any element of it is.  Values of W inside a kept block but
+ * outside the element mask are the caller's (zeros reproduce the finer
+ * mask).  Requires b >= 1 dividing n_out and n_in, at most 2^26 blocks, and
+ * every block row keeping at least one block.  max_stride and eff_stride
+ * read 0.  Host only.  Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_layout_create_from_element_mask(int64_t n_out, int64_t n_in, int32_t b,
+                                             const uint8_t *elem_mask, pf_layout **out);
+
+/*
  * Mask selection for one layer from a compute budget (Section 3.3, step 2):
  * a share lowrank_share of the budget (the paper's rule of thumb: one
  * quarter to one third) goes to the low-rank part, whose rank is the largest

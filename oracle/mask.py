@@ -178,13 +178,3 @@ def block_cover(M: np.ndarray, b1: int, b2: int) -> np.ndarray:
                 C[i:i + b1, j:j + b2] = True
     return C
 
-
-def random_block_mask(n_out: int, n_in: int, p: int, density: float, seed: int) -> np.ndarray:
-    """Random sparsity pattern of the appendix on microbenchmarking: the
-    n_out x n_in matrix is split into p x p blocks and each block is kept
-    independently with probability `density` (the expected density).  The
-    seeded draw is the pattern's definition here (numpy PCG64, stream 101)."""
-    assert n_out % p == 0 and n_in % p == 0
-    rng = np.random.Generator(np.random.PCG64([seed, 101]))
-    keep = rng.random((n_out // p, n_in // p)) < density
-    return np.kron(keep.astype(np.int8), np.ones((p, p), np.int8)).astype(bool)

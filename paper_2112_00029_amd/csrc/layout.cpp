@@ -216,6 +216,27 @@ std::string build_attention_layout(pf_layout &L, int64_t seq, int32_t b, int32_t
   return "";
 }
 
+// Layout of the (b, b)-block cover of an element mask (appendix on the cost
+// model: the block-aligned mask with the fewest nonzeros containing it):
+// block (i, j) is kept iff any element of it is nonzero.
+std::string build_cover_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
+                               const uint8_t *elem_mask) {
+  if (!elem_mask) return "mask is NULL";
+  if (b < 1 || n_out < b || n_in < b || n_out % b || n_in % b)
+    return "b must be >= 1 and divide n_out and n_in";
+  if (n_out / b > (1 << 20) || n_in / b > (1 << 20) || (n_out / b) * (n_in / b) > (1 << 26))
+    return "too many blocks";
+  const int32_t nbo = (int32_t)(n_out / b), nbi = (int32_t)(n_in / b);
+  std::vector<uint8_t> m((size_t)nbo * nbi, 0);
+  for (int64_t i = 0; i < n_out; ++i) {
+    const uint8_t *row = elem_mask + i * n_in;
+    uint8_t *mb = m.data() + (size_t)(i / b) * nbi;
+    for (int64_t j = 0; j < n_in; ++j)
+      if (row[j]) mb[j / b] = 1;
+  }
+  return build_layout_from_mask(L, nbo, nbi, b, m.data());
+}
+
 std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, int32_t b,
                                    const uint8_t *mask) {
   if (b < 1) return "block size b must be >= 1";

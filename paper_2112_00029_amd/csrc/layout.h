@@ -52,6 +52,9 @@ std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, 
 // first global_blocks block rows and columns.
 std::string build_attention_layout(pf_layout &L, int64_t seq, int32_t b, int32_t max_stride,
                                    int32_t global_blocks);
+// Layout of the (b, b)-block cover of an n_out x n_in element mask.
+std::string build_cover_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
+                               const uint8_t *elem_mask);
 std::string finish_layout(pf_layout &L);
 // Re-verify the work lists against the block-CSR.  Returns "" or an error.
 std::string check_layout(const pf_layout &L);

@@ -68,6 +68,7 @@ _SIGS = {
     "pf_layout_create": (_i32, [_i64, _i64, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_create_from_mask": (_i32, [_i32, _i32, _i32, _p, ctypes.POINTER(_p)]),
     "pf_layout_create_attention": (_i32, [_i64, _i32, _i32, _i32, ctypes.POINTER(_p)]),
+    "pf_layout_create_from_element_mask": (_i32, [_i64, _i64, _i32, _p, ctypes.POINTER(_p)]),
     "pf_select_mask": (_i32, [_i64, _i64, _i32, ctypes.c_double, ctypes.c_double,
                               ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "pf_layout_info_get": (_i32, [_p, ctypes.POINTER(pf_layout_info)]),
@@ -185,6 +186,18 @@ def pf_layout_create_from_mask(nb_out: int, nb_in: int, b: int, block_mask) -> L
 def pf_layout_create_attention(seq: int, b: int, max_stride: int, global_blocks: int = 0) -> Layout:
     h = _p()
     _check(_lib.pf_layout_create_attention(seq, b, max_stride, global_blocks, ctypes.byref(h)))
+    return Layout(h.value)
+
+
+def pf_layout_create_from_element_mask(n_out: int, n_in: int, b: int, elem_mask) -> Layout:
+    """elem_mask: (n_out, n_in) array-like, nonzero = kept element; the layout
+    is its (b, b)-block cover."""
+    m = np.ascontiguousarray(np.asarray(elem_mask).astype(bool).astype(np.uint8))
+    if m.shape != (n_out, n_in):
+        raise ValueError(f"elem_mask shape {m.shape} != ({n_out}, {n_in})")
+    h = _p()
+    _check(_lib.pf_layout_create_from_element_mask(n_out, n_in, b, m.ctypes.data_as(_p),
+                                                   ctypes.byref(h)))
     return Layout(h.value)
 
 

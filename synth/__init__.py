@@ -8,8 +8,8 @@ tensor has its own stream), scaled by its standard deviation and rounded to
 bfloat16 with round-to-nearest-even when the workload is bf16.  Both the CPU
 oracle and the GPU path consume exactly these bits.
 """
-from .gen import (Workload, WORKLOADS, bf16_bits_from_f32, f32_from_bf16_bits,
+from .gen import (Workload, WORKLOADS, random_block_mask, bf16_bits_from_f32, f32_from_bf16_bits,
                   draw, draw_int)
 
-__all__ = ["Workload", "WORKLOADS", "bf16_bits_from_f32", "f32_from_bf16_bits",
+__all__ = ["Workload", "WORKLOADS", "random_block_mask", "bf16_bits_from_f32", "f32_from_bf16_bits",
            "draw", "draw_int"]

@@ -102,6 +102,12 @@ WORKLOADS = {
     "attn_global_8x12x4096x64": Workload(
         "attn_global_8x12x4096x64", "attention", "bf16", B=8, H=12, S=4096, d=64,
         b=64, max_stride=64, std_x=1.0, std_dy=1.0, global_blocks=1),
+    # Pattern microbenchmark (appendix on microbenchmarking): forward product
+    # of a 4096 x 4096 weight over 4096 tokens for random p x p block patterns
+    # of 10% expected density and the flat block butterfly + low-rank layer
+    # selected for a 10% budget, on the 32 x 32 block cover of each pattern.
+    "patterns_4096x4096": Workload(
+        "patterns_4096x4096", "patterns", "bf16", T=4096, K=4096, N=4096, b=32),
     # Large layer 4096 -> 16384, 16384 tokens, 128x128 blocks, strides < 32.
     "linear_16384x4096_b128": Workload(
         "linear_16384x4096_b128", "linear", "bf16", T=16384, K=4096, N=16384,
@@ -113,3 +119,14 @@ WORKLOADS = {
         "linear_16384x4096_b32", "linear", "bf16", T=16384, K=4096, N=16384,
         b=32, max_stride=32, r=256),
 }
+
+
+def random_block_mask(n_out: int, n_in: int, p: int, density: float, seed: int) -> np.ndarray:
+    """Random sparsity pattern of the paper's pattern microbenchmark: the
+    n_out x n_in matrix is split into p x p blocks and each block is kept
+    independently with probability `density` (the expected density).
+    Element mask, bool.  numpy PCG64 seeded with [seed, 101]."""
+    assert n_out % p == 0 and n_in % p == 0
+    rng = np.random.Generator(np.random.PCG64([seed, 101]))
+    keep = rng.random((n_out // p, n_in // p)) < density
+    return np.kron(keep.astype(np.int8), np.ones((p, p), np.int8)).astype(bool)

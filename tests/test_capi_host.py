@@ -7,6 +7,7 @@ import ctypes
 import numpy as np
 import pytest
 
+import synth
 from oracle import mask as om
 
 pf = pytest.importorskip("paper_2112_00029_amd.pixelfly")
@@ -225,3 +226,31 @@ def test_select_mask_errors():
                  (1000, 1024, 32, 0.5, 0.25), (1024, 1024, 0, 0.5, 0.25)]:
         with pytest.raises(pf.PixelflyError):
             pf.pf_select_mask(*args)
+
+
+@pytest.mark.parametrize("n,p,d,b", [(1024, 4, 0.05, 32), (1024, 16, 0.2, 32), (512, 8, 0.1, 64),
+                                      (768, 1, 0.002, 32), (256, 32, 0.5, 128)])
+def test_cover_layout_bit_exact_vs_oracle(n, p, d, b):
+    """pf_layout_create_from_element_mask against the oracle's block cover."""
+    E = synth.random_block_mask(n, n, p, d, seed=5)
+    C = om.block_cover(E, b, b)
+    Mb = C[::b, ::b]
+    if not Mb.any(axis=1).all():
+        pytest.skip("draw left an empty block row")
+    L = pf.pf_layout_create_from_element_mask(n, n, b, E)
+    info = pf.pf_layout_info_get(L)
+    ref = om.block_csr(Mb)
+    for name, r in zip(["row_ptr", "col_idx", "col_ptr", "row_idx", "tperm"], ref):
+        assert np.array_equal(info[name], r), name
+    pf.pf_layout_check(L)
+
+
+def test_cover_layout_errors():
+    E = np.ones((64, 64), bool)
+    for args in [(64, 64, 0, E), (64, 60, 32, E[:, :60]), (64, 64, 48, E)]:
+        with pytest.raises(pf.PixelflyError):
+            pf.pf_layout_create_from_element_mask(*args)
+    E2 = np.zeros((64, 64), bool)
+    E2[:32] = True  # second block row empty
+    with pytest.raises(pf.PixelflyError):
+        pf.pf_layout_create_from_element_mask(64, 64, 32, E2)

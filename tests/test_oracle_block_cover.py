@@ -12,6 +12,7 @@ import itertools
 import numpy as np
 import pytest
 
+import synth
 from oracle import mask as om
 
 
@@ -52,9 +53,28 @@ def test_expected_cover_density(p, d, b):
     holds (b / p)^2 independent draws, so it is kept with probability
     1 - (1 - d)^((b / p)^2)."""
     n = 1024
-    M = om.random_block_mask(n, n, p, d, seed=3)
+    M = synth.random_block_mask(n, n, p, d, seed=3)
     assert abs(M.mean() - d) < 4 * np.sqrt(d * (1 - d) / (n // p) ** 2) + 1e-12
     C = om.block_cover(M, b, b)
     expect = 1 - (1 - d) ** ((b // p) ** 2)
     nblk = (n // b) ** 2
     assert abs(C.mean() - expect) < 4 * np.sqrt(expect * (1 - expect) / nblk) + 1e-9
+
+
+def test_paper_actual_densities():
+    """The paper's printed actual densities for random 8x8, 16x16 and 32x32
+    blocks (tests/golden/microbench_actual_density.txt) against the closed
+    form at 10% expected density, and against the oracle's cover of one
+    seeded 4096 x 4096 draw."""
+    import os
+    rows = []
+    for line in open(os.path.join(os.path.dirname(__file__), "golden", "microbench_actual_density.txt")):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            p, pct = line.split()
+            rows.append((int(p), float(pct) / 100))
+    for p, printed in rows:
+        closed = 1 - 0.9 ** ((32 // p) ** 2)
+        assert abs(closed - printed) < 0.005, (p, closed, printed)
+        C = om.block_cover(synth.random_block_mask(4096, 4096, p, 0.10, seed=0), 32, 32)
+        assert abs(C.mean() - printed) < 0.01, (p, C.mean(), printed)
