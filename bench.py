@@ -520,6 +520,136 @@ class Patterns:
         return fl / el / 1e12, f"oracle forward (fp64, dense masked) on {Ts} of {wl.T} tokens x {reps} reps, {el:.1f} s"
 
 
+# ---------------------------------------------------------------------------
+# Flat butterfly vs product form
+# ---------------------------------------------------------------------------
+class Butterfly:
+    """Forward + backward of the flat block butterfly (one block-sparse layer
+    with every stride up to the maximum; the timed step, at the workload's
+    maximum stride) and, measured beside it for each maximum stride, the
+    product form: a chain of factor layers I + B_k, forward through every
+    factor, then backward-data and backward-weight through each in reverse.
+    Appendix on benchmarking the butterfly multiply."""
+    calls = ["flat"]
+
+    def __init__(self, torch, pf, wl, seed=0):
+        self.torch, self.pf, self.wl, self.dtype = torch, pf, wl, "bf16"
+        T, n, b = wl.T, wl.N, wl.b
+        dr = lambda shape, st, s: dev_bf16(torch, synth.draw(shape, st, seed, s, "bf16")[1])
+        e = lambda *sh: torch.empty(*sh, dtype=torch.bfloat16, device="cuda")
+        self.X, self.dY = dr((T, n), 1.0, 1), dr((T, n), 1.0, 5)
+        self.Y, self.dX = e(T, n), e(T, n)
+        self.strides = [k for k in (2, 4, 8, 16, 32) if k <= min(wl.max_stride, n // b)]
+        self.flat = {}
+        for ms in self.strides:
+            L = pf.pf_layout_create(n, n, b, ms)
+            pf.pf_layout_upload(L)
+            nz = pf.pf_layout_info_get(L)["nnzb"]
+            self.flat[ms] = dict(L=L, nnzb=nz, W=dr((nz, b, b), 1.0 / np.sqrt(nz * b / (n // b)), 2),
+                                 dW=e(nz, b, b))
+        self.fac = {}
+        for k in self.strides:
+            L = pf.pf_layout_create_factor(n, b, k)
+            pf.pf_layout_upload(L)
+            nz = 2 * (n // b)
+            self.fac[k] = dict(L=L, W=dr((nz, b, b), 1.0 / np.sqrt(2 * b), 20 + k), dW=e(nz, b, b),
+                               act=e(T, n), g=e(T, n))
+        self.wsb = max(pf.pf_workspace_bytes(c["L"], T, 0, "bf16")
+                       for c in list(self.flat.values()) + list(self.fac.values()))
+        self.ws = torch.empty(max(self.wsb, 256), dtype=torch.uint8, device="cuda")
+        self.nnzb = self.flat[self.strides[-1]]["nnzb"]
+
+    def _flat(self, ms):
+        pf, T, c = self.pf, self.wl.T, self.flat[ms]
+        kw = dict(workspace=self.ws, ws_bytes=self.wsb)
+        pf.pf_linear_fwd(c["L"], "bf16", T, 0, self.X, c["W"], None, None, self.Y, None, **kw)
+        pf.pf_linear_bwd_data(c["L"], "bf16", T, 0, self.dY, c["W"], None, None, None, self.dX, **kw)
+        pf.pf_linear_bwd_weight(c["L"], "bf16", T, 0, self.dY, self.X, None, None, c["dW"], None,
+                                None, self.ws, self.wsb)
+
+    def _product(self, ms):
+        pf, T = self.pf, self.wl.T
+        kw = dict(workspace=self.ws, ws_bytes=self.wsb)
+        ks = [k for k in self.strides if k <= ms]
+        x = self.X
+        for k in ks:
+            c = self.fac[k]
+            pf.pf_linear_fwd(c["L"], "bf16", T, 0, x, c["W"], None, None, c["act"], None, **kw)
+            x = c["act"]
+        g = self.dY
+        for i in reversed(range(len(ks))):
+            c = self.fac[ks[i]]
+            xin = self.X if i == 0 else self.fac[ks[i - 1]]["act"]
+            pf.pf_linear_bwd_weight(c["L"], "bf16", T, 0, g, xin, None, None, c["dW"], None, None,
+                                    self.ws, self.wsb)
+            pf.pf_linear_bwd_data(c["L"], "bf16", T, 0, g, c["W"], None, None, None, c["g"], **kw)
+            g = c["g"]
+
+    def call(self, name):
+        self._flat(self.strides[-1])
+
+    def flops(self):
+        wl = self.wl
+        return 3 * 2 * wl.T * self.nnzb * wl.b * wl.b, 0, 3 * 2 * wl.T * wl.N * wl.K
+
+    def kernel_work(self):
+        wl = self.wl
+        w = _layer_work(wl.T, wl.K, wl.N, 0, self.nnzb * wl.b * wl.b, 2)
+        return {k: w[k] for k in ("spmm_fwd", "spmm_bwd_data", "sddmm")}
+
+    def extra(self):
+        rows = []
+        for ms in self.strides:
+            tf = timed(self.torch, lambda ms=ms: self._flat(ms), 20, 3)
+            tp = timed(self.torch, lambda ms=ms: self._product(ms), 20, 3)
+            rows.append({"max_stride": ms, "flat_ms": tf, "product_ms": tp,
+                         "product_over_flat": tp / tf,
+                         "factors": len([k for k in self.strides if k <= ms])})
+        return {"flat_vs_product": rows}
+
+    def dense_setup(self):
+        torch, wl = self.torch, self.wl
+        self.Wd = torch.randn(wl.N, wl.K, dtype=torch.bfloat16, device="cuda") * 0.02
+        self.dWd = torch.empty(wl.N, wl.K, dtype=torch.bfloat16, device="cuda")
+        self.dwsb = self.pf.pf_dense_workspace_bytes("bf16", self.pf.PF_OP_TN, wl.N, wl.K, wl.T)
+        self.dws = torch.empty(max(self.dwsb, 256), dtype=torch.uint8, device="cuda")
+
+    def dense_step(self):
+        pf, wl = self.pf, self.wl
+        pf.pf_dense_gemm("bf16", pf.PF_OP_NT, wl.T, wl.N, wl.K, self.X, self.Wd, self.Y)
+        pf.pf_dense_gemm("bf16", pf.PF_OP_NN, wl.T, wl.K, wl.N, self.dY, self.Wd, self.dX)
+        pf.pf_dense_gemm("bf16", pf.PF_OP_TN, wl.N, wl.K, wl.T, self.dY, self.X, self.dWd,
+                         self.dws, self.dwsb)
+
+    def torch_dense_step(self):
+        torch = self.torch
+        torch.matmul(self.X, self.Wd.t(), out=self.Y)
+        torch.matmul(self.dY, self.Wd, out=self.dX)
+        torch.matmul(self.dY.t(), self.X, out=self.dWd)
+
+    def cpu_baseline(self, budget_s=12.0):
+        from oracle import linear as ol
+        from oracle import mask as om
+        wl = self.wl
+        M, (row_ptr, col_idx, *_x) = om.layout(wl.N, wl.K, wl.b, wl.max_stride)
+        Mel = om.element_mask(M, wl.b)
+        Ts = 1024
+        X = synth.draw((Ts, wl.K), 1.0, 0, 1, "bf16")[0]
+        dY = synth.draw((Ts, wl.N), 1.0, 0, 5, "bf16")[0]
+        W = synth.draw((int(M.sum()), wl.b, wl.b), 0.1, 0, 2, "bf16")[0]
+        Wd = ol.unpack(W, row_ptr, col_idx, wl.N // wl.b, wl.K // wl.b, wl.b)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            ol.forward(X, Wd)
+            ol.backward(X, Wd, Mel, dY)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= budget_s or reps >= 1000:
+                break
+        fl = 3 * 2 * Ts * int(M.sum()) * wl.b * wl.b * reps
+        return fl / el / 1e12, f"oracle flat fwd+bwd (fp64, dense masked) on {Ts} of {wl.T} tokens x {reps} reps, {el:.1f} s"
+
+
 def _layer_work(T, K, N, r, w, e):
     """(flops, bytes) per step of the kernel classes of one K -> N layer with
     w kept weight elements, r-rank factors and e-byte elements."""
@@ -567,7 +697,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     wl = synth.WORKLOADS[args.workload]
     R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention,
-         "patterns": Patterns}[wl.kind](torch, pf, wl)
+         "patterns": Patterns, "butterfly": Butterfly}[wl.kind](torch, pf, wl)
 
     if args.copy_probe:
         n = args.copy_probe << 20
@@ -671,6 +801,8 @@ def main():
     if wl.kind == "attention":
         cfg.update(B=wl.B, H=wl.H, S=wl.S, d=wl.d, b=wl.b, max_stride=wl.max_stride,
                    global_blocks=wl.global_blocks)
+    elif wl.kind == "butterfly":
+        cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=wl.max_stride, r=0)
     elif wl.kind == "patterns":
         cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=R.ms, r=R.r, budget=Patterns.DENSITY)
     else:

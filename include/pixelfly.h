@@ -147,6 +147,22 @@ pf_status pf_layout_create_from_element_mask(int64_t n_out, int64_t n_in, int32_
                                              const uint8_t *elem_mask, pf_layout **out);
 
 /*
+ * Layout of one factor of the butterfly product form, I + B_k, for an n x n
+ * matrix with block size b: the butterfly factor matrix B_k^{(n/b)}
+ * (Section 3.1: n/(b k) block-diagonal copies of a size-k factor
+ * [[D1 D2],[D3 D4]] with diagonal D_i, in b x b block units) plus the
+ * identity, i.e. block (p, q) kept iff p == q or p XOR q == k / 2: two
+ * blocks per block row.  The residual butterfly (I + lam B_n) ... (I +
+ * lam B_2) (Section 3.2) runs as a chain of layers on these layouts, its
+ * flat first-order term as one layer on pf_layout_create(n, n, b, k_max);
+ * the appendix on benchmarking the butterfly multiply compares the two.
+ * Requires b >= 1 dividing n, n / b <= 16384, k a power of two >= 2
+ * dividing n / b.  max_stride and eff_stride read k.  Host only.
+ * Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_layout_create_factor(int64_t n, int32_t b, int32_t k, pf_layout **out);
+
+/*
  * Mask selection for one layer from a compute budget (Section 3.3, step 2):
  * a share lowrank_share of the budget (the paper's rule of thumb: one
  * quarter to one third) goes to the low-rank part, whose rank is the largest

@@ -464,6 +464,29 @@ pf_status pf_layout_create_from_element_mask(int64_t n_out, int64_t n_in, int32_
   return PF_OK;
 }
 
+pf_status pf_layout_create_factor(int64_t n, int32_t b, int32_t k, pf_layout **out) {
+  if (!out) return fail(PF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  pf_layout *L = new (std::nothrow) pf_layout();
+  if (!L) return fail(PF_ERR_NOMEM, "host allocation failed");
+  std::string e;
+  try {
+    e = pf::build_factor_layout(*L, n, b, k);
+  } catch (const std::bad_alloc &) {
+    delete L;
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  } catch (...) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, "layout build failed");
+  }
+  if (!e.empty()) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, e);
+  }
+  *out = L;
+  return PF_OK;
+}
+
 pf_status pf_select_mask(int64_t n_out, int64_t n_in, int32_t b, double budget,
                          double lowrank_share, int32_t *r_out, int32_t *max_stride_out,
                          int64_t *params_out) {

@@ -216,6 +216,26 @@ std::string build_attention_layout(pf_layout &L, int64_t seq, int32_t b, int32_t
   return "";
 }
 
+// One butterfly factor of the product form, I + B_k of the factor matrix
+// B_k^{(n/b)} (Section 3.1: block-diagonal copies of a size-k factor whose
+// quadrants are diagonal), in block units: (p, q) kept iff p == q or
+// p XOR q == k / 2.
+std::string build_factor_layout(pf_layout &L, int64_t n, int32_t b, int32_t k) {
+  if (b < 1 || n < b || n % b) return "b must be >= 1 and divide n";
+  const int64_t nb = n / b;
+  if (nb > 16384) return "n / b must be <= 16384";
+  if (k < 2 || (k & (k - 1)) || k > nb || nb % k)
+    return "k must be a power of two >= 2 dividing n / b";
+  std::vector<uint8_t> m((size_t)nb * nb, 0);
+  for (int64_t p = 0; p < nb; ++p) {
+    m[(size_t)p * nb + p] = 1;
+    m[(size_t)p * nb + (p ^ (k / 2))] = 1;
+  }
+  std::string e = build_layout_from_mask(L, (int32_t)nb, (int32_t)nb, b, m.data());
+  if (e.empty()) L.max_stride = L.eff_stride = k;
+  return e;
+}
+
 // Layout of the (b, b)-block cover of an element mask (appendix on the cost
 // model: the block-aligned mask with the fewest nonzeros containing it):
 // block (i, j) is kept iff any element of it is nonzero.

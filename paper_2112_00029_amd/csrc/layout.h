@@ -52,6 +52,8 @@ std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, 
 // first global_blocks block rows and columns.
 std::string build_attention_layout(pf_layout &L, int64_t seq, int32_t b, int32_t max_stride,
                                    int32_t global_blocks);
+// Layout of I + B_k (one factor of the butterfly product form), n x n.
+std::string build_factor_layout(pf_layout &L, int64_t n, int32_t b, int32_t k);
 // Layout of the (b, b)-block cover of an n_out x n_in element mask.
 std::string build_cover_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
                                const uint8_t *elem_mask);

@@ -69,6 +69,7 @@ _SIGS = {
     "pf_layout_create_from_mask": (_i32, [_i32, _i32, _i32, _p, ctypes.POINTER(_p)]),
     "pf_layout_create_attention": (_i32, [_i64, _i32, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_create_from_element_mask": (_i32, [_i64, _i64, _i32, _p, ctypes.POINTER(_p)]),
+    "pf_layout_create_factor": (_i32, [_i64, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_select_mask": (_i32, [_i64, _i64, _i32, ctypes.c_double, ctypes.c_double,
                               ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "pf_layout_info_get": (_i32, [_p, ctypes.POINTER(pf_layout_info)]),
@@ -198,6 +199,12 @@ def pf_layout_create_from_element_mask(n_out: int, n_in: int, b: int, elem_mask)
     h = _p()
     _check(_lib.pf_layout_create_from_element_mask(n_out, n_in, b, m.ctypes.data_as(_p),
                                                    ctypes.byref(h)))
+    return Layout(h.value)
+
+
+def pf_layout_create_factor(n: int, b: int, k: int) -> Layout:
+    h = _p()
+    _check(_lib.pf_layout_create_factor(n, b, k, ctypes.byref(h)))
     return Layout(h.value)
 
 

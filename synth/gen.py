@@ -108,6 +108,12 @@ WORKLOADS = {
     # selected for a 10% budget, on the 32 x 32 block cover of each pattern.
     "patterns_4096x4096": Workload(
         "patterns_4096x4096", "patterns", "bf16", T=4096, K=4096, N=4096, b=32),
+    # Flat butterfly vs its product form (appendix on benchmarking the
+    # butterfly multiply): 1024 x 1024, 32 x 32 blocks, batch 2048, maximum
+    # stride swept 2 .. 32; the timed step is the flat layer at stride 32.
+    "butterfly_1024_b32": Workload(
+        "butterfly_1024_b32", "butterfly", "bf16", T=2048, K=1024, N=1024, b=32,
+        max_stride=32, std_x=1.0, std_dy=1.0),
     # Large layer 4096 -> 16384, 16384 tokens, 128x128 blocks, strides < 32.
     "linear_16384x4096_b128": Workload(
         "linear_16384x4096_b128", "linear", "bf16", T=16384, K=4096, N=16384,

@@ -1,0 +1,69 @@
+"""GPU parity of the butterfly product form (Section 3.2: a product of
+factors with the support of I + B_k, largest stride leftmost) run as a chain
+of block-sparse layers on pf_layout_create_factor layouts, against the dense
+product of the same factors: forward, input gradient through the chain, and
+the gradient of the last factor on its blocks.  bf16, rel. Frobenius <= 2e-2
+(every link stores its activation in bf16)."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import linear as ol
+from oracle import mask as om
+from tests._gpu_util import TOL, empty, rel_fro, to_dev, to_host, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("n,b,ms,T", [(1024, 32, 8, 300), (1024, 32, 32, 2048), (512, 64, 8, 130)])
+def test_product_chain(n, b, ms, T):
+    torch = torch_cuda()
+    from paper_2112_00029_amd import pixelfly as pf
+    print(f"[butterfly] n={n} b={b} max_stride={ms} T={T}", flush=True)
+    nb = n // b
+    ks = [k for k in (2, 4, 8, 16, 32, 64, 128) if k <= min(ms, nb)]
+    X, Xr = synth.draw((T, n), 1.0, 3, 1, "bf16")
+    dY, dYr = synth.draw((T, n), 1.0, 3, 5, "bf16")
+    F, layouts, Wdev = {}, {}, {}
+    for i, k in enumerate(ks):
+        S = om.factor_matrix_support(nb, k)
+        row_ptr, col_idx, *_r = om.block_csr(S)
+        P, Pr = synth.draw((2 * nb, b, b), 1.0 / np.sqrt(2 * b), 3, 20 + i, "bf16")
+        F[k] = ol.unpack(P, row_ptr, col_idx, nb, nb, b)
+        L = pf.pf_layout_create_factor(n, b, k)
+        pf.pf_layout_upload(L)
+        layouts[k], Wdev[k] = L, to_dev(Pr)
+    wsb = max(pf.pf_workspace_bytes(layouts[k], T, 0, "bf16") for k in ks)
+    ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device="cuda")
+    acts = [to_dev(Xr)]
+    for k in ks:  # x <- x F_k^T, smallest stride first
+        y = empty((T, n), "bf16")
+        pf.pf_linear_fwd(layouts[k], "bf16", T, 0, acts[-1], Wdev[k], None, None, y, None,
+                         workspace=ws, ws_bytes=wsb)
+        acts.append(y)
+    g = to_dev(dYr)
+    dF_last = None
+    for i, k in reversed(list(enumerate(ks))):
+        if i == len(ks) - 1:
+            dF_last = empty((2 * nb, b, b), "bf16")
+            pf.pf_linear_bwd_weight(layouts[k], "bf16", T, 0, g, acts[i], None, None, dF_last,
+                                    None, None, ws, wsb)
+        gx = empty((T, n), "bf16")
+        pf.pf_linear_bwd_data(layouts[k], "bf16", T, 0, g, Wdev[k], None, None, None, gx,
+                              workspace=ws, ws_bytes=wsb)
+        g = gx
+    torch.cuda.synchronize()
+    M = np.eye(n)
+    for k in reversed(ks):
+        M = M @ F[k]  # F_kmax ... F_2
+    x_prev = X.copy()
+    for k in ks[:-1]:
+        x_prev = x_prev @ F[k].T
+    S_last = om.element_mask(om.factor_matrix_support(nb, ks[-1]), b)
+    row_ptr, col_idx, *_r = om.block_csr(om.factor_matrix_support(nb, ks[-1]))
+    ref = {"Y": X @ M.T, "dX": dY @ M, "dF_last": ol.pack((dY.T @ x_prev) * S_last, row_ptr, col_idx, nb, b)}
+    got = {"Y": to_host(acts[-1]), "dX": to_host(g), "dF_last": to_host(dF_last)}
+    for key in ref:
+        e = rel_fro(got[key], ref[key])
+        print(f"  {key}: rel_fro={e:.3e}", flush=True)
+        assert e <= TOL["bf16"], (key, e)

@@ -254,3 +254,22 @@ def test_cover_layout_errors():
     E2[:32] = True  # second block row empty
     with pytest.raises(pf.PixelflyError):
         pf.pf_layout_create_from_element_mask(64, 64, 32, E2)
+
+
+@pytest.mark.parametrize("n,b,k", [(1024, 32, 2), (1024, 32, 32), (512, 64, 4), (64, 1, 64)])
+def test_factor_layout_vs_oracle(n, b, k):
+    """pf_layout_create_factor against the oracle's factor-matrix support
+    (built from the butterfly factor definition) plus the identity."""
+    L = pf.pf_layout_create_factor(n, b, k)
+    info = pf.pf_layout_info_get(L)
+    S = om.factor_matrix_support(n // b, k) | np.eye(n // b, dtype=bool)
+    ref = om.block_csr(S)
+    for name, r in zip(["row_ptr", "col_idx", "col_ptr", "row_idx", "tperm"], ref):
+        assert np.array_equal(info[name], r), name
+    assert info["nnzb"] == 2 * (n // b)
+
+
+def test_factor_layout_errors():
+    for args in [(1024, 32, 3), (1024, 32, 64), (1000, 32, 2), (1024, 32, 1)]:
+        with pytest.raises(pf.PixelflyError):
+            pf.pf_layout_create_factor(*args)
