@@ -249,11 +249,18 @@ SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   return p;
 }
 
-// Split-token plan of the TN kernel: aim for about 4096 workgroups (token
-// splits also shorten each workgroup's serial chain and its L2 footprint),
-// power-of-two splits of at least 512 tokens, at most PF_TN_MAX_SPLIT; and
-// enough splits that one split's rows stay below 2^31 bytes (32-bit buffer
-// offsets).
+// Split-token plan of the TN kernel.  Few work items (under one round of
+// kTNSlots resident workgroups): the split of at most PF_TN_MAX_SPLIT parts of
+// at least 512 tokens that minimises rounds x steps per workgroup.  Many
+// items: aim for about 4096 workgroups (token splits also shorten each
+// workgroup's serial chain and its L2 footprint) with power-of-two splits of
+// at least 512 tokens, at most PF_TN_MAX_SPLIT, keeping the fp32 partial
+// traffic in check.  Always enough splits that one split's rows stay below
+// 2^31 bytes (32-bit buffer offsets).
+constexpr int64_t kTNSlots = 512;  // two TN workgroups per CU on 256 CUs
+#ifndef PF_TN_ROUND_ITEMS
+#define PF_TN_ROUND_ITEMS kTNSlots
+#endif
 #ifndef PF_TN_MAX_SPLIT
 #define PF_TN_MAX_SPLIT 8
 #endif
@@ -268,9 +275,24 @@ TNPlan tn_plan(int items, int64_t T, int64_t row_bytes) {
   TNPlan p{1, ((T + 63) / 64) * 64, 0};
   const int64_t min_split = (T * row_bytes + 0x7fffffffLL - 1) / 0x7fffffffLL;
   int64_t ns = 1;
-  const int64_t want = std::max<int64_t>(1, 4096 / std::max(1, items));
   const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(PF_TN_MAX_SPLIT, T / 512));
-  while (ns * 2 <= std::min(want, cap)) ns *= 2;
+  if (items < PF_TN_ROUND_ITEMS) {
+    // Few items: the split that finishes soonest when kTNSlots workgroups
+    // run at a time, i.e. fewest (rounds x 64-token steps per workgroup);
+    // the smaller split on ties (fewer partials).
+    int64_t best = -1;
+    for (int64_t c = 1; c <= cap; ++c) {
+      const int64_t chunk = ((T + c - 1) / c + 63) / 64 * 64, nsr = (T + chunk - 1) / chunk;
+      const int64_t cost = ((items * nsr + kTNSlots - 1) / kTNSlots) * (chunk / 64);
+      if (best < 0 || cost < best) {
+        best = cost;
+        ns = nsr;
+      }
+    }
+  } else {
+    const int64_t want = std::max<int64_t>(1, 4096 / std::max(1, items));
+    while (ns * 2 <= std::min(want, cap)) ns *= 2;
+  }
   ns = std::max(ns, min_split);
   if (ns > 1) {
     const int64_t chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
