@@ -124,12 +124,20 @@ __device__ __forceinline__ void attn_order(int L, int BH, int nb, int nlong, int
 
 // Forward
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BQ * LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BQ * LDV];
+// NG groups of 4 waves share one 64-query block: group g takes the row's
+// kept blocks g, g + NG, ... (each group has its own double-buffered K/V
+// tiles; all groups run the same number of iterations so every barrier is
+// reached by the whole workgroup) and the groups' softmax states (reference,
+// sum, unnormalised O) are merged through LDS in group order at the end.
+// NG = 1 is the plain kernel; NG = 4 serves the long rows of global stripes.
+template <int NG>
+__global__ __launch_bounds__(256 * NG) void attn_fwd_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[NG][2][BQ * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[NG][2][BQ * LDV];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
+  const int grp = NG > 1 ? __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8) : 0;
+  const int bid = xcd_remap_a(blockIdx.x, gridDim.x) + a.first;
   int bh, qb;
   attn_order(bid, a.BH, a.nbq, a.nlong, bh, qb);
   const int64_t head = (int64_t)bh * a.S * D;
@@ -144,76 +152,121 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
   qf[1] = frag_rows_g(Q, q0, 32, lane);
 
   const int p0 = a.row_ptr[qb], p1 = a.row_ptr[qb + 1];
+  const int iters = (p1 - p0 + NG - 1) / NG;
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   Tile64 tk, tv;
-  tk.load(K + (int64_t)a.col_idx[p0] * BQ * D, tid);
-  tv.load(V + (int64_t)a.col_idx[p0] * BQ * D, tid);
-  tk.store(Ks[0], LDK, tid);
-  tv.store(Vs[0], LDV, tid);
+  if (p0 + grp < p1) {
+    tk.load(K + (int64_t)a.col_idx[p0 + grp] * BQ * D, tid);
+    tv.load(V + (int64_t)a.col_idx[p0 + grp] * BQ * D, tid);
+    tk.store(Ks[grp][0], LDK, tid);
+    tv.store(Vs[grp][0], LDV, tid);
+  }
   __syncthreads();
 
-  for (int p = p0; p < p1; ++p) {
-    const int cur = (p - p0) & 1;
-    if (p + 1 < p1) {
-      tk.load(K + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
-      tv.load(V + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
+  for (int it = 0; it < iters; ++it) {
+    const int cur = it & 1;
+    const int p = p0 + it * NG + grp;
+    const bool valid = p < p1, next = p + NG < p1;
+    if (next) {
+      tk.load(K + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
+      tv.load(V + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
     }
-    // S^T[key][query] for 64 keys x this wave's 16 queries.
-    f32x4 s[4];
+    if (valid) {
+      // S^T[key][query] for 64 keys x this wave's 16 queries.
+      f32x4 s[4];
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt) {
-      s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 0, lane), qf[0], s[mt]);
-      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 32, lane), qf[1], s[mt]);
+      for (int mt = 0; mt < 4; ++mt) {
+        s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        s[mt] = MFMA16(frag_rows(Ks[grp][cur], LDK, mt * 16, 0, lane), qf[0], s[mt]);
+        s[mt] = MFMA16(frag_rows(Ks[grp][cur], LDK, mt * 16, 32, lane), qf[1], s[mt]);
+      }
+      float bmax = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bmax = fmaxf(bmax, s[mt][j]);
+      bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
+      bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+      // The softmax reference m_run moves only when some row's maximum grew
+      // by more than 8 (log2 units): until then the probabilities stay below
+      // 2^8 and the rescale of O and l, a wave-uniform branch, is skipped.
+      const float m_cand = fmaxf(m_run, bmax * c);
+      if (__builtin_amdgcn_ballot_w64(m_cand > m_run + 8.0f)) {
+        const float alpha = fast_exp2(m_run - m_cand);
+        m_run = m_cand;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) o[dt][j] *= alpha;
+      }
+      float rs = 0.f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float e = fast_exp2(s[mt][j] * c - m_run);
+          s[mt][j] = e;
+          rs += e;
+        }
+      rs += __shfl_xor(rs, 16);
+      rs += __shfl_xor(rs, 32);
+      l_run += rs;
+      // O^T[dim][query] += V^T[dim][key] P^T[key][query]
+      const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        o[dt] = MFMA16(fragA_tr_perm(Vs[grp][cur], LDV, 0, dt * 16, lane), pb0, o[dt]);
+        o[dt] = MFMA16(fragA_tr_perm(Vs[grp][cur], LDV, 32, dt * 16, lane), pb1, o[dt]);
+      }
     }
-    float bmax = -INFINITY;
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bmax = fmaxf(bmax, s[mt][j]);
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-    // The softmax reference m_run moves only when some row's maximum grew by
-    // more than 8 (log2 units): until then the probabilities stay below 2^8
-    // and the rescale of O and l, a wave-uniform branch, is skipped.
-    const float m_cand = fmaxf(m_run, bmax * c);
-    if (__builtin_amdgcn_ballot_w64(m_cand > m_run + 8.0f)) {
-      const float alpha = fast_exp2(m_run - m_cand);
-      m_run = m_cand;
-      l_run *= alpha;
+    if (next) {
+      tk.store(Ks[grp][cur ^ 1], LDK, tid);
+      tv.store(Vs[grp][cur ^ 1], LDV, tid);
+    }
+    __syncthreads();
+  }
+
+  if constexpr (NG > 1) {
+    // Merge: groups 1.. leave (m, l, o) per lane in their K tiles (18 floats
+    // x 64 lanes x 4 waves = exactly one group's K tiles), group 0 combines
+    // them relative to the largest reference.  A group without blocks has
+    // m = -inf and contributes 0.
+    float *mrg = (float *)&Ks[grp][0][0] + wave * (18 * 64) + lane;
+    if (grp > 0) {
+      mrg[0] = m_run;
+      mrg[64] = l_run;
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) o[dt][j] *= alpha;
-    }
-    float rs = 0.f;
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float e = fast_exp2(s[mt][j] * c - m_run);
-        s[mt][j] = e;
-        rs += e;
-      }
-    rs += __shfl_xor(rs, 16);
-    rs += __shfl_xor(rs, 32);
-    l_run += rs;
-    // O^T[dim][query] += V^T[dim][key] P^T[key][query]
-    const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
-#pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      o[dt] = MFMA16(fragA_tr_perm(Vs[cur], LDV, 0, dt * 16, lane), pb0, o[dt]);
-      o[dt] = MFMA16(fragA_tr_perm(Vs[cur], LDV, 32, dt * 16, lane), pb1, o[dt]);
-    }
-    if (p + 1 < p1) {
-      tk.store(Ks[cur ^ 1], LDK, tid);
-      tv.store(Vs[cur ^ 1], LDV, tid);
+        for (int j = 0; j < 4; ++j) mrg[(2 + dt * 4 + j) * 64] = o[dt][j];
     }
     __syncthreads();
+    if (grp > 0) return;
+    float m = m_run;
+#pragma unroll
+    for (int g = 1; g < NG; ++g) m = fmaxf(m, ((float *)&Ks[g][0][0])[wave * (18 * 64) + lane]);
+    const float s0 = fast_exp2(m_run - m);
+    l_run *= s0;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[dt][j] *= s0;
+#pragma unroll
+    for (int g = 1; g < NG; ++g) {
+      const float *src = (const float *)&Ks[g][0][0] + wave * (18 * 64) + lane;
+      const float sg = src[0] == -INFINITY ? 0.f : fast_exp2(src[0] - m);
+      l_run += src[64] * sg;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[dt][j] += src[(2 + dt * 4 + j) * 64] * sg;
+    }
+    m_run = m;
   }
 
   const float inv = 1.f / l_run;
@@ -232,12 +285,16 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Backward, pass 1: delta and dQ (one workgroup per query block)
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BQ * LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BQ * LDK];
+// NG groups of 4 waves split the row's kept blocks as in the forward; their
+// dQ partial sums are added through LDS in group order.
+template <int NG>
+__global__ __launch_bounds__(256 * NG) void attn_bwd_dq_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[NG][2][BQ * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[NG][2][BQ * LDK];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
+  const int grp = NG > 1 ? __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8) : 0;
+  const int bid = xcd_remap_a(blockIdx.x, gridDim.x) + a.first;
   int bh, qb;
   attn_order(bid, a.BH, a.nbq, a.nlong, bh, qb);
   const int64_t head = (int64_t)bh * a.S * D;
@@ -273,36 +330,42 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
     delta += __shfl_xor(delta, 16);
     delta += __shfl_xor(delta, 32);
   }
-  if (lane < 16) a.delta[(int64_t)bh * a.S + q] = delta;
+  if (lane < 16 && grp == 0) a.delta[(int64_t)bh * a.S + q] = delta;
   const float lse2 = a.lse_in[(int64_t)bh * a.S + q] * kLog2e;
 
   const int p0 = a.row_ptr[qb], p1 = a.row_ptr[qb + 1];
+  const int iters = (p1 - p0 + NG - 1) / NG;
   f32x4 dq[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) dq[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   Tile64 tk, tv;
-  tk.load(K + (int64_t)a.col_idx[p0] * BQ * D, tid);
-  tv.load(V + (int64_t)a.col_idx[p0] * BQ * D, tid);
-  tk.store(Ks[0], LDK, tid);
-  tv.store(Vs[0], LDK, tid);
+  if (p0 + grp < p1) {
+    tk.load(K + (int64_t)a.col_idx[p0 + grp] * BQ * D, tid);
+    tv.load(V + (int64_t)a.col_idx[p0 + grp] * BQ * D, tid);
+    tk.store(Ks[grp][0], LDK, tid);
+    tv.store(Vs[grp][0], LDK, tid);
+  }
   __syncthreads();
 
-  for (int p = p0; p < p1; ++p) {
-    const int cur = (p - p0) & 1;
-    if (p + 1 < p1) {
-      tk.load(K + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
-      tv.load(V + (int64_t)a.col_idx[p + 1] * BQ * D, tid);
+  for (int it = 0; it < iters; ++it) {
+    const int cur = it & 1;
+    const int p = p0 + it * NG + grp;
+    const bool valid = p < p1, next = p + NG < p1;
+    if (next) {
+      tk.load(K + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
+      tv.load(V + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
     }
+    if (valid) {
     f32x4 s[4], dp[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 0, lane), qf[0], s[mt]);
-      s[mt] = MFMA16(frag_rows(Ks[cur], LDK, mt * 16, 32, lane), qf[1], s[mt]);
+      s[mt] = MFMA16(frag_rows(Ks[grp][cur], LDK, mt * 16, 0, lane), qf[0], s[mt]);
+      s[mt] = MFMA16(frag_rows(Ks[grp][cur], LDK, mt * 16, 32, lane), qf[1], s[mt]);
       dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      dp[mt] = MFMA16(frag_rows(Vs[cur], LDK, mt * 16, 0, lane), dof[0], dp[mt]);
-      dp[mt] = MFMA16(frag_rows(Vs[cur], LDK, mt * 16, 32, lane), dof[1], dp[mt]);
+      dp[mt] = MFMA16(frag_rows(Vs[grp][cur], LDK, mt * 16, 0, lane), dof[0], dp[mt]);
+      dp[mt] = MFMA16(frag_rows(Vs[grp][cur], LDK, mt * 16, 32, lane), dof[1], dp[mt]);
     }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
@@ -314,14 +377,37 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
     const bf16x8 d0 = pack_perm(s[0], s[1]), d1 = pack_perm(s[2], s[3]);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      dq[dt] = MFMA16(fragA_tr_perm(Ks[cur], LDK, 0, dt * 16, lane), d0, dq[dt]);
-      dq[dt] = MFMA16(fragA_tr_perm(Ks[cur], LDK, 32, dt * 16, lane), d1, dq[dt]);
+      dq[dt] = MFMA16(fragA_tr_perm(Ks[grp][cur], LDK, 0, dt * 16, lane), d0, dq[dt]);
+      dq[dt] = MFMA16(fragA_tr_perm(Ks[grp][cur], LDK, 32, dt * 16, lane), d1, dq[dt]);
     }
-    if (p + 1 < p1) {
-      tk.store(Ks[cur ^ 1], LDK, tid);
-      tv.store(Vs[cur ^ 1], LDK, tid);
+    }
+    if (next) {
+      tk.store(Ks[grp][cur ^ 1], LDK, tid);
+      tv.store(Vs[grp][cur ^ 1], LDK, tid);
     }
     __syncthreads();
+  }
+
+  if constexpr (NG > 1) {
+    // Groups 1.. leave their 16 partial sums per lane in their K tiles;
+    // group 0 adds them in group order.
+    float *mrg = (float *)&Ks[grp][0][0] + wave * (16 * 64) + lane;
+    if (grp > 0) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mrg[(dt * 4 + j) * 64] = dq[dt][j];
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g = 1; g < NG; ++g) {
+      const float *src = (const float *)&Ks[g][0][0] + wave * (16 * 64) + lane;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dq[dt][j] += src[(dt * 4 + j) * 64];
+    }
   }
 
   bf16_t *dQ = (bf16_t *)a.dQ + head + (int64_t)q * D;
@@ -337,13 +423,17 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Backward, pass 2: dK and dV (one workgroup per key block)
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[2][BQ * LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t dOs[2][BQ * LDK];
-  __shared__ float ls[2][BQ], ds[2][BQ];
+// NG groups of 4 waves split the column's kept blocks as in the forward;
+// their dK and dV partial sums are added through LDS in group order.
+template <int NG>
+__global__ __launch_bounds__(256 * NG) void attn_bwd_dkv_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[NG][2][BQ * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t dOs[NG][2][BQ * LDK];
+  __shared__ float ls[NG][2][BQ], ds[NG][2][BQ];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int bid = xcd_remap_a(blockIdx.x, gridDim.x);
+  const int tid = threadIdx.x & 255, lane = tid & 63, wave = tid >> 6;
+  const int grp = NG > 1 ? __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8) : 0;
+  const int bid = xcd_remap_a(blockIdx.x, gridDim.x) + a.first;
   int bh, kb;
   attn_order(bid, a.BH, a.nbq, a.nlong, bh, kb);
   const int64_t head = (int64_t)bh * a.S * D;
@@ -380,49 +470,87 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
     if (tid < BQ) { rl = lse[qrow + tid] * kLog2e; rd = dl[qrow + tid]; }
   };
   auto sstore = [&](int buf) {
-    tq.store(Qs[buf], LDK, tid);
-    td.store(dOs[buf], LDK, tid);
-    if (tid < BQ) { ls[buf][tid] = rl; ds[buf][tid] = rd; }
+    tq.store(Qs[grp][buf], LDK, tid);
+    td.store(dOs[grp][buf], LDK, tid);
+    if (tid < BQ) { ls[grp][buf][tid] = rl; ds[grp][buf][tid] = rd; }
   };
-  gload(p0);
-  sstore(0);
+  const int iters = (p1 - p0 + NG - 1) / NG;
+  if (p0 + grp < p1) {
+    gload(p0 + grp);
+    sstore(0);
+  }
   __syncthreads();
 
-  for (int p = p0; p < p1; ++p) {
-    const int cur = (p - p0) & 1;
-    if (p + 1 < p1) gload(p + 1);
+  for (int it = 0; it < iters; ++it) {
+    const int cur = it & 1;
+    const int p = p0 + it * NG + grp;
+    const bool valid = p < p1, next = p + NG < p1;
+    if (next) gload(p + NG);
+    if (valid) {
     // S[query][key], dP[query][key] for 64 queries x this wave's 16 keys.
     f32x4 s[4], dp[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
       s[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      s[mt] = MFMA16(frag_rows(Qs[cur], LDK, mt * 16, 0, lane), kf[0], s[mt]);
-      s[mt] = MFMA16(frag_rows(Qs[cur], LDK, mt * 16, 32, lane), kf[1], s[mt]);
+      s[mt] = MFMA16(frag_rows(Qs[grp][cur], LDK, mt * 16, 0, lane), kf[0], s[mt]);
+      s[mt] = MFMA16(frag_rows(Qs[grp][cur], LDK, mt * 16, 32, lane), kf[1], s[mt]);
       dp[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      dp[mt] = MFMA16(frag_rows(dOs[cur], LDK, mt * 16, 0, lane), vf[0], dp[mt]);
-      dp[mt] = MFMA16(frag_rows(dOs[cur], LDK, mt * 16, 32, lane), vf[1], dp[mt]);
+      dp[mt] = MFMA16(frag_rows(dOs[grp][cur], LDK, mt * 16, 0, lane), vf[0], dp[mt]);
+      dp[mt] = MFMA16(frag_rows(dOs[grp][cur], LDK, mt * 16, 32, lane), vf[1], dp[mt]);
     }
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int qi = mt * 16 + (lane >> 4) * 4 + j;
-        const float pr = fast_exp2(s[mt][j] * c - ls[cur][qi]);
+        const float pr = fast_exp2(s[mt][j] * c - ls[grp][cur][qi]);
         s[mt][j] = pr;
-        dp[mt][j] = pr * (dp[mt][j] - ds[cur][qi]);  // dS
+        dp[mt][j] = pr * (dp[mt][j] - ds[grp][cur][qi]);  // dS
       }
     const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
     const bf16x8 sb0 = pack_perm(dp[0], dp[1]), sb1 = pack_perm(dp[2], dp[3]);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      dv[dt] = MFMA16(fragA_tr_perm(dOs[cur], LDK, 0, dt * 16, lane), pb0, dv[dt]);
-      dv[dt] = MFMA16(fragA_tr_perm(dOs[cur], LDK, 32, dt * 16, lane), pb1, dv[dt]);
-      dk[dt] = MFMA16(fragA_tr_perm(Qs[cur], LDK, 0, dt * 16, lane), sb0, dk[dt]);
-      dk[dt] = MFMA16(fragA_tr_perm(Qs[cur], LDK, 32, dt * 16, lane), sb1, dk[dt]);
+      dv[dt] = MFMA16(fragA_tr_perm(dOs[grp][cur], LDK, 0, dt * 16, lane), pb0, dv[dt]);
+      dv[dt] = MFMA16(fragA_tr_perm(dOs[grp][cur], LDK, 32, dt * 16, lane), pb1, dv[dt]);
+      dk[dt] = MFMA16(fragA_tr_perm(Qs[grp][cur], LDK, 0, dt * 16, lane), sb0, dk[dt]);
+      dk[dt] = MFMA16(fragA_tr_perm(Qs[grp][cur], LDK, 32, dt * 16, lane), sb1, dk[dt]);
     }
-    if (p + 1 < p1) sstore(cur ^ 1);
+    }
+    if (next) sstore(cur ^ 1);
     __syncthreads();
   }
+  }
+
+  if constexpr (NG > 1) {
+    // Groups 1.. leave their 32 partial sums per lane in their Q and dO
+    // tiles; group 0 adds them in group order.  (The key block's kept-block
+    // count is workgroup-uniform, so every thread reaches this barrier.)
+    float *mk = (float *)&Qs[grp][0][0] + wave * (16 * 64) + lane;
+    float *mv = (float *)&dOs[grp][0][0] + wave * (16 * 64) + lane;
+    if (grp > 0) {
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          mk[(dt * 4 + j) * 64] = dk[dt][j];
+          mv[(dt * 4 + j) * 64] = dv[dt][j];
+        }
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g = 1; g < NG; ++g) {
+      const float *sk = (const float *)&Qs[g][0][0] + wave * (16 * 64) + lane;
+      const float *sv = (const float *)&dOs[g][0][0] + wave * (16 * 64) + lane;
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          dk[dt][j] += sk[(dt * 4 + j) * 64];
+          dv[dt][j] += sv[(dt * 4 + j) * 64];
+        }
+    }
   }
 
   const int key = k0 + (lane & 15);
@@ -440,25 +568,42 @@ __global__ __launch_bounds__(256) void attn_bwd_dkv_kernel(AttnArgs a) {
   }
 }
 
-hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s) {
-  const int64_t grid = (int64_t)a.BH * a.nbq;
+// Launchers.  part 0: every block row (column) with the plain kernel;
+// part 1: the nlong global rows (columns) of every head with the grouped
+// kernel; part 2: the remaining rows with the plain kernel.
+namespace {
+template <typename F1, typename FG>
+hipError_t attn_launch(F1 plain, FG grouped, int ng, AttnArgs a, int part, hipStream_t s) {
+  int64_t grid;
+  if (part == 1) {
+    grid = (int64_t)a.BH * a.nlong;
+    a.first = 0;
+  } else if (part == 2) {
+    grid = (int64_t)a.BH * (a.nbq - a.nlong);
+    a.first = a.BH * a.nlong;
+  } else {
+    grid = (int64_t)a.BH * a.nbq;
+    a.first = 0;
+  }
   if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  launch_kernel(attn_fwd_kernel, dim3((unsigned)grid), dim3(256), s, a);
+  if (part == 1)
+    launch_kernel(grouped, dim3((unsigned)grid), dim3(256 * ng), s, a);
+  else
+    launch_kernel(plain, dim3((unsigned)grid), dim3(256), s, a);
   return hipGetLastError();
 }
+}  // namespace
 
-hipError_t launch_attn_bwd_dq(const AttnArgs &a, hipStream_t s) {
-  const int64_t grid = (int64_t)a.BH * a.nbq;
-  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  launch_kernel(attn_bwd_dq_kernel, dim3((unsigned)grid), dim3(256), s, a);
-  return hipGetLastError();
+hipError_t launch_attn_fwd(const AttnArgs &a, int part, hipStream_t s) {
+  return attn_launch(attn_fwd_kernel<1>, attn_fwd_kernel<4>, 4, a, part, s);
 }
 
-hipError_t launch_attn_bwd_dkv(const AttnArgs &a, hipStream_t s) {
-  const int64_t grid = (int64_t)a.BH * a.nbq;
-  if (grid <= 0 || grid > 0x7fffffff) return hipErrorInvalidValue;
-  launch_kernel(attn_bwd_dkv_kernel, dim3((unsigned)grid), dim3(256), s, a);
-  return hipGetLastError();
+hipError_t launch_attn_bwd_dq(const AttnArgs &a, int part, hipStream_t s) {
+  return attn_launch(attn_bwd_dq_kernel<1>, attn_bwd_dq_kernel<4>, 4, a, part, s);
+}
+
+hipError_t launch_attn_bwd_dkv(const AttnArgs &a, int part, hipStream_t s) {
+  return attn_launch(attn_bwd_dkv_kernel<1>, attn_bwd_dkv_kernel<2>, 2, a, part, s);
 }
 
 }  // namespace pf

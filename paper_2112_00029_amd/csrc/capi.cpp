@@ -1020,8 +1020,18 @@ pf_status pf_attn_fwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
   a.nlong = L->global_blocks;
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
-  Timed t(PF_KERNEL_ATTN_FWD, (hipStream_t)stream);
-  return hip_status(pf::launch_attn_fwd(a, (hipStream_t)stream), "attention forward kernel");
+  hipStream_t s = (hipStream_t)stream;
+  if (a.nlong > 0) {
+    {
+      Timed t(PF_KERNEL_ATTN_FWD, s);
+      if ((st = hip_status(pf::launch_attn_fwd(a, 1, s), "attention forward kernel")) != PF_OK) return st;
+    }
+    if (a.nlong == a.nbq) return PF_OK;
+    Timed t(PF_KERNEL_ATTN_FWD, s);
+    return hip_status(pf::launch_attn_fwd(a, 2, s), "attention forward kernel");
+  }
+  Timed t(PF_KERNEL_ATTN_FWD, s);
+  return hip_status(pf::launch_attn_fwd(a, 0, s), "attention forward kernel");
 }
 
 size_t pf_attn_workspace_bytes(int32_t B, int32_t H, int32_t Sq) {
@@ -1054,12 +1064,21 @@ pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
   hipStream_t s = (hipStream_t)stream;
-  {
+  // Parts: 0 (all rows) without global stripes, else 1 (the stripes'
+  // long rows / columns, grouped kernels) then 2 (the rest).
+  const int parts[2] = {a.nlong > 0 ? 1 : 0, 2};
+  const int nparts = a.nlong > 0 && a.nlong < a.nbq ? 2 : 1;
+  for (int i = 0; i < nparts; ++i) {
     Timed t(PF_KERNEL_ATTN_BWD_DQ, s);
-    if ((st = hip_status(pf::launch_attn_bwd_dq(a, s), "attention dQ kernel")) != PF_OK) return st;
+    if ((st = hip_status(pf::launch_attn_bwd_dq(a, parts[i], s), "attention dQ kernel")) != PF_OK)
+      return st;
   }
-  Timed t(PF_KERNEL_ATTN_BWD_DKV, s);
-  return hip_status(pf::launch_attn_bwd_dkv(a, s), "attention dK/dV kernel");
+  for (int i = 0; i < nparts; ++i) {
+    Timed t(PF_KERNEL_ATTN_BWD_DKV, s);
+    if ((st = hip_status(pf::launch_attn_bwd_dkv(a, parts[i], s), "attention dK/dV kernel")) != PF_OK)
+      return st;
+  }
+  return PF_OK;
 }
 
 size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K) {

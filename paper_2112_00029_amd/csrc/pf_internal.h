@@ -150,6 +150,7 @@ struct AttnArgs {
   float *delta;
   int BH, S, nbq;
   int nlong;            // leading block rows / columns kept whole (global stripes)
+  int first;            // logical id of the launch's first workgroup (set by the launcher)
   float scale;
   const int32_t *row_ptr, *col_idx, *col_ptr, *row_idx;
 };
@@ -183,8 +184,11 @@ hipError_t launch_mix_dgamma(int dtype, const void *S, const void *T_lr, int64_t
                              hipStream_t s);
 hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
                            const void *Hpre, void *out, hipStream_t s);
-hipError_t launch_attn_fwd(const AttnArgs &a, hipStream_t s);
-hipError_t launch_attn_bwd_dq(const AttnArgs &a, hipStream_t s);
-hipError_t launch_attn_bwd_dkv(const AttnArgs &a, hipStream_t s);
+// Attention launches: part 0 covers every block row (column); with global
+// stripes, part 1 runs their nlong long rows (columns) on the grouped
+// kernels and part 2 the rest.
+hipError_t launch_attn_fwd(const AttnArgs &a, int part, hipStream_t s);
+hipError_t launch_attn_bwd_dq(const AttnArgs &a, int part, hipStream_t s);
+hipError_t launch_attn_bwd_dkv(const AttnArgs &a, int part, hipStream_t s);
 
 }  // namespace pf

@@ -86,3 +86,15 @@ def test_attention_global_workload_shape():
 
 def test_attention_global_wide_stripes_small_stride():
     _run(1, 2, 1024, 4, heads=[(0, 0), (0, 1)], g=3)
+
+
+def test_attention_global_every_row():
+    """Stripes as wide as the sequence: every block row is long (only the
+    grouped kernels run) and the mask is dense."""
+    _run(1, 2, 512, 8, heads=[(0, 0), (0, 1)], g=8)
+
+
+def test_attention_global_rows_shorter_than_groups():
+    """Two key blocks per row: two of the four groups of the forward / dQ
+    kernels own no block and must contribute nothing."""
+    _run(1, 2, 128, 2, heads=[(0, 0), (0, 1)], g=1)
