@@ -273,3 +273,35 @@ def test_factor_layout_errors():
     for args in [(1024, 32, 3), (1024, 32, 64), (1000, 32, 2), (1024, 32, 1)]:
         with pytest.raises(pf.PixelflyError):
             pf.pf_layout_create_factor(*args)
+
+
+def test_mixed_call_errors_before_any_launch():
+    """The mixing-weight calls check gamma and every argument before the
+    layout state (no HIP work happens for any of these)."""
+    L = pf.pf_layout_create(256, 256, 32, 4)
+    nan = float("nan")
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_linear_fwd_mixed(L, pf.PF_BF16, 128, 32, nan, A16, A16, A16, A16, A16, A16, stream=0)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_linear_fwd_mixed(L, pf.PF_BF16, 128, 32, 0.5, A16, A16, A16, A16, A16, A16, stream=0)
+    assert e.value.status == pf.PF_ERR_STATE
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_linear_bwd_data_mixed(L, pf.PF_BF16, 128, 32, float("inf"), A16, A16, A16, A16, A16,
+                                    A16, stream=0)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_linear_bwd_data_mixed(L, pf.PF_BF16, 128, 32, 0.5, A16, A16, A16, A16, None, A16,
+                                    stream=0)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG
+    args = [A16] * 8  # dY, X, Wblk, T_lr, S, dW, dU, dV
+    for dg, want in [(None, pf.PF_ERR_INVALID_ARG), (A16 + 2, pf.PF_ERR_INVALID_ARG),
+                     (A16, pf.PF_ERR_STATE)]:
+        with pytest.raises(pf.PixelflyError) as e:
+            pf.pf_linear_bwd_weight_mixed(L, pf.PF_BF16, 128, 32, 0.5, *args, dg, A16, 1 << 30,
+                                          stream=0)
+        assert e.value.status == want, dg
+    with pytest.raises(pf.PixelflyError) as e:  # Wblk is required (the dgamma term)
+        pf.pf_linear_bwd_weight_mixed(L, pf.PF_BF16, 128, 32, 0.5, A16, A16, None, A16, A16, A16,
+                                      A16, A16, A16, A16, 1 << 30, stream=0)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG

@@ -7,6 +7,7 @@ calls give the same dgamma bit for bit (fixed summation order)."""
 import numpy as np
 import pytest
 
+import synth
 from oracle import linear as ol
 from oracle import mask as om
 from tests._gpu_util import TOL, empty, rel_fro, to_dev, to_host, torch_cuda
@@ -79,3 +80,33 @@ def test_mixed_parity(n_out, n_in, b, ms, T, r, dtype, gamma, epi):
     eg = abs(g1 - g["dgamma"]) / terms
     print(f"  dgamma: got={g1:.6e} ref={g['dgamma']:.6e} rel={eg:.3e}", flush=True)
     assert eg <= tol
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_mixed_bwd_data_gelu_epilogue(dtype):
+    """Backward-data of the mixed layer with the GELU-derivative epilogue:
+    dX = (dY (gamma B) + (1 - gamma) (dY U) V) * gelu'(aux), the form the
+    second layer of an MLP hands back through the activation."""
+    torch = torch_cuda()
+    from paper_2112_00029_amd import pixelfly as pf
+    n_out, n_in, b, ms, T, r, gamma = 768, 3072, 32, 16, 700, 96, 0.35
+    print(f"[mixed-gelu] {n_out}x{n_in} b={b} T={T} r={r} {dtype} gamma={gamma}", flush=True)
+    std = (1.0, 1.0 / np.sqrt(6 * 32), 1.0 / 32, 1.0) if dtype == "fp32" else (0.02,) * 4
+    inp = _inputs(n_out, n_in, b, ms, T, r, dtype, std=std)
+    aux, aux_raw = synth.draw((T, n_in), 1.0, 0, 9, dtype)  # pre-activation, ~N(0, 1)
+    L = pf.pf_layout_create(n_out, n_in, b, ms)
+    pf.pf_layout_upload(L)
+    d = {k: to_dev(v) for k, v in inp["raw"].items()}
+    a_dev = to_dev(aux_raw)
+    S, dX = empty((T, r), dtype), empty((T, n_in), dtype)
+    wsb = pf.pf_workspace_bytes(L, T, r, dtype)
+    ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device="cuda")
+    pf.pf_linear_bwd_data_mixed(L, dtype, T, r, gamma, d["dY"], d["W"], d["U"], d["V"], S, dX,
+                                pf.PF_EPI_GELU, a_dev, ws, wsb)
+    torch.cuda.synchronize()
+    g = ol.backward_mixed(inp["X"], inp["Wd"], inp["Mel"], inp["dY"], inp["U"], inp["V"], gamma)
+    tol = TOL[dtype]
+    for k, got, ref in [("S", to_host(S), g["S"]), ("dX", to_host(dX), g["dX"] * ol.gelu_grad(aux))]:
+        e = rel_fro(got, ref)
+        print(f"  {k}: rel_fro={e:.3e}", flush=True)
+        assert e <= tol, (k, e)
