@@ -275,7 +275,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
                    uint32_t &colb) __attribute__((always_inline)) {
     const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
     const bool sp = c < nsteps;
-    const int kcol = DENSE ? c : ld_meta(&a.kcols[kcol_off + min(c, nsteps - 1)]);
+    const int kcol = DENSE ? c : ld_meta(&a.kcols[kcol_off + max(min(c, nsteps - 1), 0)]);
     base = sp ? a_base : l_base;
     bytes = sp ? a_bytes : (c < vblocks ? l_bytes : 0);
     ldb = (uint32_t)((sp ? a.lda : a.ldl) * 2);
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       bytes = c < nsteps ? BIG : 0;
     } else {
       const bool sp = c < nsteps;
-      const int64_t blk = ld_meta(&a.blks[blk_off + min(c, nsteps - 1) * G + g]);
+      const int64_t blk = ld_meta(&a.blks[blk_off + max(min(c, nsteps - 1), 0) * G + g]);
       const int cr = c - nsteps;
       const bf16_t *sp_base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
       const bf16_t *lr_base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK

@@ -156,26 +156,41 @@ struct Stage8 {
 // Register stage 0 carries even steps, stage 1 odd steps; step s lives in
 // LDS buffer s % 2.  The loads of step s+2 are in flight while step s is
 // computed.
+//
+// Loads are issued for up to two steps past the end (load must accept any
+// s < total + 2: its reads stay inside the operands or read zeros); only
+// compute stops at total.  With no branch around a load, the
+// wait before each store covers just the older register stage: a branch
+// there makes the compiler wait for every outstanding load at the top of
+// the loop, the younger stage included, and each step then pays a whole
+// memory round trip.
 template <typename Load, typename Store, typename Compute>
 __device__ __forceinline__ void pipeline(int total, Stage8 &ra0, Stage8 &rb0, Stage8 &ra1,
                                          Stage8 &rb1, Load &&load, Store &&store,
                                          Compute &&compute) {
   if (total <= 0) return;
+  // Every entry to the loop body (first or repeated) has the same two
+  // register stages in flight, the older one first; the loop runs whole
+  // pairs of steps and an odd last step follows it, so no path leaves the
+  // body early.
   load(0, ra0, rb0);
-  if (total > 1) load(1, ra1, rb1);
-  store(ra0, rb0, 0);
-  __syncthreads();
-  for (int s = 0; s < total; s += 2) {
-    if (s + 2 < total) load(s + 2, ra0, rb0);
-    compute(0, s);
-    if (s + 1 < total) store(ra1, rb1, 1);
+  load(1, ra1, rb1);
+  const int pairs = total >> 1;
+  for (int p = 0; p < pairs; ++p) {
+    const int s = 2 * p;
+    store(ra0, rb0, 0);
     __syncthreads();
-    if (s + 1 < total) {
-      if (s + 3 < total) load(s + 3, ra1, rb1);
-      compute(1, s + 1);
-      if (s + 2 < total) store(ra0, rb0, 0);
-      __syncthreads();
-    }
+    load(s + 2, ra0, rb0);
+    compute(0, s);
+    store(ra1, rb1, 1);
+    __syncthreads();
+    load(s + 3, ra1, rb1);
+    compute(1, s + 1);
+  }
+  if (total & 1) {
+    store(ra0, rb0, 0);
+    __syncthreads();
+    compute(0, total - 1);
   }
 }
 
@@ -293,7 +308,7 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
                    uint32_t &colb) __attribute__((always_inline)) {
     const int k0 = (s_begin + s) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
     const bool sp = c < nsteps;
-    const int kcol = DENSE ? c : a.kcols[kcol_off + min(c, nsteps - 1)];
+    const int kcol = DENSE ? c : a.kcols[kcol_off + max(min(c, nsteps - 1), 0)];
     base = sp ? a_base : l_base;
     bytes = sp ? a_bytes : (c < vblocks ? l_bytes : 0);
     ldb = (uint32_t)((sp ? a.lda : a.ldl) * ES);
@@ -311,7 +326,7 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
       bytes = c < nsteps ? BIG : 0;
     } else {
       const bool sp = c < nsteps;
-      const int64_t blk = a.blks[blk_off + min(c, nsteps - 1) * G + g];
+      const int64_t blk = a.blks[blk_off + max(min(c, nsteps - 1), 0) * G + g];
       const int cr = c - nsteps;
       const T *sp_base = B + blk * (BLK * BLK) + (BKN ? kk * BLK : kk);
       const T *lr_base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK

@@ -106,6 +106,11 @@ static void build_nt_tiles(const std::vector<int32_t> &ptr,
       tiles.push_back(t);
     }
   }
+  // One step of padding: kernels read the tables at step max(min(c, nsteps
+  // - 1), 0), so a tile without kept blocks (an empty block column on the
+  // backward-data side) still reads inside them.
+  kcols.push_back(0);
+  for (int g = 0; g < G; ++g) blks.push_back(0);
 }
 
 static int32_t csr_pos(const pf_layout &L, int i, int j) {

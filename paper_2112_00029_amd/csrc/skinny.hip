@@ -15,12 +15,13 @@
 //
 // Operands reach the MFMA straight from global memory where they can: the
 // contraction does not care in which order k is visited as long as both
-// operands agree, so lane l takes the 32 consecutive k values
-// (l / 32) * 32 .. + 31 of a step as four 16-byte loads, and 16-wide slice c
-// of the MFMA uses the 8 values c * 8 .. + 7 of that run on both sides.  That
-// serves A and a [n][k] B directly.  A [k][n] B (U) is staged per wave in a
-// private 64 x 64 LDS tile and read back with the gfx950 transpose read,
-// which hands each lane 4 consecutive k of one column.
+// operands agree, so 16-wide slice c of the MFMA takes k = c * 16 + (l / 32)
+// * 8 .. + 7 of the step in lane l, one 16-byte load.  The two lane halves
+// then read 32 adjacent bytes of a row per load, which halves the L1
+// requests of a lane-per-row load against giving each half its own 32-k
+// run.  That serves A and a [n][k] B directly.  A [k][n] B (U) is staged per
+// wave in a private 64 x 64 LDS tile and read back with the gfx950
+// transpose read, which hands each lane 4 consecutive k of one column.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -90,10 +91,10 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a) {
   const int ksteps = (a.K + SK_BK - 1) / SK_BK;
   const int h = lane >> 5, r32 = lane & 31;
 
-  // A: rows past M read as zero (range); a k run past K is pointed out of
+  // A: rows past M read as zero (range); a k slice past K is pointed out of
   // range.  Step s adds s * 128 bytes through the scalar offset.
   const rsrc_t rA = make_rsrc((const bf16_t *)a.A + t0 * a.lda, (a.M - t0) * a.lda * 2);
-  const uint32_t voffA = (uint32_t)(r32 * a.lda * 2 + h * 64);
+  const uint32_t voffA = (uint32_t)(r32 * a.lda * 2 + h * 16);
   const uint32_t OUT = 0x7ffffff0u;
   rsrc_t rB;
   uint32_t voffB[8];
@@ -101,7 +102,7 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a) {
     // V rows n0 .. n0 + 63 (rows past r read as zero).
     rB = make_rsrc((const bf16_t *)a.B + (int64_t)n0 * a.ldb, (int64_t)(a.ncols - n0) * a.ldb * 2);
 #pragma unroll
-    for (int j = 0; j < SK_NT; ++j) voffB[j] = (uint32_t)((j * 32 + r32) * a.ldb * 2 + h * 64);
+    for (int j = 0; j < SK_NT; ++j) voffB[j] = (uint32_t)((j * 32 + r32) * a.ldb * 2 + h * 16);
   } else {
     // U rows (k) of the step, columns n0 .. n0 + 63: chunk q = lane + 64 i is
     // row q / 8, 8 columns at (q % 8) * 8; columns past r are pointed out of
@@ -114,17 +115,26 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a) {
     }
   }
 
+  // Steps past the end (s * SK_BK >= K) read zeros: A and [n][k] B are
+  // pointed out of range, [k][n] B rows fall outside the buffer.  The step's
+  // byte offset goes through the scalar offset; readfirstlane makes it a
+  // scalar (else each load is wrapped in a per-lane loop).
   auto load = [&](int s, SkStage &st) __attribute__((always_inline)) {
-    const bool kin = s * SK_BK + h * 32 < a.K;
-    const uint32_t va = kin ? voffA : OUT;
+    const uint32_t soff = (uint32_t)__builtin_amdgcn_readfirstlane(s * 128);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) st.a[c] = bload(rA, va + c * 16, (uint32_t)s * 128);
+    for (int c = 0; c < 4; ++c) {
+      // K is a multiple of 32, so a 16-k slice is wholly inside or outside.
+      const bool kin = s * SK_BK + c * 16 < a.K;
+      st.a[c] = bload(rA, kin ? voffA + c * 32 : OUT, soff);
+    }
     if constexpr (!BKN) {
 #pragma unroll
       for (int j = 0; j < SK_NT; ++j)
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          st.b[j * 4 + c] = bload(rB, kin ? voffB[j] + c * 16 : OUT, (uint32_t)s * 128);
+        for (int c = 0; c < 4; ++c) {
+          const bool kin = s * SK_BK + c * 16 < a.K;
+          st.b[j * 4 + c] = bload(rB, kin ? voffB[j] + c * 32 : OUT, soff);
+        }
     } else {
       // The step's row offset goes into the per-lane offset, which the
       // buffer range check covers, so rows past K read as zero.
@@ -162,10 +172,10 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a) {
         } else {
           // Transpose read: within each 16-lane group, lanes 4m..4m+3 address
           // k row m and lane i receives column (group base + i); rows
-          // h*32 + c*8 + 0..3, then + 4..7, match the k run of A's slice c.
+          // c*16 + h*8 + 0..3, then + 4..7, match the k of A's slice c.
           const int g16 = lane >> 4, i = lane & 15;
           const int n = j * 32 + (g16 & 1) * 16 + (i & 3) * 4;
-          const int k = (g16 >> 1) * 32 + c * 8 + (i >> 2);
+          const int k = c * 16 + (g16 >> 1) * 8 + (i >> 2);
           typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
           const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tile + sk_lds_off(k, n)));
           const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(tile + sk_lds_off(k + 4, n)));
@@ -181,20 +191,22 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a) {
 
   // Three register stages: this wave's next two steps are in flight while
   // the current one is computed (the chain of a wave is up to K / (64 NW)
-  // steps long, each a memory round trip if not overlapped).
+  // steps long, each a memory round trip if not overlapped).  The loop body
+  // has no branches around its loads, so the wait before each compute
+  // leaves the two younger stages in flight; the step count is rounded up
+  // to whole rounds of three, the extra steps reading zeros.
   SkStage s0, s1, s2;
   const int n = ksteps > w ? (ksteps - w + NW - 1) / NW : 0;  // this wave's steps
+  const int n3 = (n + 2) / 3 * 3;
   auto step_of = [&](int i) { return w + i * NW; };
-  if (n > 0) load(step_of(0), s0);
-  if (n > 1) load(step_of(1), s1);
-  for (int i = 0; i < n; i += 3) {
-    if (i + 2 < n) load(step_of(i + 2), s2);
+  load(step_of(0), s0);
+  load(step_of(1), s1);
+  for (int i = 0; i < n3; i += 3) {
+    load(step_of(i + 2), s2);
     compute(s0);
-    if (i + 1 >= n) break;
-    if (i + 3 < n) load(step_of(i + 3), s0);
+    load(step_of(i + 3), s0);
     compute(s1);
-    if (i + 2 >= n) break;
-    if (i + 4 < n) load(step_of(i + 4), s1);
+    load(step_of(i + 4), s1);
     compute(s2);
   }
 
@@ -235,7 +247,10 @@ hipError_t launch_skinny(bool b_kn, const SkinnyArgs &a, hipStream_t s) {
   if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
   // Eight waves once each of four would have 16 or more steps (measured:
   // at 48 steps four waves were faster than eight).
-  const bool wide = (a.K + SK_BK - 1) / SK_BK >= 64;
+#ifndef PF_SKINNY_WIDE_STEPS
+#define PF_SKINNY_WIDE_STEPS 64
+#endif
+  const bool wide = (a.K + SK_BK - 1) / SK_BK >= PF_SKINNY_WIDE_STEPS;
   if (b_kn) {
     if (wide) launch_kernel(skinny_kernel<true, 8>, dim3((unsigned)tiles), dim3(512), s, a);
     else launch_kernel(skinny_kernel<true, 4>, dim3((unsigned)tiles), dim3(256), s, a);

@@ -48,3 +48,53 @@ def test_cover_layout_parity(n, p, d, T):
         e = rel_fro(got[k], ref[k])
         print(f"  {k}: rel_fro={e:.3e}  cover density {C.mean():.4f}", flush=True)
         assert e <= TOL["bf16"], (k, e)
+
+
+@pytest.mark.parametrize("b,T,r", [(32, 300, 32), (64, 520, 64)])
+def test_empty_block_columns_with_lowrank(b, T, r):
+    """Block masks whose first, an inner and the last block column keep no
+    block: the backward-data tiles of those columns have no kept step and
+    carry only the low-rank term (dX columns = (dY U) V there)."""
+    torch = torch_cuda()
+    from paper_2112_00029_amd import pixelfly as pf
+    nb = 24
+    n = nb * b
+    print(f"[empty-cols] n={n} b={b} T={T} r={r}", flush=True)
+    rng = np.random.default_rng([2112, b])
+    Mb = rng.random((nb, nb)) < 0.2
+    Mb[:, [0, 9, nb - 1]] = False
+    Mb[np.arange(nb), rng.choice([j for j in range(nb) if j not in (0, 9, nb - 1)], nb)] = True
+    assert not Mb[:, 0].any() and not Mb[:, nb - 1].any() and Mb.any(axis=1).all()
+    row_ptr, col_idx, *_r = om.block_csr(Mb)
+    nnzb = int(Mb.sum())
+    X, Xr = synth.draw((T, n), 0.02, 3, 1, "bf16")
+    W, Wr = synth.draw((nnzb, b, b), 0.02, 3, 2, "bf16")
+    U, Ur = synth.draw((n, r), 0.02, 3, 3, "bf16")
+    V, Vr = synth.draw((r, n), 0.02, 3, 4, "bf16")
+    dY, dYr = synth.draw((T, n), 0.02, 3, 5, "bf16")
+    Wd = ol.unpack(W, row_ptr, col_idx, nb, nb, b)
+    L = pf.pf_layout_create_from_mask(nb, nb, b, Mb.astype(np.uint8))
+    pf.pf_layout_upload(L)
+    x, w, u, v, dy = (to_dev(a) for a in (Xr, Wr, Ur, Vr, dYr))
+    Y, Tl, S, dX = empty((T, n), "bf16"), empty((T, r), "bf16"), empty((T, r), "bf16"), empty((T, n), "bf16")
+    dW, dU, dV = empty((nnzb, b, b), "bf16"), empty((n, r), "bf16"), empty((r, n), "bf16")
+    wsb = pf.pf_workspace_bytes(L, T, r, "bf16")
+    ws = torch.empty(max(wsb, 256), dtype=torch.uint8, device="cuda")
+    pf.pf_linear_fwd(L, "bf16", T, r, x, w, u, v, Y, Tl, workspace=ws, ws_bytes=wsb)
+    pf.pf_linear_bwd_data(L, "bf16", T, r, dy, w, u, v, S, dX, workspace=ws, ws_bytes=wsb)
+    pf.pf_linear_bwd_weight(L, "bf16", T, r, dy, x, Tl, S, dW, dU, dV, ws, wsb)
+    torch.cuda.synchronize()
+    Yref, Tref = ol.forward(X, Wd, U, V)
+    g = ol.backward(X, Wd, om.element_mask(Mb, b), dY, U, V)
+    ref = {"Y": Yref, "T_lr": Tref, "S": g["S"], "dX": g["dX"],
+           "dW": ol.pack(g["dW"], row_ptr, col_idx, nb, b), "dU": g["dU"], "dV": g["dV"]}
+    got = {"Y": to_host(Y), "T_lr": to_host(Tl), "S": to_host(S), "dX": to_host(dX),
+           "dW": to_host(dW), "dU": to_host(dU), "dV": to_host(dV)}
+    for k in ref:
+        e = rel_fro(got[k], ref[k])
+        print(f"  {k}: rel_fro={e:.3e}", flush=True)
+        assert e <= TOL["bf16"], (k, e)
+    # the empty columns of dX hold only the low-rank term
+    cols = np.r_[0:b, (nb - 1) * b:n]
+    e = rel_fro(got["dX"][:, cols], (g["S"] @ V)[:, cols])
+    assert e <= TOL["bf16"], ("dX empty columns", e)
