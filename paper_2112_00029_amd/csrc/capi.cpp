@@ -876,6 +876,71 @@ pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const voi
                     "backward-data kernel");
 }
 
+// Launch order of the weight-gradient items.  Workgroups reach the eight
+// XCDs in contiguous runs of launch positions, each XCD with its own L2, and
+// the dU items read whole dY column blocks that kept-block items read too:
+// placed apart, the same dY rows are fetched into two L2s.  So the dV items
+// (S and X only) go first, then, for each group of dY block columns linked
+// by a shared item (union-find over block rows of W), the group's kept-block
+// items followed by its dU items.  Without the low-rank regions, or with
+// more items than the order holds, the natural order stays.
+void set_tn_order(pf::TNArgs &a, const pf_layout *L) {
+  a.n_order = 0;
+  if (a.n_dense < 2) return;
+  const int GT = 128 / L->b;
+  const pf::TNDense &d0 = a.dr[0], &d1 = a.dr[1];
+  const int nsp = a.n_items;
+  const int nbg0 = (d0.nb_blk + GT - 1) / GT, n0 = ((d0.na_blk + GT - 1) / GT) * nbg0;
+  const int n1 = ((d1.na_blk + GT - 1) / GT) * ((d1.nb_blk + GT - 1) / GT);
+  const int total = nsp + n0 + n1;
+  if (total > pf::kTNOrderMax || total <= 0) return;
+  std::vector<int> parent(L->nb_out);
+  for (int i = 0; i < L->nb_out; ++i) parent[i] = i;
+  auto find = [&](int x) {
+    while (parent[x] != x) x = parent[x] = parent[parent[x]];
+    return x;
+  };
+  auto unite = [&](int x, int y) { parent[find(x)] = find(y); };
+  auto du_rows = [&](int q, int &r0, int &r1) {
+    r0 = (q / nbg0) * GT;
+    r1 = std::min(r0 + GT, d0.na_blk);
+  };
+  for (int i = 0; i < nsp; ++i) {
+    const pf::TNItem &it = L->tn_items[i];
+    for (int g = 1; g < it.na; ++g) unite(it.a_col[g], it.a_col[0]);
+  }
+  for (int q = 0; q < n0; ++q) {
+    int r0, r1;
+    du_rows(q, r0, r1);
+    for (int rr = r0 + 1; rr < r1; ++rr) unite(rr, r0);
+  }
+  // Buckets per group root, in order of first appearance.
+  std::vector<std::vector<int>> sp_of(L->nb_out), du_of(L->nb_out);
+  std::vector<int> roots;
+  auto note = [&](int root) {
+    if (sp_of[root].empty() && du_of[root].empty()) roots.push_back(root);
+  };
+  for (int i = 0; i < nsp; ++i) {
+    const int root = find(L->tn_items[i].a_col[0]);
+    note(root);
+    sp_of[root].push_back(i);
+  }
+  for (int q = 0; q < n0; ++q) {
+    int r0, r1;
+    du_rows(q, r0, r1);
+    const int root = find(r0);
+    note(root);
+    du_of[root].push_back(nsp + q);
+  }
+  int k = 0;
+  for (int q = 0; q < n1; ++q) a.order[k++] = (uint16_t)(nsp + n0 + q);
+  for (int root : roots) {
+    for (int i : sp_of[root]) a.order[k++] = (uint16_t)i;
+    for (int i : du_of[root]) a.order[k++] = (uint16_t)i;
+  }
+  if (k == total) a.n_order = total;
+}
+
 // Weight-gradient work list and its token split.
 pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *dY,
                    const void *X, const void *T_lr, const void *S, void *dWblk, void *dU,
@@ -886,6 +951,7 @@ pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, con
   a.Wout = dWblk;
   a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
+  set_tn_order(a, L);
   a.T = T;
   a.scale_w = a.scale_lr = 1.f;
   *plan = tn_plan(pf::tn_items_total(a, L->b), T,

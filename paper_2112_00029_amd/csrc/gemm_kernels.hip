@@ -150,29 +150,73 @@ struct Stage8 {
   }
 };
 
-// Double-buffered pipeline driver: load(s, ra, rb) issues the global loads
-// of step s into a register stage, store(ra, rb, buf) writes a register stage
-// to LDS buffer buf, compute(buf, s) runs the MFMAs of step s held in buf.
-// Register stage 0 carries even steps, stage 1 odd steps; step s lives in
-// LDS buffer s % 2.  The loads of step s+2 are in flight while step s is
-// computed.
+// Pipeline driver: load(s, ra, rb) issues the global loads of step s into a
+// register stage, store(ra, rb, buf) writes a register stage to LDS buffer
+// buf, compute(buf, s) runs the MFMAs of step s held in buf.  Four register
+// stages rotate over the steps and two LDS buffers alternate; the loads of
+// step s+3 are issued right after step s is stored, so three steps' loads
+// are in flight while one is computed (a step is a few hundred MFMA cycles,
+// well short of a loaded HBM round trip).  One barrier per step suffices:
+// buffer s % 2 is rewritten at step s only after every wave has passed the
+// barrier of step s-1, i.e. finished computing step s-2.
 //
-// Loads are issued for up to two steps past the end (load must accept any
-// s < total + 2: its reads stay inside the operands or read zeros); only
-// compute stops at total.  With no branch around a load, the
-// wait before each store covers just the older register stage: a branch
-// there makes the compiler wait for every outstanding load at the top of
-// the loop, the younger stage included, and each step then pays a whole
-// memory round trip.
+// Loads are issued for up to three steps past the end (load must accept any
+// s < total + 3: its reads stay inside the operands or read zeros); only
+// compute stops at total.  The loop runs whole groups of four steps with no
+// branch around a load, so every entry to its body has the same three
+// stages in flight, oldest first, and the wait before each store leaves the
+// two younger ones outstanding; up to three remaining steps follow it.
 template <typename Load, typename Store, typename Compute>
-__device__ __forceinline__ void pipeline(int total, Stage8 &ra0, Stage8 &rb0, Stage8 &ra1,
-                                         Stage8 &rb1, Load &&load, Store &&store,
-                                         Compute &&compute) {
+__device__ __forceinline__ void pipeline4(int total, Stage8 &ra0, Stage8 &rb0, Stage8 &ra1,
+                                          Stage8 &rb1, Stage8 &ra2, Stage8 &rb2, Stage8 &ra3,
+                                          Stage8 &rb3, Load &&load, Store &&store,
+                                          Compute &&compute) {
   if (total <= 0) return;
-  // Every entry to the loop body (first or repeated) has the same two
-  // register stages in flight, the older one first; the loop runs whole
-  // pairs of steps and an odd last step follows it, so no path leaves the
-  // body early.
+  load(0, ra0, rb0);
+  load(1, ra1, rb1);
+  load(2, ra2, rb2);
+  auto step = [&](int s, Stage8 &ra, Stage8 &rb, Stage8 &na, Stage8 &nb,
+                  int buf) __attribute__((always_inline)) {
+    store(ra, rb, buf);
+    __syncthreads();
+    load(s + 3, na, nb);
+    compute(buf, s);
+  };
+  const int quads = total >> 2;
+  for (int p = 0; p < quads; ++p) {
+    const int s = 4 * p;
+    step(s, ra0, rb0, ra3, rb3, 0);
+    step(s + 1, ra1, rb1, ra0, rb0, 1);
+    step(s + 2, ra2, rb2, ra1, rb1, 0);
+    step(s + 3, ra3, rb3, ra2, rb2, 1);
+  }
+  const int rem = total & 3, s = 4 * quads;
+  if (rem > 0) {
+    store(ra0, rb0, 0);
+    __syncthreads();
+    compute(0, s);
+  }
+  if (rem > 1) {
+    store(ra1, rb1, 1);
+    __syncthreads();
+    compute(1, s + 1);
+  }
+  if (rem > 2) {
+    store(ra2, rb2, 0);
+    __syncthreads();
+    compute(0, s + 2);
+  }
+}
+
+// The same with two register stages (loads one step ahead), for the fp32
+// kernels, whose fragments leave no room for four stages: loads may run
+// two steps past the end; whole pairs of steps in the loop, an odd last
+// step after it.
+template <typename Load, typename Store, typename Compute>
+__device__ __forceinline__ void pipeline2(int total, Stage8 &ra0, Stage8 &rb0, Stage8 &ra1,
+                                          Stage8 &rb1, Load &&load, Store &&store,
+                                          Compute &&compute) {
+  if (total <= 0) return;
   load(0, ra0, rb0);
   load(1, ra1, rb1);
   const int pairs = total >> 1;
@@ -449,8 +493,9 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
     }
   };
 
-  Stage8 ra0, rb0, ra1, rb1;
-  pipeline(total, ra0, rb0, ra1, rb1, load, store, compute);
+  Stage8 ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3;
+  if constexpr (BF) pipeline4(total, ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3, load, store, compute);
+  else pipeline2(total, ra0, rb0, ra1, rb1, load, store, compute);
 
   // Epilogue.  The accumulators (lane: column lane % 32, rows (j/4)*8 +
   // (lane/32)*4 + j%4 of each 32 x 32 tile) go to an fp32 tile in LDS, then
@@ -647,7 +692,10 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
   const int wm = wave >> 1, wn = wave & 1;
   const int items_total = tn_items_total_dev(a, GT);
   const int bid = xcd_remap(blockIdx.x, gridDim.x);
-  const int split = bid / items_total, item = bid % items_total;
+  const int split = bid / items_total, pos = bid % items_total;
+  // The launch order comes straight from the kernel arguments (a_arg): the
+  // local copy keeps the scalar fields only.
+  const int item = a.n_order > 0 ? (int)a_arg.order[pos] : pos;
 
   TNItemView<T, BLK> v;
   v.decode(a, item);
@@ -745,8 +793,9 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
     }
   };
 
-  Stage8 ra0, rb0, ra1, rb1;
-  pipeline(nsteps, ra0, rb0, ra1, rb1, load, store, compute);
+  Stage8 ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3;
+  if constexpr (BF) pipeline4(nsteps, ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3, load, store, compute);
+  else pipeline2(nsteps, ra0, rb0, ra1, rb1, load, store, compute);
 
   if (a.nsplit > 1) {
     float *part = a.partials + ((int64_t)item * a.nsplit + split) * (TILE * TILE);

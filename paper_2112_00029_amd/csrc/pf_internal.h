@@ -32,6 +32,8 @@ inline void launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, Args..
 // (weight-gradient) tile.
 constexpr int kMaxG = 8;
 constexpr int kTNMax = 4;
+// Longest weight-gradient launch order carried in the kernel arguments.
+constexpr int kTNOrderMax = 768;
 
 // One output column-tile of the block-sparse "NT" GEMM
 //   C[:, out_blk[g]] = sum_c A[:, kcol(c)] . Bblk(g, c)^T  (+ low-rank)
@@ -127,6 +129,10 @@ struct TNArgs {
   float scale_w, scale_lr;
   const void *wdot;
   float *wdot_out;
+  // Launch order: launch position i (within a split) runs item order[i]
+  // when n_order > 0, item i otherwise.
+  int n_order;
+  uint16_t order[kTNOrderMax];
 };
 
 // Rank-r product C[M x ncols] = A[M x K] . op(B) (bf16, skinny.hip):
