@@ -190,15 +190,13 @@ pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int
 // With more tiles the tile kernel re-reads the small operand far less and
 // measured faster (4096 tokens, r = 96: rank-r kernel; 8192 tokens,
 // r = 128: tiles).
+// Rank-r products go to the rank-r kernel while 128 x 128 tiles would cover
+// fewer than PF_SKINNY_MAX_TILES of them (a quarter of the CUs).
 #ifndef PF_SKINNY_MAX_TILES
 #define PF_SKINNY_MAX_TILES 64
 #endif
-#ifndef PF_SKINNY_MAX_K
-#define PF_SKINNY_MAX_K (1 << 30)
-#endif
-bool use_skinny(int dtype, int64_t T, int r, int64_t K) {
-  return dtype == 0 && r > 0 && ((T + 127) / 128) * ((r + 127) / 128) < PF_SKINNY_MAX_TILES &&
-         K < PF_SKINNY_MAX_K;
+bool use_skinny(int dtype, int64_t T, int r) {
+  return dtype == 0 && r > 0 && ((T + 127) / 128) * ((r + 127) / 128) < PF_SKINNY_MAX_TILES;
 }
 
 // bf16 rank-r product C[M x r] = A[M x K] . op(B) on the rank-r kernel
@@ -235,7 +233,7 @@ struct SkinnyPlan {
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0};
-  if (r <= 0 || use_skinny(dtype, T, r, (int64_t)kblocks * blk)) return p;  // the rank-r kernel needs no split
+  if (r <= 0 || use_skinny(dtype, T, r)) return p;  // the rank-r kernel needs no split
   const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + 127) / 128;
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
   int64_t ns;
@@ -749,7 +747,7 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   const int dt = (int)dtype, b = L->b;
-  if (use_skinny(dt, T, r, L->n_in)) {
+  if (use_skinny(dt, T, r)) {
     st = skinny_bf16(PF_KERNEL_LOWRANK_T, false, T, X, L->n_in, V, L->n_in, (int)L->n_in, r, T_lr,
                      s, "T_lr kernel");
     if (st != PF_OK) return st;
@@ -843,7 +841,7 @@ pf_status check_bwd_weight_args(const pf_layout *L, pf_dtype dtype, int64_t T, i
 pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
                     const void *U, void *S, const SkinnyPlan &sp, float *ws, hipStream_t s) {
   if (r <= 0) return PF_OK;
-  if (use_skinny(dt, T, r, L->n_out))
+  if (use_skinny(dt, T, r))
     return skinny_bf16(PF_KERNEL_LOWRANK_S, true, T, dY, L->n_out, U, r, (int)L->n_out, r, S, s,
                        "S kernel");
   const int b = L->b;
