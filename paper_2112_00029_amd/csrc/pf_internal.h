@@ -33,7 +33,7 @@ inline void launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, Args..
 constexpr int kMaxG = 8;
 constexpr int kTNMax = 4;
 // Longest weight-gradient launch order carried in the kernel arguments.
-constexpr int kTNOrderMax = 768;
+constexpr int kTNOrderMax = 1280;
 
 // One output column-tile of the block-sparse "NT" GEMM
 //   C[:, out_blk[g]] = sum_c A[:, kcol(c)] . Bblk(g, c)^T  (+ low-rank)
