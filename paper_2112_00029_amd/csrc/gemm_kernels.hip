@@ -354,7 +354,8 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
     const bool sp = c < nsteps;
     const int kcol = DENSE ? c : a.kcols[kcol_off + max(min(c, nsteps - 1), 0)];
     base = sp ? a_base : l_base;
-    bytes = sp ? a_bytes : (c < vblocks ? l_bytes : 0);
+    // Steps past this split's range (the pipeline loads ahead) read zeros.
+    bytes = s >= total ? 0 : (sp ? a_bytes : (c < vblocks ? l_bytes : 0));
     ldb = (uint32_t)((sp ? a.lda : a.ldl) * ES);
     colb = (uint32_t)(((sp ? kcol : c - nsteps) * BLK + kk) * ES);
   };
@@ -367,7 +368,7 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
       ldb = (uint32_t)(a.ldb * ES);
       base = BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
                  : B + (ob * BLK) * a.ldb + (int64_t)c * BLK + kk;
-      bytes = c < nsteps ? BIG : 0;
+      bytes = (c < nsteps && s < total) ? BIG : 0;
     } else {
       const bool sp = c < nsteps;
       const int64_t blk = a.blks[blk_off + max(min(c, nsteps - 1), 0) * G + g];
@@ -376,7 +377,7 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
       const T *lr_base = BKN ? R + ((int64_t)cr * BLK + kk) * a.ldr + ob * BLK
                              : R + (ob * BLK) * a.ldr + (int64_t)cr * BLK + kk;
       base = sp ? sp_base : lr_base;
-      bytes = (sp || c < vblocks) ? BIG : 0;
+      bytes = ((sp || c < vblocks) && s < total) ? BIG : 0;
       ldb = (uint32_t)(sp ? BLK * ES : a.ldr * ES);
     }
   };
