@@ -767,10 +767,14 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
         static_for<TN>([&](auto tn) __attribute__((always_inline)) {
           bfg[tn] = frag_kmajor_swz((const bf16_t *)Bs, ks, wn * 64 + tn * 32, lane);
         });
+        // All four sub-tiles, live or not: a branch per MFMA splits the step
+        // into blocks the scheduler cannot overlap (the next slice's LDS reads
+        // then wait behind every MFMA), and MFMA time is not what bounds this
+        // kernel.  A dead sub-tile reads clamped, valid fragments and is
+        // never stored.
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-            if (live[tm][tn])
-              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
       });
