@@ -453,12 +453,17 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
       });
     }
   };
-  auto compute = [&](int buf, int s) __attribute__((always_inline)) {
+  // MIX: whether this instantiation checks for the mixing switch; the
+  // check is a branch per K slice, which keeps the scheduler from moving the
+  // next slice's LDS reads under the current MFMAs, so calls without the
+  // mixing weight run an instantiation without it.
+  auto compute_m = [&](int buf, int s, auto mix) __attribute__((always_inline)) {
+    constexpr bool MIX = decltype(mix)::value;
     const T *As = smem + buf * (A_ELEMS + B_ELEMS);
     const T *Bs = As + A_ELEMS;
     if constexpr (BF) {
       static_for<BK / 16>([&](auto ks) __attribute__((always_inline)) {
-        mix_switch((s_begin + s) * BK + ks * 16);
+        if constexpr (MIX) mix_switch((s_begin + s) * BK + ks * 16);
         bf16x8 af[TM], bfg[TN];
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           af[tm] = frag_rmajor((const bf16_t *)As, LDA_S, ks, wm * WTM + tm * 32, lane);
@@ -475,7 +480,7 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
       });
     } else {
       static_for<BK / 2>([&](auto ks) __attribute__((always_inline)) {
-        mix_switch((s_begin + s) * BK + ks * 2);
+        if constexpr (MIX) mix_switch((s_begin + s) * BK + ks * 2);
         float af[TM], bfg[TN];
         const int kq = ks * 2 + (lane >> 5);
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
@@ -495,8 +500,13 @@ __global__ __launch_bounds__(256, 2) void nt_kernel(NTArgs a_arg) {
   };
 
   Stage8 ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3;
-  if constexpr (BF) pipeline4(total, ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3, load, store, compute);
-  else pipeline2(total, ra0, rb0, ra1, rb1, load, store, compute);
+  auto run = [&](auto mix) __attribute__((always_inline)) {
+    auto compute = [&](int buf, int s) __attribute__((always_inline)) { compute_m(buf, s, mix); };
+    if constexpr (BF) pipeline4(total, ra0, rb0, ra1, rb1, ra2, rb2, ra3, rb3, load, store, compute);
+    else pipeline2(total, ra0, rb0, ra1, rb1, load, store, compute);
+  };
+  if (a.mix) run(std::true_type{});
+  else run(std::false_type{});
 
   // Epilogue.  The accumulators (lane: column lane % 32, rows (j/4)*8 +
   // (lane/32)*4 + j%4 of each 32 x 32 tile) go to an fp32 tile in LDS, then
