@@ -374,10 +374,12 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   // Mixing weight: scale the kept-block sums once, at the first low-rank
   // K-block (virtual K index nsteps * BLK).
   const int kswitch = nsteps * BLK;
-  auto compute = [&](const uint8_t *sb, int t) __attribute__((always_inline)) {
+  // The switch check is a branch per K slice; launches without the mixing
+  // weight run an instantiation without it (see the loop below).
+  auto compute_m = [&](const uint8_t *sb, int t, auto mix) __attribute__((always_inline)) {
     sfor<BK / 16>([&](auto ks) __attribute__((always_inline)) {
       constexpr int h = (ks * 16) / KW, kq = ks % (KW / 16);
-      if (a.mix && (s_begin + t) * BK + ks * 16 == kswitch) {
+      if (decltype(mix)::value && (s_begin + t) * BK + ks * 16 == kswitch) {
         sfor<TN>([&](auto tn) __attribute__((always_inline)) {
           sfor<TM>([&](auto tm) __attribute__((always_inline)) {
 #pragma unroll
@@ -409,32 +411,39 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   sfor<NS - 1>([&](auto j) __attribute__((always_inline)) {
     if (j < total) issue(j, stage(j));
   });
-  for (int t0 = 0; t0 < total; t0 += NS) {
-    bool done = false;
-    sfor<NS>([&](auto j) __attribute__((always_inline)) {
-      if (done) return;
-      const int t = t0 + j;
-      if (t >= total) {
-        done = true;
-        return;
-      }
-      // Copies of steps t+1 .. t+NS-2 that were issued may still be in
-      // flight; step t's must have landed.
-      const int ahead = min(NS - 2, total - 1 - t);
-      if constexpr (NS == 2) {
-        wait_vm<0>();
-      } else if constexpr (NS == 3) {
-        if (ahead >= 1) wait_vm<DPS>(); else wait_vm<0>();
-      } else {
-        if (ahead >= 2) wait_vm<2 * DPS>();
-        else if (ahead == 1) wait_vm<DPS>();
-        else wait_vm<0>();
-      }
-      barrier();
-      if (t + NS - 1 < total) issue(t + NS - 1, stage(std::integral_constant<int, (j + NS - 1) % NS>{}));
-      compute(stage(j), t);
-    });
-  }
+  auto run = [&](auto mix) __attribute__((always_inline)) {
+    auto compute = [&](const uint8_t *sb, int t) __attribute__((always_inline)) {
+      compute_m(sb, t, mix);
+    };
+    for (int t0 = 0; t0 < total; t0 += NS) {
+      bool done = false;
+      sfor<NS>([&](auto j) __attribute__((always_inline)) {
+        if (done) return;
+        const int t = t0 + j;
+        if (t >= total) {
+          done = true;
+          return;
+        }
+        // Copies of steps t+1 .. t+NS-2 that were issued may still be in
+        // flight; step t's must have landed.
+        const int ahead = min(NS - 2, total - 1 - t);
+        if constexpr (NS == 2) {
+          wait_vm<0>();
+        } else if constexpr (NS == 3) {
+          if (ahead >= 1) wait_vm<DPS>(); else wait_vm<0>();
+        } else {
+          if (ahead >= 2) wait_vm<2 * DPS>();
+          else if (ahead == 1) wait_vm<DPS>();
+          else wait_vm<0>();
+        }
+        barrier();
+        if (t + NS - 1 < total) issue(t + NS - 1, stage(std::integral_constant<int, (j + NS - 1) % NS>{}));
+        compute(stage(j), t);
+      });
+    }
+  };
+  if (a.mix) run(std::true_type{});
+  else run(std::false_type{});
 
   // Epilogue.  Lane l of accumulator (tn, tm) holds token row tm*32 + l%32
   // and, for q = 0..3, output columns tn*32 + q*8 + (l/32)*4 + 0..3.  Full
