@@ -800,8 +800,7 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
         });
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-            if (live[tm][tn])
-              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
+            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
       });
