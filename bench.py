@@ -47,7 +47,11 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=100)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="mlp_fc1_768x3072", choices=sorted(synth.WORKLOADS))
+    p.add_argument("--workload", default="linear_16384x4096_b128", choices=sorted(synth.WORKLOADS))
+    p.add_argument("--no-sweep", action="store_true",
+                   help="skip the block-size sweep that follows the 16384 x 4096 layer")
+    p.add_argument("--no-cold", action="store_true",
+                   help="skip the cold-cache pass (1 GiB written between steps)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true")
     p.add_argument("--no-kernel-timing", action="store_true",
@@ -103,13 +107,25 @@ def measured_traffic(workload, kernel):
 
 
 def dev_bf16(torch, raw):
-    return torch.from_numpy(raw.view(np.int16).copy()).cuda().view(torch.bfloat16)
+    return torch.from_numpy(raw.view(np.int16)).cuda().view(torch.bfloat16)
 
 
 def dev_any(torch, raw):
     if raw.dtype == np.uint16:
         return dev_bf16(torch, raw)
     return torch.from_numpy(raw).cuda()
+
+
+# Device copies of seeded inputs, shared by the workloads of one run (the
+# block-size sweep draws the same X, U, V, dY for every block size).
+_DEV_CACHE = {}
+
+
+def dev_draw(torch, shape, std, seed, stream, dtype):
+    key = (tuple(shape), float(std), seed, stream, dtype)
+    if key not in _DEV_CACHE:
+        _DEV_CACHE[key] = dev_any(torch, synth.draw(shape, std, seed, stream, dtype, values=False)[1])
+    return _DEV_CACHE[key]
 
 
 # ---------------------------------------------------------------------------
@@ -124,7 +140,7 @@ class Linear:
         self.L = pf.pf_layout_create(N, K, b, ms)
         pf.pf_layout_upload(self.L)
         self.nnzb = pf.pf_layout_info_get(self.L)["nnzb"]
-        dr = lambda shape, std, stream: dev_any(torch, synth.draw(shape, std, seed, stream, dt)[1])
+        dr = lambda shape, std, stream: dev_draw(torch, shape, std, seed, stream, dt)
         self.X = dr((T, K), wl.std_x, 1)
         self.W = dr((self.nnzb, b, b), wl.std_w, 2)
         self.U = dr((N, r), wl.std_uv, 3)
@@ -662,6 +678,30 @@ def _layer_work(T, K, N, r, w, e):
     }
 
 
+def cpu_meta():
+    """CPU model (from /proc/cpuinfo, as lscpu reports it) and the BLAS
+    library numpy runs the oracle on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = f"{i.get('internal_api')} {i.get('version')} ({i.get('threading_layer', '')})"
+                break
+    except Exception:
+        pass
+    return {"cpu_model": model, "blas": blas, "host_cpus": len(os.sched_getaffinity(0))}
+
+
 def blas_threads():
     try:
         from threadpoolctl import threadpool_info
@@ -686,36 +726,10 @@ def timed(torch, fn, steps, warmup):
     return s.elapsed_time(e) / steps
 
 
-def main():
-    args = parse()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(see the sharding design notes); use --gpus 1", file=sys.stderr)
-        sys.exit(2)
-    import torch
-    from paper_2112_00029_amd import pixelfly as pf
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    wl = synth.WORKLOADS[args.workload]
-    R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention,
-         "patterns": Patterns, "butterfly": Butterfly}[wl.kind](torch, pf, wl)
-
-    if args.copy_probe:
-        n = args.copy_probe << 20
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
-
-    calls = [c for c in args.calls_only.split(",") if c] or R.calls
-    if "dense" in calls:  # profiling aid: the dense comparator step as one call
-        R.dense_setup()
-        base_call = R.call
-        R.call = lambda c: R.dense_step() if c == "dense" else base_call(c)
-    # Warmup, then the timed region: K whole steps bracketed by two events
-    # only (nothing else recorded in between), which gives ms_per_step.
+def measure(torch, pf, R, args, calls):
+    """Warmup, the timed region (K whole steps between two events), the
+    kernel-timing region and the cold-cache pass.  Returns (ms_per_step,
+    per_kernel, cold_ms_per_step)."""
     for _ in range(args.warmup):
         for c in calls:
             R.call(c)
@@ -732,71 +746,87 @@ def main():
     # Kernel-timing region: the same K steps again with the library's
     # per-launch events (pf_timing_begin: each dispatch records its start and
     # end), which give per-kernel durations and the roofline entry.
-    kernel_timing = not args.no_kernel_timing
-    if kernel_timing:
+    per_kernel = {}
+    if not args.no_kernel_timing:
         pf.pf_timing_begin(args.steps * 8)
         for _ in range(args.steps):
             for c in calls:
                 R.call(c)
         torch.cuda.synchronize()
-    kt = pf.pf_timing_end() if kernel_timing else {}
-    per_kernel = {c: {"launches_per_step": n / args.steps, "avg_ms": avg,
-                      "ms_per_step": n * avg / args.steps} for c, (n, avg) in kt.items() if n}
-    if args.calls_only:
-        print(json.dumps({"calls_only": calls, "ms_per_step": ms, "per_kernel": per_kernel}))
-        return
+        kt = pf.pf_timing_end()
+        per_kernel = {c: {"launches_per_step": n / args.steps, "avg_ms": avg,
+                          "ms_per_step": n * avg / args.steps} for c, (n, avg) in kt.items() if n}
 
-    sparse, lowrank, dense_fl = R.flops()
-    value = sparse / (ms * 1e-3) / 1e12
-    peak = PEAK_BF16_TFLOPS if R.dtype == "bf16" else PEAK_FP32_TFLOPS
+    # Cold cache: 1 GiB written between steps (outside each step's event
+    # pair) evicts the operands from the L2s and the 256 MB MALL, so every
+    # step starts from HBM.
+    cold = None
+    if not args.no_cold:
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        n = max(3, min(args.steps, 20))
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(n)]
+        for i in range(n):
+            scratch.fill_(i & 0xff)
+            evs[i][0].record()
+            for c in calls:
+                R.call(c)
+            evs[i][1].record()
+        torch.cuda.synchronize()
+        cold = sum(a.elapsed_time(b) for a, b in evs) / n
+        del scratch
+    return ms, per_kernel, cold
 
-    dense_ms = torch_ms = None
-    if not args.no_dense:
-        R.dense_setup()
-        dense_ms = timed(torch, R.dense_step, max(5, args.steps // 4), 3)
-        if wl.kind != "attention":
-            torch_ms = timed(torch, R.torch_dense_step, max(5, args.steps // 4), 3)
-    extra = R.extra() if hasattr(R, "extra") else {}
 
-    # Roofline of the dominant kernel: the kernel class with the most time
-    # per step, its algorithmic work per launch over its mean launch time
-    # (HIP events recorded by the library around each launch, in the
-    # kernel-timing region, on the stream the kernel ran on).
-    roof = None
+def roofline(R, wl, per_kernel):
+    """Roofline of the dominant kernel: the kernel class with the most time
+    per step, its algorithmic work per launch over its mean launch time (HIP
+    events recorded by the library around each launch, in the kernel-timing
+    region, on the stream the kernel ran on)."""
     work = R.kernel_work()
     cand = {c: v for c, v in per_kernel.items() if c in work}
-    if cand:
-        dom = max(cand, key=lambda c: cand[c]["ms_per_step"])
-        lps, t = cand[dom]["launches_per_step"], cand[dom]["avg_ms"] * 1e-3
-        fl, by = work[dom][0] / lps, work[dom][1] / lps
-        ai = fl / by
-        if R.dtype == "bf16" and ai >= RIDGE_BF16:
-            roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
-        elif R.dtype == "bf16":
-            roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-        else:  # fp32: MFMA fp32 peak vs HBM by the same ridge rule
-            if ai >= PEAK_FP32_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
-                roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
-            else:
-                roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
-        roof["frac"] = roof["achieved"] / roof["peak"]
-        tr, why = measured_traffic(wl.name, dom)
-        roof["traffic"] = tr["bytes"] if tr else None
-        if tr:
-            roof["traffic_detail"] = {"fetch_bytes": tr["fetch"], "write_bytes": tr["write"],
-                                      "over_algorithmic": tr["bytes"] / by, "source": "profiles/" + tr["file"]}
+    if not cand:
+        return None
+    dom = max(cand, key=lambda c: cand[c]["ms_per_step"])
+    lps, t = cand[dom]["launches_per_step"], cand[dom]["avg_ms"] * 1e-3
+    fl, by = work[dom][0] / lps, work[dom][1] / lps
+    ai = fl / by
+    if R.dtype == "bf16" and ai >= RIDGE_BF16:
+        roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s"}
+    elif R.dtype == "bf16":
+        roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    else:  # fp32: MFMA fp32 peak vs HBM by the same ridge rule
+        if ai >= PEAK_FP32_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9):
+            roof = {"bound": "mfma", "achieved": fl / t / 1e12, "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s"}
         else:
-            roof["traffic_detail"] = why
-        roof.update({"kernel": dom, "avg_launch_ms": cand[dom]["avg_ms"], "launches_per_step": lps,
-                     "algorithmic_bytes_per_launch": by, "flops_per_launch": fl,
-                     "flop_per_byte": ai,
-                     "tflops_per_launch": fl / t / 1e12, "gbs_per_launch": by / t / 1e9})
+            roof = {"bound": "hbm", "achieved": by / t / 1e9, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    tr, why = measured_traffic(wl.name, dom)
+    roof["traffic"] = tr["bytes"] if tr else None
+    if tr:
+        roof["traffic_detail"] = {"fetch_bytes": tr["fetch"], "write_bytes": tr["write"],
+                                  "over_algorithmic": tr["bytes"] / by, "source": "profiles/" + tr["file"]}
+    else:
+        roof["traffic_detail"] = why
+    roof.update({"kernel": dom, "avg_launch_ms": cand[dom]["avg_ms"], "launches_per_step": lps,
+                 "algorithmic_bytes_per_launch": by, "flops_per_launch": fl,
+                 "flop_per_byte": ai,
+                 "tflops_per_launch": fl / t / 1e12, "gbs_per_launch": by / t / 1e9})
+    # Every kernel class of the step on the same footing (fraction of the
+    # peak its arithmetic intensity makes it bound by).
+    kinds = {}
+    for c, v in cand.items():
+        f, b_ = work[c][0] / v["launches_per_step"], work[c][1] / v["launches_per_step"]
+        tt = v["avg_ms"] * 1e-3
+        mf = R.dtype == "bf16" and f / b_ >= RIDGE_BF16
+        kinds[c] = {"bound": "mfma" if mf else "hbm",
+                    "frac": (f / tt / 1e12 / PEAK_BF16_TFLOPS) if mf else (b_ / tt / 1e9 / PEAK_HBM_GBS),
+                    "tflops": f / tt / 1e12, "gbs": b_ / tt / 1e9}
+    roof["per_kernel_frac"] = kinds
+    return roof
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        v, sample = R.cpu_baseline()
-        cpu = {"value": v, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle", "sample": sample}
 
+def config_of(wl, R):
     cfg = {"workload": wl.name}
     if wl.kind == "attention":
         cfg.update(B=wl.B, H=wl.H, S=wl.S, d=wl.d, b=wl.b, max_stride=wl.max_stride,
@@ -807,22 +837,121 @@ def main():
         cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=R.ms, r=R.r, budget=Patterns.DENSITY)
     else:
         cfg.update(T=wl.T, K=wl.K, N=wl.N, b=wl.b, max_stride=wl.max_stride, r=wl.r)
+    return cfg
+
+
+def run_workload(torch, pf, args, name, dense=None, cpu=True):
+    """One workload: its measurement, dense comparator and CPU baseline.
+    dense: (in-library, torch) ms per step already measured at this dense
+    shape (the block-size sweep shares it), else measured here."""
+    wl = synth.WORKLOADS[name]
+    R = {"linear": Linear, "mlp_pair": MlpPair, "attention": Attention,
+         "patterns": Patterns, "butterfly": Butterfly}[wl.kind](torch, pf, wl)
+    calls = [c for c in args.calls_only.split(",") if c] or R.calls
+    if "dense" in calls:  # profiling aid: the dense comparator step as one call
+        R.dense_setup()
+        base_call = R.call
+        R.call = lambda c: R.dense_step() if c == "dense" else base_call(c)
+    ms, per_kernel, cold = measure(torch, pf, R, args, calls)
+    if args.calls_only:
+        return {"calls_only": calls, "ms_per_step": ms, "per_kernel": per_kernel}, R
+
+    sparse, lowrank, dense_fl = R.flops()
+    value = sparse / (ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if R.dtype == "bf16" else PEAK_FP32_TFLOPS
+    if dense is None:
+        dense_ms = torch_ms = None
+        if not args.no_dense:
+            R.dense_setup()
+            dense_ms = timed(torch, R.dense_step, max(5, args.steps // 4), 3)
+            if wl.kind != "attention":
+                torch_ms = timed(torch, R.torch_dense_step, max(5, args.steps // 4), 3)
+    else:
+        dense_ms, torch_ms = dense
+    best_dense = min(x for x in (dense_ms, torch_ms) if x) if (dense_ms or torch_ms) else None
+    extra = R.extra() if hasattr(R, "extra") else {}
+
+    cpu_b = None
+    if cpu and not args.no_cpu_baseline:
+        v, sample = R.cpu_baseline()
+        cpu_b = {"value": v, "unit": "TFLOP/s", "cores": blas_threads(), "kind": "oracle",
+                 "sample": sample, **cpu_meta()}
+
     out = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": R.dtype, "data": "synthetic (seeded, shapes of the workload)",
-        "config": cfg,
+        "config": config_of(wl, R),
         "pct_peak": 100.0 * value / peak,
         "useful_tflops_incl_lowrank": (sparse + lowrank) / (ms * 1e-3) / 1e12,
+        "cold_ms_per_step": cold,
+        "cold_value": (sparse / (cold * 1e-3) / 1e12) if cold else None,
+        # Speedup over the faster of the two dense steps of the same shape:
+        # the library's own MFMA GEMM and torch.matmul (hipBLASLt).
+        "speedup_vs_dense": (best_dense / ms) if best_dense else None,
+        "speedup_vs_library_dense": (dense_ms / ms) if dense_ms else None,
+        "speedup_vs_torch_dense": (torch_ms / ms) if torch_ms else None,
         "dense_ms_per_step": dense_ms,
-        "speedup_vs_dense": (dense_ms / ms) if dense_ms else None,
         "dense_tflops": (dense_fl / (dense_ms * 1e-3) / 1e12) if dense_ms else None,
         "torch_dense_ms_per_step": torch_ms,
+        "torch_dense_tflops": (dense_fl / (torch_ms * 1e-3) / 1e12) if torch_ms else None,
         "per_kernel": per_kernel,
-        "roofline": roof,
-        "cpu_baseline": cpu,
+        "roofline": roofline(R, wl, per_kernel),
+        "cpu_baseline": cpu_b,
     }
     out.update(extra)
+    return out, R
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see the sharding design notes); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2112_00029_amd import pixelfly as pf
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    if args.copy_probe:
+        n = args.copy_probe << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    out, R = run_workload(torch, pf, args, args.workload)
+    if args.calls_only:
+        print(json.dumps(out))
+        return
+    # The 16384 x 4096 layer is quoted as a sweep over the block size (the
+    # MFMA-utilisation curve): the other two block sizes run in the same
+    # process on the same inputs and the same dense comparator.
+    sweep_of = {f"linear_16384x4096_b{b}": b for b in (128, 64, 32)}
+    if args.workload in sweep_of and not args.no_sweep:
+        dense = (out["dense_ms_per_step"], out["torch_dense_ms_per_step"])
+        rows = [{"b": sweep_of[args.workload], "workload": args.workload,
+                 "ms_per_step": out["ms_per_step"], "value": out["value"],
+                 "pct_peak": out["pct_peak"], "cold_ms_per_step": out["cold_ms_per_step"],
+                 "speedup_vs_dense": out["speedup_vs_dense"],
+                 "dominant": out["roofline"] and {k: out["roofline"][k] for k in ("kernel", "bound", "frac")}}]
+        del R
+        for name in sweep_of:
+            if name == args.workload:
+                continue
+            o, R2 = run_workload(torch, pf, args, name, dense=dense, cpu=False)
+            rows.append({"b": sweep_of[name], "workload": name, "ms_per_step": o["ms_per_step"],
+                         "value": o["value"], "pct_peak": o["pct_peak"],
+                         "cold_ms_per_step": o["cold_ms_per_step"],
+                         "speedup_vs_dense": o["speedup_vs_dense"],
+                         "useful_tflops_incl_lowrank": o["useful_tflops_incl_lowrank"],
+                         "per_kernel": o["per_kernel"],
+                         "dominant": o["roofline"] and {k: o["roofline"][k] for k in ("kernel", "bound", "frac")}})
+            del R2
+        out["block_size_sweep"] = sorted(rows, key=lambda r: -r["b"])
     print(json.dumps(out))
 
 

@@ -202,6 +202,33 @@ pf_status pf_layout_plan_get(const pf_layout *layout, int32_t *stats,
                              int32_t n);
 
 /*
+ * Diagnostic: the kernels and work split a forward + backward step of T
+ * tokens at rank r runs on this layout (host only; the layout need not be
+ * uploaded).  The rank-r products T_lr = X V^T and S = dY U report kernel 0
+ * (r = 0, not run), 1 (the rank-r kernel: 32-token x 64-column workgroups)
+ * or 2 (the tile kernel in dense mode), the number of workgroups that split
+ * one output tile's K range (fp32 partials summed by a second pass when
+ * above 1) and the output tile (tokens x columns).  The block-sparse
+ * products report their output tile and kernel family (1: operands copied
+ * global -> LDS directly; 0: staged through registers).  The weight
+ * gradient reports its work items (kept-block tiles plus the dU and dV
+ * tiles), the token split and the tokens per split.  Errors as the compute
+ * calls' argument checks: INVALID_ARG, UNSUPPORTED.
+ */
+typedef struct {
+  int32_t lowrank_t_kernel, lowrank_t_split, lowrank_t_tile_m, lowrank_t_tile_n;
+  int32_t lowrank_s_kernel, lowrank_s_split, lowrank_s_tile_m, lowrank_s_tile_n;
+  int32_t fwd_tile_m, fwd_tile_n, fwd_direct_lds;
+  int32_t bwd_tile_m, bwd_tile_n, bwd_direct_lds;
+  int32_t tn_items, tn_split;
+  int64_t tn_chunk;
+  uint64_t workspace_bytes; /* pf_workspace_bytes of the same arguments */
+} pf_linear_plan;
+
+pf_status pf_linear_plan_get(const pf_layout *layout, pf_dtype dtype, int64_t T,
+                             int32_t r, pf_linear_plan *out);
+
+/*
  * Copy the layout's index arrays and kernel work lists to the current HIP
  * device (one-time, synchronous on `stream`).  Must precede compute calls;
  * the layout then serves that device only.  Errors: INVALID_ARG, HIP, NOMEM,

@@ -2,8 +2,8 @@
 
 Test infrastructure only.
 
-Layer (Section 3.3, model sparsification; the learnable mixing weight is taken
-as folded into W and U by the caller):
+Layer (Section 3.3, model sparsification; the learnable mixing weight of the
+same section is in forward_mixed / backward_mixed below):
     Y = X (M o W)^T + (X V^T) U^T
 with X: T x K, W: N x K kept on the b x b blocks of the flat block butterfly
 mask M, U: N x r, V: r x K.  The low-rank product is applied as U (V^T x)
@@ -62,12 +62,17 @@ def backward(X, Wd, Mel, dY, U=None, V=None):
     dU, dV, S = dY U when the low-rank term is present."""
     out = {"dX": dY @ Wd, "dW": (dY.T @ X) * Mel}
     if U is not None and U.shape[1] > 0:
-        S = dY @ U
-        out["S"] = S
-        out["dX"] = out["dX"] + S @ V
-        out["dU"] = dY.T @ (X @ V.T)
-        out["dV"] = S.T @ X
+        lr = lowrank_grads(X, dY, U, V)
+        out.update(lr)
+        out["dX"] = out["dX"] + lr["S"] @ V
     return out
+
+
+def lowrank_grads(X, dY, U, V):
+    """The low-rank part of the backward alone: S = dY U, dU = dY^T (X V^T),
+    dV = S^T X (backward() adds S V to dX)."""
+    S = dY @ U
+    return {"S": S, "dU": dY.T @ (X @ V.T), "dV": S.T @ X}
 
 
 def forward_blockloop(X, Wblk, row_ptr, col_idx, nb_out: int, b: int):

@@ -20,7 +20,16 @@ LIB = os.path.join(PKG, "libpixelfly.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["layout.cpp", "capi.cpp", "gemm_kernels.hip", "gemm_dma.hip", "skinny.hip", "attn_kernels.hip"]
+# (source, object name, defines): the two GEMM sources are compiled once per
+# part (their launchers say which instantiations each part holds) so that
+# the template instantiations compile in parallel.
+SOURCES = (
+    [("layout.cpp", "layout", ()), ("capi.cpp", "capi", ()),
+     ("skinny.hip", "skinny", ()), ("attn_kernels.hip", "attn_kernels", ())]
+    + [("gemm_kernels.hip", f"gemm_kernels_p{p}", (f"PF_GK_PART={p}",)) for p in range(7)]
+    + [("gemm_dma.hip", f"gemm_dma_b{b}_{k}", (f"PF_PART_BLK={b}", f"PF_PART_BKN={k}"))
+       for b in (32, 64, 128) for k in (0, 1)]
+)
 
 # Per-source extra flags.  The attention kernels feed MFMA results straight
 # into VALU softmax arithmetic: asking for the VGPR form of MFMA keeps those
@@ -38,9 +47,9 @@ FLAGS = [
 ]
 
 
-def _compile(src: str, build_dir: str = BUILD, defines=()) -> str:
-    obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, *SOURCE_FLAGS.get(src, []), *[f"-D{d}" for d in defines]]
+def _compile(src: str, build_dir: str = BUILD, defines=(), name=None, part=()) -> str:
+    obj = os.path.join(build_dir, (name or os.path.splitext(src)[0]) + ".o")
+    cmd = [HIPCC, *FLAGS, *SOURCE_FLAGS.get(src, []), *[f"-D{d}" for d in (*part, *defines)]]
     if src.endswith(".cpp"):
         cmd += ["-x", "hip"]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
@@ -57,8 +66,11 @@ def _compile(src: str, build_dir: str = BUILD, defines=()) -> str:
 def build(verbose: bool = True, lib: str = LIB, build_dir: str = BUILD, defines=()) -> str:
     """Compile and link; `defines` are extra -D tuning macros."""
     os.makedirs(build_dir, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, build_dir, defines), SOURCES))
+    # Largest parts first (the NT parts of the direct-to-LDS family).
+    order = sorted(SOURCES, key=lambda e: not e[0].startswith("gemm"))
+    workers = max(1, min(len(order), os.cpu_count() or 1))
+    with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+        objs = list(ex.map(lambda e: _compile(e[0], build_dir, defines, e[1], e[2]), order))
     tmp = lib + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -19,7 +19,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "pf_internal.h"
+#include "pf_launch.h"
 
 namespace pf {
 

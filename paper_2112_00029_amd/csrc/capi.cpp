@@ -1,6 +1,6 @@
 // C ABI of libpixelfly.so: argument validation (all before any enqueue) and
 // dispatch to the HIP kernels.  See include/pixelfly.h for the contract.
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 
 #include <algorithm>
 #include <cmath>
@@ -20,6 +20,14 @@ namespace pf {
 LaunchEvents &next_launch_events() {
   thread_local LaunchEvents e;
   return e;
+}
+
+int tn_items_total(const TNArgs &a, int blk) {
+  const int GT = 128 / blk;
+  int n = a.n_items;
+  for (int r = 0; r < a.n_dense; ++r)
+    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
+  return n;
 }
 }  // namespace pf
 
@@ -105,11 +113,23 @@ pf_status check_state(const pf_layout *L) {
   return PF_OK;
 }
 
+// Kernels address a tile of up to 512 token rows of any operand with 32-bit
+// buffer offsets: 512 rows of the widest operand must stay below 2^31 bytes.
+constexpr int64_t kMaxRowBytes = 0x7fffffffLL / 512;
+
 pf_status check_dtype_r(pf_dtype dt, int64_t T, int32_t r, int32_t b) {
   if (dt != PF_BF16 && dt != PF_FP32) return fail(PF_ERR_INVALID_ARG, "bad dtype");
   if (T < 1) return fail(PF_ERR_INVALID_ARG, "T must be >= 1");
   if (T > ((int64_t)1 << 31) / 2) return fail(PF_ERR_INVALID_ARG, "T too large");
   if (r < 0 || r % b) return fail(PF_ERR_INVALID_ARG, "r must be a non-negative multiple of b");
+  return PF_OK;
+}
+
+pf_status check_extent(const pf_layout *L, pf_dtype dt, int32_t r) {
+  const int64_t es = dt == PF_BF16 ? 2 : 4;
+  if (std::max<int64_t>({L->n_out, L->n_in, r}) * es > kMaxRowBytes)
+    return fail(PF_ERR_UNSUPPORTED, "rows wider than " + std::to_string(kMaxRowBytes) +
+                                        " bytes are not supported");
   return PF_OK;
 }
 
@@ -137,24 +157,40 @@ bool ntd_width(int dtype, int blk, int G) {
   return PF_NTD && dtype == 0 && (w == 128 || w == 256 || (w == 64 && blk <= 64));
 }
 
-// kmax: the most K-blocks (kept + low-rank) of any tile of the launch.
+// The NT kernel one launch runs: the family (direct-to-LDS or
+// register-staged), its variant, and the token x column output tile.
+struct NTChoice {
+  bool dma;
+  int variant;
+  int bm, bn;
+};
+
+// kmax: the most K-blocks (kept + low-rank) of any tile of the launch; bm:
+// token tile of the register-staged family.
+NTChoice nt_choose(int dtype, int blk, int G, int bm, int kmax, int64_t M, int ntiles, int nsplit,
+                   bool dense) {
+  if (!ntd_width(dtype, blk, G)) return NTChoice{false, 0, bm, G * blk};
+  // 128-column outputs: 512-token tiles once they still make 512+
+  // workgroups; for block-sparse tiles, short K-steps with three workgroups
+  // per CU when every tile has at most 8 steps of 64 and one round of
+  // workgroups covers them.
+  const int w = G * blk;
+  if (w == 128) {
+    const int64_t ns = std::max(1, nsplit);
+    const int64_t wg = ((M + 127) / 128) * ntiles * ns;
+    const int64_t steps = ((int64_t)kmax * blk + 63) / 64;
+    if (((M + 511) / 512) * ntiles * ns >= 512) return NTChoice{true, pf::NTD_TALL, 512, 128};
+    if (!dense && steps <= 8 && wg <= 768) return NTChoice{true, pf::NTD_SHORT_K, 128, 128};
+    return NTChoice{true, pf::NTD_DEFAULT, 128, 128};
+  }
+  return NTChoice{true, pf::NTD_DEFAULT, 256, w};  // 256 x 256 and 256 x 64 tiles
+}
+
 hipError_t nt_launch(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm, int kmax,
                      const pf::NTArgs &a, hipStream_t s) {
   Timed t(kc, s);
-  if (ntd_width(dtype, blk, G)) {
-    // 128-column outputs: 512-token tiles once they still make 512+
-    // workgroups; for block-sparse tiles, short K-steps with three
-    // workgroups per CU when every tile has at most 8 steps of 64 and one
-    // round of workgroups covers them.
-    int variant = pf::NTD_DEFAULT;
-    if (G * blk == 128) {
-      const int64_t wg = ((a.M + 127) / 128) * a.ntiles * std::max(1, a.nsplit);
-      const int64_t steps = ((int64_t)kmax * blk + 63) / 64;
-      if (((a.M + 511) / 512) * a.ntiles * std::max(1, a.nsplit) >= 512) variant = pf::NTD_TALL;
-      else if (!a.dense && steps <= 8 && wg <= 768) variant = pf::NTD_SHORT_K;
-    }
-    return pf::launch_ntd(blk, G, b_kn, variant, a, s);
-  }
+  const NTChoice c = nt_choose(dtype, blk, G, bm, kmax, a.M, a.ntiles, a.nsplit, a.dense != 0);
+  if (c.dma) return pf::launch_ntd(blk, G, b_kn, c.variant, a, s);
   return pf::launch_nt(dtype, blk, G, b_kn, bm, a, s);
 }
 
@@ -195,8 +231,17 @@ pf_status dense_nt(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int
 #ifndef PF_SKINNY_MAX_TILES
 #define PF_SKINNY_MAX_TILES 64
 #endif
-bool use_skinny(int dtype, int64_t T, int r) {
-  return dtype == 0 && r > 0 && ((T + 127) / 128) * ((r + 127) / 128) < PF_SKINNY_MAX_TILES;
+// The rank-r kernel addresses its operands through 32-bit buffer ranges and
+// points steps past the end at the offset 0x7ffffff0, which must lie outside
+// every range: A's 32-row tile (32 K-long rows) and the whole r x K (or
+// K x r) second operand.  Larger shapes take the tile kernel.
+bool skinny_fits(int64_t K, int r) {
+  const int64_t lim = 0x7ffffff0LL;
+  return 32 * K * 2 < lim && (int64_t)r * K * 2 < lim;
+}
+bool use_skinny(int dtype, int64_t T, int r, int64_t K) {
+  return dtype == 0 && r > 0 && ((T + 127) / 128) * ((r + 127) / 128) < PF_SKINNY_MAX_TILES &&
+         skinny_fits(K, r);
 }
 
 // bf16 rank-r product C[M x r] = A[M x K] . op(B) on the rank-r kernel
@@ -233,7 +278,7 @@ struct SkinnyPlan {
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0};
-  if (r <= 0 || use_skinny(dtype, T, r)) return p;  // the rank-r kernel needs no split
+  if (r <= 0 || use_skinny(dtype, T, r, (int64_t)kblocks * blk)) return p;  // no split
   const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + 127) / 128;
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
   int64_t ns;
@@ -300,7 +345,13 @@ TNPlan tn_plan(int items, int64_t T, int64_t row_bytes) {
   }
   ns = std::max(ns, min_split);
   if (ns > 1) {
-    const int64_t chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
+    int64_t chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
+    // Rounding the chunk up to whole 64-token steps can push a split's rows
+    // past the 32-bit buffer range again: take more splits until it fits.
+    while (chunk * row_bytes > 0x7fffffffLL && chunk > 64) {
+      ++ns;
+      chunk = ((T + ns - 1) / ns + 63) / 64 * 64;
+    }
     ns = (T + chunk - 1) / chunk;
     if (ns > 1) {
       p.nsplit = (int)ns;
@@ -318,6 +369,31 @@ size_t mix_dgamma_bytes(int items) {
   return ((size_t)items * 16 + pf::kMixDotParts) * sizeof(float) + 256;
 }
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Tile list of a block-sparse NT launch: the wide list (256-column bf16
+// tiles) once the token count fills them, else the narrow one.
+struct NTList {
+  bool wide;
+  int G, ntiles, kmax;
+  const pf::NTTile *tiles;
+  const int32_t *kcols, *blks;
+};
+NTList fwd_list(const pf_layout *L, int dt, int64_t T) {
+  const bool wide = ntd_width(dt, L->b, L->G_fwd_w) && L->G_fwd_w * L->b == 256 && T >= PF_WIDE_MIN_T;
+  if (wide)
+    return NTList{true, L->G_fwd_w, (int)L->fwd_tiles_w.size(), L->kmax_fwd, L->d_fwd_tiles_w,
+                  L->d_kcols_fwd_w, L->d_blks_fwd_w};
+  return NTList{false, L->G_fwd, (int)L->fwd_tiles.size(), L->kmax_fwd, L->d_fwd_tiles,
+                L->d_kcols_fwd, L->d_blks_fwd};
+}
+NTList bwd_list(const pf_layout *L, int dt, int64_t T) {
+  const bool wide = ntd_width(dt, L->b, L->G_bwd_w) && L->G_bwd_w * L->b == 256 && T >= PF_WIDE_MIN_T;
+  if (wide)
+    return NTList{true, L->G_bwd_w, (int)L->bwd_tiles_w.size(), L->kmax_bwd, L->d_bwd_tiles_w,
+                  L->d_kcols_bwd_w, L->d_blks_bwd_w};
+  return NTList{false, L->G_bwd, (int)L->bwd_tiles.size(), L->kmax_bwd, L->d_bwd_tiles,
+                L->d_kcols_bwd, L->d_blks_bwd};
+}
 
 void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
                      const void *X, const void *T_lr, const void *S, void *dU, void *dV) {
@@ -686,6 +762,68 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
   return std::max({tn, fwd, bwd}) + mix_dgamma_bytes(items);
 }
 
+pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
+                             pf_linear_plan *o) {
+  if (!o) return fail(PF_ERR_INVALID_ARG, "out is NULL");
+  pf_status st = check_layout_arg(L);
+  if (st != PF_OK) return st;
+  if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = check_extent(L, dtype, r)) != PF_OK) return st;
+  const int dt = (int)dtype, b = L->b;
+  pf_linear_plan p{};
+  // Rank-r products: the same decisions as enqueue of T_lr and S.
+  auto rank = [&](int64_t K, int kblocks, bool b_kn, int32_t *v) {
+    if (r <= 0) return;
+    if (use_skinny(dt, T, r, K)) {
+      v[0] = 1;
+      v[1] = 1;
+      v[2] = 32;
+      v[3] = 64;
+      return;
+    }
+    const SkinnyPlan sp = skinny_plan(dtype, b, T, kblocks, r);
+    const int G = 128 / b;
+    const NTChoice c = nt_choose(dt, b, G, sp.bm, (kblocks + sp.nsplit - 1) / sp.nsplit, T,
+                                 (r / b + G - 1) / G, sp.nsplit, true);
+    (void)b_kn;
+    v[0] = 2;
+    v[1] = sp.nsplit;
+    v[2] = c.bm;
+    v[3] = c.bn;
+  };
+  int32_t t[4] = {0, 0, 0, 0}, sv[4] = {0, 0, 0, 0};
+  rank(L->n_in, L->nb_in, false, t);
+  rank(L->n_out, L->nb_out, true, sv);
+  p.lowrank_t_kernel = t[0];
+  p.lowrank_t_split = t[1];
+  p.lowrank_t_tile_m = t[2];
+  p.lowrank_t_tile_n = t[3];
+  p.lowrank_s_kernel = sv[0];
+  p.lowrank_s_split = sv[1];
+  p.lowrank_s_tile_m = sv[2];
+  p.lowrank_s_tile_n = sv[3];
+  const NTList f = fwd_list(L, dt, T), g = bwd_list(L, dt, T);
+  const NTChoice cf = nt_choose(dt, b, f.G, 128, f.kmax + r / b, T, f.ntiles, 1, false);
+  const NTChoice cg = nt_choose(dt, b, g.G, 128, g.kmax + r / b, T, g.ntiles, 1, false);
+  p.fwd_tile_m = cf.bm;
+  p.fwd_tile_n = cf.bn;
+  p.fwd_direct_lds = cf.dma;
+  p.bwd_tile_m = cg.bm;
+  p.bwd_tile_n = cg.bn;
+  p.bwd_direct_lds = cg.dma;
+  pf::TNArgs a{};
+  a.n_items = (int)L->tn_items.size();
+  fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+  const int items = pf::tn_items_total(a, b);
+  const TNPlan tp = tn_plan(items, T, std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
+  p.tn_items = items;
+  p.tn_split = tp.nsplit;
+  p.tn_chunk = tp.chunk;
+  p.workspace_bytes = pf_workspace_bytes(L, T, r, dtype);
+  *o = p;
+  return PF_OK;
+}
+
 // Checks a caller workspace against a need of `need` bytes.
 static pf_status need_ws(size_t need, const void *ws, size_t ws_bytes) {
   if (need == 0) return PF_OK;
@@ -733,6 +871,7 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = check_extent(L, dtype, r)) != PF_OK) return st;
   if ((st = need_ptr(X, "X")) != PF_OK || (st = need_ptr(Wblk, "Wblk")) != PF_OK ||
       (st = need_ptr(Y, "Y")) != PF_OK)
     return st;
@@ -747,7 +886,7 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   const int dt = (int)dtype, b = L->b;
-  if (use_skinny(dt, T, r)) {
+  if (use_skinny(dt, T, r, L->n_in)) {
     st = skinny_bf16(PF_KERNEL_LOWRANK_T, false, T, X, L->n_in, V, L->n_in, (int)L->n_in, r, T_lr,
                      s, "T_lr kernel");
     if (st != PF_OK) return st;
@@ -766,15 +905,14 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
   a.C2 = epi == PF_EPI_GELU ? Y_pre : nullptr;
   a.epi = (int)epi;
   a.M = T;
-  const bool wide = ntd_width(dt, b, L->G_fwd_w) && L->G_fwd_w * b == 256 && T >= PF_WIDE_MIN_T;
-  a.tiles = wide ? L->d_fwd_tiles_w : L->d_fwd_tiles;
-  a.ntiles = (int)(wide ? L->fwd_tiles_w.size() : L->fwd_tiles.size());
-  a.kcols = wide ? L->d_kcols_fwd_w : L->d_kcols_fwd;
-  a.blks = wide ? L->d_blks_fwd_w : L->d_blks_fwd;
+  const NTList tl = fwd_list(L, dt, T);
+  a.tiles = tl.tiles;
+  a.ntiles = tl.ntiles;
+  a.kcols = tl.kcols;
+  a.blks = tl.blks;
   a.nsplit = 1;
   set_mix(a, mix);
-  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, wide ? L->G_fwd_w : L->G_fwd, false, 128,
-                              L->kmax_fwd + a.nlr, a, s),
+  return hip_status(nt_launch(PF_KERNEL_SPMM_FWD, dt, b, tl.G, false, 128, tl.kmax + a.nlr, a, s),
                     "forward kernel");
 }
 
@@ -811,6 +949,7 @@ pf_status check_bwd_data_args(const pf_layout *L, pf_dtype dtype, int64_t T, int
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = check_extent(L, dtype, r)) != PF_OK) return st;
   if ((st = need_ptr(dY, "dY")) != PF_OK || (st = need_ptr(Wblk, "Wblk")) != PF_OK ||
       (st = need_ptr(dX, "dX")) != PF_OK)
     return st;
@@ -828,6 +967,7 @@ pf_status check_bwd_weight_args(const pf_layout *L, pf_dtype dtype, int64_t T, i
   pf_status st = check_layout_arg(L);
   if (st != PF_OK) return st;
   if ((st = check_dtype_r(dtype, T, r, L->b)) != PF_OK) return st;
+  if ((st = check_extent(L, dtype, r)) != PF_OK) return st;
   if ((st = need_ptr(dY, "dY")) != PF_OK || (st = need_ptr(X, "X")) != PF_OK ||
       (st = need_ptr(dWblk, "dWblk")) != PF_OK)
     return st;
@@ -841,7 +981,7 @@ pf_status check_bwd_weight_args(const pf_layout *L, pf_dtype dtype, int64_t T, i
 pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
                     const void *U, void *S, const SkinnyPlan &sp, float *ws, hipStream_t s) {
   if (r <= 0) return PF_OK;
-  if (use_skinny(dt, T, r))
+  if (use_skinny(dt, T, r, L->n_out))
     return skinny_bf16(PF_KERNEL_LOWRANK_S, true, T, dY, L->n_out, U, r, (int)L->n_out, r, S, s,
                        "S kernel");
   const int b = L->b;
@@ -862,15 +1002,14 @@ pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const voi
   a.aux = aux;
   a.epi = (int)epi;
   a.M = T;
-  const bool wide = ntd_width(dt, b, L->G_bwd_w) && L->G_bwd_w * b == 256 && T >= PF_WIDE_MIN_T;
-  a.tiles = wide ? L->d_bwd_tiles_w : L->d_bwd_tiles;
-  a.ntiles = (int)(wide ? L->bwd_tiles_w.size() : L->bwd_tiles.size());
-  a.kcols = wide ? L->d_kcols_bwd_w : L->d_kcols_bwd;
-  a.blks = wide ? L->d_blks_bwd_w : L->d_blks_bwd;
+  const NTList tl = bwd_list(L, dt, T);
+  a.tiles = tl.tiles;
+  a.ntiles = tl.ntiles;
+  a.kcols = tl.kcols;
+  a.blks = tl.blks;
   a.nsplit = 1;
   set_mix(a, mix);
-  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, wide ? L->G_bwd_w : L->G_bwd, true,
-                              128, L->kmax_bwd + a.nlr, a, s),
+  return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, b, tl.G, true, 128, tl.kmax + a.nlr, a, s),
                     "backward-data kernel");
 }
 

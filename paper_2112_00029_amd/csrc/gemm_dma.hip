@@ -31,7 +31,7 @@
 #include <algorithm>
 #include <type_traits>
 
-#include "pf_internal.h"
+#include "pf_launch.h"
 
 // Token rows per group of the workgroup order (a group covers the token
 // tiles of PF_GROUP_ROWS rows x a run of output tiles, so both operands are
@@ -571,8 +571,15 @@ hipError_t ntd_cfg(int variant, const NTArgs &a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
+}  // namespace
+
+// The launcher of one (block size, B orientation) pair.  The build compiles
+// this file once per pair (PF_PART_BLK, PF_PART_BKN) so that the
+// instantiations compile in parallel; launch_ntd in the C ABI code picks the
+// pair.
 template <int BLK, bool BKN>
-hipError_t ntd_g(int G, int variant, bool dense, const NTArgs &a, hipStream_t s) {
+hipError_t launch_ntd_bb(int G, int variant, const NTArgs &a, hipStream_t s) {
+  const bool dense = a.dense != 0;
   auto go = [&](auto g) {
     constexpr int GG = decltype(g)::value;
     return dense ? ntd_cfg<BLK, GG, BKN, true>(variant, a, s)
@@ -585,21 +592,9 @@ hipError_t ntd_g(int G, int variant, bool dense, const NTArgs &a, hipStream_t s)
   return hipErrorInvalidValue;
 }
 
-
-}  // namespace
-
-hipError_t launch_ntd(int blk, int G, bool b_kn, int variant, const NTArgs &a, hipStream_t s) {
-  const bool dense = a.dense != 0;
-  switch (blk) {
-    case 32:
-      return b_kn ? ntd_g<32, true>(G, variant, dense, a, s) : ntd_g<32, false>(G, variant, dense, a, s);
-    case 64:
-      return b_kn ? ntd_g<64, true>(G, variant, dense, a, s) : ntd_g<64, false>(G, variant, dense, a, s);
-    case 128:
-      return b_kn ? ntd_g<128, true>(G, variant, dense, a, s)
-                  : ntd_g<128, false>(G, variant, dense, a, s);
-  }
-  return hipErrorInvalidValue;
-}
+#if defined(PF_PART_BLK) && defined(PF_PART_BKN)
+template hipError_t launch_ntd_bb<PF_PART_BLK, (PF_PART_BKN != 0)>(int, int, const NTArgs &,
+                                                                    hipStream_t);
+#endif
 
 }  // namespace pf

@@ -31,7 +31,13 @@
 #include <algorithm>
 #include <type_traits>
 
-#include "pf_internal.h"
+#include "pf_launch.h"
+
+// Part of this file an object holds (see the launchers at the end).
+#ifndef PF_GK_PART
+#define PF_GK_PART -1
+#endif
+#define PF_GK_HAS(p) (PF_GK_PART < 0 || PF_GK_PART == (p))
 
 namespace pf {
 
@@ -942,6 +948,7 @@ __global__ __launch_bounds__(256) void mix_dot_kernel(const T *__restrict__ S,
   if (threadIdx.x == 0) out[blockIdx.x] = tot;
 }
 
+#if PF_GK_HAS(0)
 __global__ __launch_bounds__(256) void mix_final_kernel(const float *__restrict__ wparts, int nw,
                                                         const float *__restrict__ sparts, int ns,
                                                         float *__restrict__ dgamma) {
@@ -968,6 +975,7 @@ hipError_t launch_mix_dgamma(int dtype, const void *S, const void *T_lr, int64_t
                 n > 0 ? kMixDotParts : 0, dgamma);
   return hipGetLastError();
 }
+#endif
 
 // ---------------------------------------------------------------------------
 // GELU backward (standalone elementwise form)
@@ -979,8 +987,13 @@ __global__ __launch_bounds__(256) void gelu_bwd_kernel(int64_t n, const T *dH, c
 }
 
 // ---------------------------------------------------------------------------
-// Launchers
+// Launchers.  The build compiles this file once per part (PF_GK_PART): 0
+// holds the small kernels and the dispatch, 1-4 the NT kernel for (bf16 |
+// fp32) x (B as [n][k] | [k][n]), 5-6 the TN kernel for bf16 | fp32, so that
+// the template instantiations compile in parallel.  Without PF_GK_PART the
+// file holds everything.
 // ---------------------------------------------------------------------------
+
 template <typename T, int BLK, int G, bool BKN, int BM, bool DENSE>
 static hipError_t nt_go(const NTArgs &a, hipStream_t s) {
   const int64_t mtiles = (a.M + BM - 1) / BM;
@@ -1021,7 +1034,7 @@ static hipError_t nt_dispatch_g(int G, int bm, bool dense, const NTArgs &a, hipS
 }
 
 template <typename T, bool BKN>
-static hipError_t nt_dispatch_b(int blk, int G, int bm, bool dense, const NTArgs &a, hipStream_t s) {
+hipError_t launch_nt_tb(int blk, int G, int bm, bool dense, const NTArgs &a, hipStream_t s) {
   switch (blk) {
     case 32: return nt_dispatch_g<T, 32, BKN>(G, bm, dense, a, s);
     case 64: return nt_dispatch_g<T, 64, BKN>(G, bm, dense, a, s);
@@ -1029,36 +1042,18 @@ static hipError_t nt_dispatch_b(int blk, int G, int bm, bool dense, const NTArgs
     default: return hipErrorInvalidValue;
   }
 }
-
-hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a, hipStream_t s) {
-  const bool dense = a.dense != 0;
-  if (dtype == 0)
-    return b_kn ? nt_dispatch_b<bf16_t, true>(blk, G, bm, dense, a, s)
-                : nt_dispatch_b<bf16_t, false>(blk, G, bm, dense, a, s);
-  return b_kn ? nt_dispatch_b<float, true>(blk, G, bm, dense, a, s)
-              : nt_dispatch_b<float, false>(blk, G, bm, dense, a, s);
-}
-
-hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
-                              void *C, int64_t ldc, hipStream_t s) {
-  const int64_t n4 = M * ncols / 4;
-  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n4 + 255) / 256, 4096));
-  if (dtype == 0)
-    launch_kernel(reduce_rows_kernel<bf16_t>,
-                  dim3((unsigned)blocks), dim3(256), s, nsplit, P, M, ncols, (bf16_t *)C, ldc);
-  else
-    launch_kernel(reduce_rows_kernel<float>,
-                  dim3((unsigned)blocks), dim3(256), s, nsplit, P, M, ncols, (float *)C, ldc);
-  return hipGetLastError();
-}
-
-int tn_items_total(const TNArgs &a, int blk) {
-  const int GT = 128 / blk;
-  int n = a.n_items;
-  for (int r = 0; r < a.n_dense; ++r)
-    n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
-  return n;
-}
+#if PF_GK_HAS(1)
+template hipError_t launch_nt_tb<bf16_t, false>(int, int, int, bool, const NTArgs &, hipStream_t);
+#endif
+#if PF_GK_HAS(2)
+template hipError_t launch_nt_tb<bf16_t, true>(int, int, int, bool, const NTArgs &, hipStream_t);
+#endif
+#if PF_GK_HAS(3)
+template hipError_t launch_nt_tb<float, false>(int, int, int, bool, const NTArgs &, hipStream_t);
+#endif
+#if PF_GK_HAS(4)
+template hipError_t launch_nt_tb<float, true>(int, int, int, bool, const NTArgs &, hipStream_t);
+#endif
 
 template <typename T, int BLK>
 static hipError_t tn_go(const TNArgs &a, hipStream_t s) {
@@ -1076,38 +1071,62 @@ static hipError_t tn_reduce_go(const TNArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s) {
-  if (dtype == 0) {
-    switch (blk) {
-      case 32: return tn_go<bf16_t, 32>(a, s);
-      case 64: return tn_go<bf16_t, 64>(a, s);
-      case 128: return tn_go<bf16_t, 128>(a, s);
-    }
-  } else {
-    switch (blk) {
-      case 32: return tn_go<float, 32>(a, s);
-      case 64: return tn_go<float, 64>(a, s);
-      case 128: return tn_go<float, 128>(a, s);
-    }
+template <typename T>
+hipError_t launch_tn_t(int blk, const TNArgs &a, hipStream_t s) {
+  switch (blk) {
+    case 32: return tn_go<T, 32>(a, s);
+    case 64: return tn_go<T, 64>(a, s);
+    case 128: return tn_go<T, 128>(a, s);
   }
   return hipErrorInvalidValue;
 }
-
-hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s) {
-  if (dtype == 0) {
-    switch (blk) {
-      case 32: return tn_reduce_go<bf16_t, 32>(a, s);
-      case 64: return tn_reduce_go<bf16_t, 64>(a, s);
-      case 128: return tn_reduce_go<bf16_t, 128>(a, s);
-    }
-  } else {
-    switch (blk) {
-      case 32: return tn_reduce_go<float, 32>(a, s);
-      case 64: return tn_reduce_go<float, 64>(a, s);
-      case 128: return tn_reduce_go<float, 128>(a, s);
-    }
+template <typename T>
+hipError_t launch_tn_reduce_t(int blk, const TNArgs &a, hipStream_t s) {
+  switch (blk) {
+    case 32: return tn_reduce_go<T, 32>(a, s);
+    case 64: return tn_reduce_go<T, 64>(a, s);
+    case 128: return tn_reduce_go<T, 128>(a, s);
   }
   return hipErrorInvalidValue;
+}
+#if PF_GK_HAS(5)
+template hipError_t launch_tn_t<bf16_t>(int, const TNArgs &, hipStream_t);
+template hipError_t launch_tn_reduce_t<bf16_t>(int, const TNArgs &, hipStream_t);
+#endif
+#if PF_GK_HAS(6)
+template hipError_t launch_tn_t<float>(int, const TNArgs &, hipStream_t);
+template hipError_t launch_tn_reduce_t<float>(int, const TNArgs &, hipStream_t);
+#endif
+
+#if PF_GK_HAS(0)
+hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a, hipStream_t s) {
+  const bool dense = a.dense != 0;
+  if (dtype == 0)
+    return b_kn ? launch_nt_tb<bf16_t, true>(blk, G, bm, dense, a, s)
+                : launch_nt_tb<bf16_t, false>(blk, G, bm, dense, a, s);
+  return b_kn ? launch_nt_tb<float, true>(blk, G, bm, dense, a, s)
+              : launch_nt_tb<float, false>(blk, G, bm, dense, a, s);
+}
+
+hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
+                              void *C, int64_t ldc, hipStream_t s) {
+  const int64_t n4 = M * ncols / 4;
+  const int64_t blocks = std::max<int64_t>(1, std::min<int64_t>((n4 + 255) / 256, 4096));
+  if (dtype == 0)
+    launch_kernel(reduce_rows_kernel<bf16_t>,
+                  dim3((unsigned)blocks), dim3(256), s, nsplit, P, M, ncols, (bf16_t *)C, ldc);
+  else
+    launch_kernel(reduce_rows_kernel<float>,
+                  dim3((unsigned)blocks), dim3(256), s, nsplit, P, M, ncols, (float *)C, ldc);
+  return hipGetLastError();
+}
+
+hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s) {
+  return dtype == 0 ? launch_tn_t<bf16_t>(blk, a, s) : launch_tn_t<float>(blk, a, s);
+}
+
+hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s) {
+  return dtype == 0 ? launch_tn_reduce_t<bf16_t>(blk, a, s) : launch_tn_reduce_t<float>(blk, a, s);
 }
 
 hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH, const void *Hpre, void *out, hipStream_t s) {
@@ -1123,5 +1142,6 @@ hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH, const void *Hpr
                   (float *)out);
   return hipGetLastError();
 }
+#endif
 
 }  // namespace pf

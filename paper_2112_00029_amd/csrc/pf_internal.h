@@ -2,8 +2,7 @@
 // Not part of the public ABI (see include/pixelfly.h).
 #pragma once
 
-#include <hip/hip_ext.h>
-#include <hip/hip_runtime.h>
+#include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
 namespace pf {
@@ -16,17 +15,6 @@ struct LaunchEvents {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 LaunchEvents &next_launch_events();
-
-template <typename F, typename... Args>
-inline void launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
-  LaunchEvents &e = next_launch_events();
-  if (e.start) {
-    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e.start, e.stop, 0, args...);
-    e.start = e.stop = nullptr;
-  } else {
-    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
-  }
-}
 
 // Maximum block rows one NT output tile covers, and blocks per side of a TN
 // (weight-gradient) tile.
@@ -171,13 +159,47 @@ hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs 
 // tiles (NTD_TALL) or short K-steps with more workgroups per CU
 // (NTD_SHORT_K).
 enum { NTD_DEFAULT = 0, NTD_TALL = 1, NTD_SHORT_K = 2 };
-hipError_t launch_ntd(int blk, int G, bool b_kn, int variant, const NTArgs &a, hipStream_t s);
+// Per-(block size, B orientation) parts (one object file each).
+template <int BLK, bool BKN>
+hipError_t launch_ntd_bb(int G, int variant, const NTArgs &a, hipStream_t s);
+// Each part is instantiated in its own object only.
+extern template hipError_t launch_ntd_bb<32, false>(int, int, const NTArgs &, hipStream_t);
+extern template hipError_t launch_ntd_bb<32, true>(int, int, const NTArgs &, hipStream_t);
+extern template hipError_t launch_ntd_bb<64, false>(int, int, const NTArgs &, hipStream_t);
+extern template hipError_t launch_ntd_bb<64, true>(int, int, const NTArgs &, hipStream_t);
+extern template hipError_t launch_ntd_bb<128, false>(int, int, const NTArgs &, hipStream_t);
+extern template hipError_t launch_ntd_bb<128, true>(int, int, const NTArgs &, hipStream_t);
+inline hipError_t launch_ntd(int blk, int G, bool b_kn, int variant, const NTArgs &a,
+                             hipStream_t s) {
+  switch (blk) {
+    case 32: return b_kn ? launch_ntd_bb<32, true>(G, variant, a, s) : launch_ntd_bb<32, false>(G, variant, a, s);
+    case 64: return b_kn ? launch_ntd_bb<64, true>(G, variant, a, s) : launch_ntd_bb<64, false>(G, variant, a, s);
+    case 128: return b_kn ? launch_ntd_bb<128, true>(G, variant, a, s) : launch_ntd_bb<128, false>(G, variant, a, s);
+  }
+  return hipErrorInvalidValue;
+}
 // Sum split partials P[nsplit][M][ncols] (fp32) into C (dtype, row stride ldc).
 hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, int64_t ncols,
                               void *C, int64_t ldc, hipStream_t s);
 // The TN kernel, and (a.nsplit > 1) the pass that sums its split partials.
 hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
 hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s);
+// Per-element-type parts of the register-staged kernels (one object file
+// each): T is uint16_t (bf16 storage) or float.
+template <typename T, bool BKN>
+hipError_t launch_nt_tb(int blk, int G, int bm, bool dense, const NTArgs &a, hipStream_t s);
+template <typename T>
+hipError_t launch_tn_t(int blk, const TNArgs &a, hipStream_t s);
+template <typename T>
+hipError_t launch_tn_reduce_t(int blk, const TNArgs &a, hipStream_t s);
+extern template hipError_t launch_nt_tb<uint16_t, false>(int, int, int, bool, const NTArgs &, hipStream_t);
+extern template hipError_t launch_nt_tb<uint16_t, true>(int, int, int, bool, const NTArgs &, hipStream_t);
+extern template hipError_t launch_nt_tb<float, false>(int, int, int, bool, const NTArgs &, hipStream_t);
+extern template hipError_t launch_nt_tb<float, true>(int, int, int, bool, const NTArgs &, hipStream_t);
+extern template hipError_t launch_tn_t<uint16_t>(int, const TNArgs &, hipStream_t);
+extern template hipError_t launch_tn_t<float>(int, const TNArgs &, hipStream_t);
+extern template hipError_t launch_tn_reduce_t<uint16_t>(int, const TNArgs &, hipStream_t);
+extern template hipError_t launch_tn_reduce_t<float>(int, const TNArgs &, hipStream_t);
 int tn_items_total(const TNArgs &a, int blk);
 hipError_t launch_skinny(bool b_kn, const SkinnyArgs &a, hipStream_t s);
 // dgamma of the mixing weight: partial sums of <S, T_lr> (n elements,

@@ -25,7 +25,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "pf_internal.h"
+#include "pf_launch.h"
 
 namespace pf {
 namespace {
@@ -91,9 +91,12 @@ __global__ __launch_bounds__(64 * NW) void skinny_kernel(SkinnyArgs a) {
   const int ksteps = (a.K + SK_BK - 1) / SK_BK;
   const int h = lane >> 5, r32 = lane & 31;
 
-  // A: rows past M read as zero (range); a k slice past K is pointed out of
-  // range.  Step s adds s * 128 bytes through the scalar offset.
-  const rsrc_t rA = make_rsrc((const bf16_t *)a.A + t0 * a.lda, (a.M - t0) * a.lda * 2);
+  // A: the workgroup's 32 rows only, rows past M read as zero (range); a k
+  // slice past K is pointed out of range (the host keeps 32 rows of A and
+  // all of B below that offset).  Step s adds s * 128 bytes through the
+  // scalar offset.
+  const int64_t a_rows = a.M - t0 < SK_TM ? a.M - t0 : SK_TM;
+  const rsrc_t rA = make_rsrc((const bf16_t *)a.A + t0 * a.lda, a_rows * a.lda * 2);
   const uint32_t voffA = (uint32_t)(r32 * a.lda * 2 + h * 16);
   const uint32_t OUT = 0x7ffffff0u;
   rsrc_t rB;

@@ -64,6 +64,15 @@ class pf_layout_info(ctypes.Structure):
                 ("row_idx", ctypes.POINTER(_i32)), ("tperm", ctypes.POINTER(_i32))]
 
 
+class pf_linear_plan(ctypes.Structure):
+    _fields_ = [(n, _i32) for n in (
+        "lowrank_t_kernel", "lowrank_t_split", "lowrank_t_tile_m", "lowrank_t_tile_n",
+        "lowrank_s_kernel", "lowrank_s_split", "lowrank_s_tile_m", "lowrank_s_tile_n",
+        "fwd_tile_m", "fwd_tile_n", "fwd_direct_lds", "bwd_tile_m", "bwd_tile_n",
+        "bwd_direct_lds", "tn_items", "tn_split")] + [("tn_chunk", _i64),
+                                                       ("workspace_bytes", ctypes.c_uint64)]
+
+
 _SIGS = {
     "pf_layout_create": (_i32, [_i64, _i64, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_create_from_mask": (_i32, [_i32, _i32, _i32, _p, ctypes.POINTER(_p)]),
@@ -75,6 +84,7 @@ _SIGS = {
     "pf_layout_info_get": (_i32, [_p, ctypes.POINTER(pf_layout_info)]),
     "pf_layout_check": (_i32, [_p]),
     "pf_layout_plan_get": (_i32, [_p, ctypes.POINTER(_i32), _i32]),
+    "pf_linear_plan_get": (_i32, [_p, _i32, _i64, _i32, ctypes.POINTER(pf_linear_plan)]),
     "pf_layout_upload": (_i32, [_p, _p]),
     "pf_layout_destroy": (None, [_p]),
     "pf_workspace_bytes": (_sz, [_p, _i64, _i32, _i32]),
@@ -242,6 +252,13 @@ def pf_layout_plan_get(layout: Layout) -> dict:
     keys = ["G_fwd", "fwd_tiles", "G_bwd", "bwd_tiles", "tn_items", "tn_kept",
             "G_fwd_wide", "fwd_tiles_wide", "G_bwd_wide", "bwd_tiles_wide"]
     return dict(zip(keys, list(st)))
+
+
+def pf_linear_plan_get(layout: Layout, dtype, T: int, r: int) -> dict:
+    """The kernels and splits a linear step of T tokens at rank r runs."""
+    p = pf_linear_plan()
+    _check(_lib.pf_linear_plan_get(layout.handle, _dt(dtype), T, r, ctypes.byref(p)))
+    return {n: getattr(p, n) for n, _t in pf_linear_plan._fields_}
 
 
 def pf_layout_upload(layout: Layout, stream=None) -> None:

@@ -13,9 +13,15 @@ STREAMS = {"X": 1, "W": 2, "U": 3, "V": 4, "dY": 5, "W2": 6, "U2": 7, "V2": 8,
 def bf16_bits_from_f32(a: np.ndarray) -> np.ndarray:
     """float32 -> bfloat16 bit patterns (uint16), round to nearest even."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    bias = ((u >> 16) & 1) + 0x7FFF
-    return ((u + bias) >> 16).astype(np.uint16)
+    u = a.reshape(-1).view(np.uint32)
+    # u + 0x7FFF + (bit 16 of u), in 32-bit arithmetic: a sum past 2^32
+    # (negative NaNs only) wraps to below 0x8000, and so gives the same top
+    # half (0) as the exact sum truncated to 16 bits.
+    r = (u >> 16) & 1
+    r += 0x7FFF
+    r += u
+    r >>= 16
+    return r.astype(np.uint16).reshape(a.shape)
 
 
 def f32_from_bf16_bits(h: np.ndarray) -> np.ndarray:
@@ -24,20 +30,22 @@ def f32_from_bf16_bits(h: np.ndarray) -> np.ndarray:
     return (h.astype(np.uint32) << 16).view(np.float32)
 
 
-def draw(shape, std: float, seed: int, stream: int, dtype: str):
+def draw(shape, std: float, seed: int, stream: int, dtype: str, values: bool = True):
     """One N(0, std^2) tensor.
 
     Returns ``(values_f64, raw)`` where ``raw`` is what the GPU consumes:
     uint16 bf16 bits for ``dtype == "bf16"``, float32 for ``"fp32"``; and
-    ``values_f64`` is exactly that tensor upcast to float64.
+    ``values_f64`` is exactly that tensor upcast to float64 (None when
+    ``values`` is False).
     """
     rng = np.random.default_rng([seed, stream])
-    a = (rng.standard_normal(size=shape, dtype=np.float32) * np.float32(std))
+    a = rng.standard_normal(size=shape, dtype=np.float32)
+    a *= np.float32(std)
     if dtype == "bf16":
         raw = bf16_bits_from_f32(a)
-        return f32_from_bf16_bits(raw).astype(np.float64), raw
+        return (f32_from_bf16_bits(raw).astype(np.float64) if values else None), raw
     if dtype == "fp32":
-        return a.astype(np.float64), a
+        return (a.astype(np.float64) if values else None), a
     raise ValueError(dtype)
 
 

@@ -6,7 +6,7 @@ import pytest
 import synth
 from oracle import attention as oa
 from oracle import mask as om
-from tests._gpu_util import TOL, empty, rel_fro, to_dev, to_host, torch_cuda
+from tests._gpu_util import check_close, empty, to_dev, to_host, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -37,15 +37,17 @@ def _run(B, H, S, ms, heads, seed=0, check_bwd=True, g=0):
     Og, lg = to_host(O), lse.cpu().numpy().astype(np.float64)
     dQg, dKg, dVg = to_host(dQ), to_host(dK), to_host(dV)
     for (x, y) in heads:
+        print(f"  head {(x, y)}", flush=True)
         o, l, _ = oa.forward_head(Q[x, y], K[x, y], V[x, y], Mel, scale)
-        errs = {"O": rel_fro(Og[x, y], o), "lse": rel_fro(lg[x, y], l)}
+        # Each query (key) row against at least the RMS row norm: gradient
+        # rows of keys that receive little attention are small next to the
+        # rounding of the probabilities that feed them.
+        pairs = [("O", Og[x, y], o), ("lse", lg[x, y], l)]
         if check_bwd:
             rq, rk, rv = oa.backward_head(Q[x, y], K[x, y], V[x, y], Mel, scale, dO[x, y])
-            errs.update(dQ=rel_fro(dQg[x, y], rq), dK=rel_fro(dKg[x, y], rk),
-                        dV=rel_fro(dVg[x, y], rv))
-        print(f"  head {(x, y)}: " + " ".join(f"{k}={e:.2e}" for k, e in errs.items()), flush=True)
-        for kk, e in errs.items():
-            assert e <= TOL["bf16"], (kk, (x, y), e)
+            pairs += [("dQ", dQg[x, y], rq), ("dK", dKg[x, y], rk), ("dV", dVg[x, y], rv)]
+        for kk, gv, rv_ in pairs:
+            check_close(kk, gv, rv_, "bf16", row_floor=1.0)
 
 
 def test_attention_full_sequence_sampled_heads():

@@ -11,7 +11,8 @@ import pytest
 import synth
 from oracle import linear as ol
 from oracle import mask as om
-from tests._gpu_util import TOL, bf16_round, empty, rel_fro, to_dev, to_host, torch_cuda
+from tests._gpu_util import (TOL, bf16_round, check_close, empty, rel_fro, to_dev, to_host,
+                             torch_cuda)
 
 pytestmark = pytest.mark.gpu
 
@@ -39,14 +40,15 @@ def _inputs(n_out, n_in, b, ms, T, r, dtype, seed=0, std=(0.02, 0.02, 0.02, 0.02
                 raw=dict(X=Xr, W=Wr, U=Ur, V=Vr, dY=dYr))
 
 
-def _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp):
-    """fwd, bwd-data, bwd-weight through the C ABI; returns float64 outputs."""
+def _run_gpu_dev(n_out, n_in, b, ms, T, r, dtype, raw, timing=False):
+    """fwd, bwd-data, bwd-weight through the C ABI; returns the device
+    outputs, the layout and (timing) the launches per kernel class."""
     torch = torch_cuda()
     from paper_2112_00029_amd import pixelfly as pf
     print(f"[linear] n_out={n_out} n_in={n_in} b={b} ms={ms} T={T} r={r} {dtype}", flush=True)
     L = pf.pf_layout_create(n_out, n_in, b, ms)
     pf.pf_layout_upload(L)
-    d = {k: to_dev(v) for k, v in inp["raw"].items()}
+    d = {k: to_dev(v) for k, v in raw.items()}
     Y = empty((T, n_out), dtype)
     dX = empty((T, n_in), dtype)
     dW = empty(tuple(d["W"].shape), dtype)
@@ -58,18 +60,29 @@ def _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp):
     V = d["V"] if r else None
     ws_bytes = pf.pf_workspace_bytes(L, T, r, dtype)
     ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device="cuda")
-    pf.pf_linear_fwd(L, dtype, T, r, d["X"], d["W"], U, V, Y, Tl if r else None,
-                     workspace=ws, ws_bytes=ws_bytes)
-    pf.pf_linear_bwd_data(L, dtype, T, r, d["dY"], d["W"], U, V, S if r else None, dX,
-                          workspace=ws, ws_bytes=ws_bytes)
-    pf.pf_linear_bwd_weight(L, dtype, T, r, d["dY"], d["X"], Tl if r else None,
-                            S if r else None, dW, dU if r else None, dV if r else None,
-                            ws, ws_bytes)
-    torch.cuda.synchronize()
-    out = dict(Y=to_host(Y), dX=to_host(dX), dW=to_host(dW))
+    if timing:
+        pf.pf_timing_begin(8)
+    try:
+        pf.pf_linear_fwd(L, dtype, T, r, d["X"], d["W"], U, V, Y, Tl if r else None,
+                         workspace=ws, ws_bytes=ws_bytes)
+        pf.pf_linear_bwd_data(L, dtype, T, r, d["dY"], d["W"], U, V, S if r else None, dX,
+                              workspace=ws, ws_bytes=ws_bytes)
+        pf.pf_linear_bwd_weight(L, dtype, T, r, d["dY"], d["X"], Tl if r else None,
+                                S if r else None, dW, dU if r else None, dV if r else None,
+                                ws, ws_bytes)
+        torch.cuda.synchronize()
+    finally:
+        kt = pf.pf_timing_end() if timing else None
+    out = dict(Y=Y, dX=dX, dW=dW)
     if r:
-        out.update(T_lr=to_host(Tl), S=to_host(S), dU=to_host(dU), dV=to_host(dV))
-    return out, L
+        out.update(T_lr=Tl, S=S, dU=dU, dV=dV)
+    return out, L, kt
+
+
+def _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp):
+    """As _run_gpu_dev, outputs read back as float64 arrays."""
+    out, L, _kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, dtype, inp["raw"])
+    return {k: to_host(v) for k, v in out.items()}, L
 
 
 def _oracle(inp, r, b):
@@ -123,11 +136,8 @@ def test_linear_parity(n_out, n_in, b, ms, T, r, dtype):
     got, _ = _run_gpu(n_out, n_in, b, ms, T, r, dtype, inp)
     ref = _oracle(inp, r, b)
     ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
-    tol = TOL[dtype]
     for k in ["Y", "dX", "dW"] + (["T_lr", "S", "dU", "dV"] if r else []):
-        e = rel_fro(got[k], ref[k])
-        print(f"  {k}: rel_fro={e:.3e}", flush=True)
-        assert e <= tol, (k, e)
+        check_close(k, got[k], ref[k], dtype)
 
 
 def test_fp32_integer_inputs_bit_exact():
@@ -156,19 +166,28 @@ def test_bf16_integer_inputs_bit_exact(b):
         assert np.array_equal(got[k], bf16_round(ref[k])), k
 
 
-def test_mlp_pair_gelu():
+@pytest.mark.parametrize("T", [390, 8192], ids=["T390", "T8192_full"])
+def test_mlp_pair_gelu(T):
     """Two layers 1024 -> 4096 -> GELU -> 1024 (b = 64, stride 16, r = 128)
     with the GELU epilogues: forward keeps the pre-activation, backward-data
-    of the second layer applies gelu'(pre-activation)."""
+    of the second layer applies gelu'(pre-activation).  At the workload's
+    8192 tokens the GELU epilogues run on 256 x 256 tiles and the rank-r
+    products on the split-K tile kernel."""
     torch = torch_cuda()
     from paper_2112_00029_amd import pixelfly as pf
-    T, K, N, b, ms, r = 390, 1024, 4096, 64, 16, 128
+    K, N, b, ms, r = 1024, 4096, 64, 16, 128
     dtype = "bf16"
     l1 = _inputs(N, K, b, ms, T, r, dtype, seed=0)
     l2 = _inputs(K, N, b, ms, T, r, dtype, seed=1)
-    print("[mlp_pair] T=390", flush=True)
+    print(f"[mlp_pair] T={T}", flush=True)
     L1 = pf.pf_layout_create(N, K, b, ms)
     L2 = pf.pf_layout_create(K, N, b, ms)
+    if T == 8192:
+        p1, p2 = pf.pf_linear_plan_get(L1, dtype, T, r), pf.pf_linear_plan_get(L2, dtype, T, r)
+        assert (p1["fwd_tile_m"], p1["fwd_tile_n"]) == (256, 256), p1  # GELU forward, wide
+        assert (p2["bwd_tile_m"], p2["bwd_tile_n"]) == (256, 256), p2  # GELU backward, wide
+        assert p1["lowrank_t_kernel"] == 2 and p1["lowrank_s_split"] > 1, p1
+        assert p2["lowrank_t_kernel"] == 2 and p2["lowrank_t_split"] > 1, p2
     pf.pf_layout_upload(L1)
     pf.pf_layout_upload(L2)
     X = to_dev(l1["raw"]["X"])
@@ -211,9 +230,7 @@ def test_mlp_pair_gelu():
         "dU1": (dU1, ref_b["l1"]["dU"]), "dV1": (dV1, ref_b["l1"]["dV"]),
     }
     for k, (g, rf) in checks.items():
-        e = rel_fro(to_host(g), rf)
-        print(f"  {k}: rel_fro={e:.3e}", flush=True)
-        assert e <= TOL[dtype], (k, e)
+        check_close(k, to_host(g), rf, dtype)
 
 
 def test_repeat_calls_are_deterministic():
@@ -244,3 +261,102 @@ def test_kernel_timing_hook_counts_launches():
         assert kt[c][0] == 1 and kt[c][1] > 0, (c, kt[c])
     for c in ("gelu_bwd", "attn_fwd", "attn_bwd_dq", "attn_bwd_dkv", "dense"):
         assert kt[c][0] == 0, (c, kt[c])
+
+
+# ---------------------------------------------------------------------------
+# The 16384 x 4096 layer (4096 -> 16384, r = 256, strides < 32 blocks) on the
+# paths its full size runs: split-K rank-r products with the bf16 row
+# reduction, the weight gradient's many-items token split, wide and tall
+# tiles.
+# ---------------------------------------------------------------------------
+LARGE = dict(n_out=16384, n_in=4096, ms=32, r=256)
+
+
+def _reductions(kt):
+    return kt["reduce"][0]
+
+
+@pytest.mark.parametrize("b", [128, 64, 32])
+def test_large_layer_T4096_all_outputs(b):
+    """Every output element against the oracle at 4096 tokens: T_lr and S run
+    on the tile kernel with an 8-way K split and the bf16 row reduction, the
+    weight gradient on its many-items token split."""
+    from paper_2112_00029_amd import pixelfly as pf
+    n_out, n_in, ms, r, T = LARGE["n_out"], LARGE["n_in"], LARGE["ms"], LARGE["r"], 4096
+    plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
+    print(f"[plan b={b} T={T}] {plan}", flush=True)
+    assert plan["lowrank_t_kernel"] == 2 and plan["lowrank_t_split"] > 1, plan
+    assert plan["lowrank_s_kernel"] == 2 and plan["lowrank_s_split"] > 1, plan
+    assert plan["tn_items"] >= 512 and plan["tn_split"] > 1, plan
+    inp = _inputs(n_out, n_in, b, ms, T, r, "bf16")
+    out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", inp["raw"], timing=True)
+    assert _reductions(kt) == 3, kt  # T_lr, S and the weight-gradient splits ran
+    got = {k: to_host(v) for k, v in out.items()}
+    ref = _oracle(inp, r, b)
+    ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
+    for k in ["Y", "dX", "dW", "T_lr", "S", "dU", "dV"]:
+        check_close(k, got[k], ref[k], "bf16")
+
+
+@pytest.fixture(scope="module")
+def large_full_inputs():
+    """Seeded inputs of the full 16384-token layer shared by every block size
+    (X, U, V, dY do not depend on b)."""
+    T, n_out, n_in, r = 16384, LARGE["n_out"], LARGE["n_in"], LARGE["r"]
+    X, Xr = synth.draw((T, n_in), 0.02, 0, 1, "bf16")
+    U, Ur = synth.draw((n_out, r), 0.02, 0, 3, "bf16")
+    V, Vr = synth.draw((r, n_in), 0.02, 0, 4, "bf16")
+    dY, dYr = synth.draw((T, n_out), 0.02, 0, 5, "bf16")
+    return dict(T=T, X=X, U=U, V=V, dY=dY, raw=dict(X=Xr, U=Ur, V=Vr, dY=dYr))
+
+
+@pytest.mark.parametrize("b", [128, 64, 32])
+def test_large_layer_full_size_sampled(large_full_inputs, b):
+    """The 16384-token workload in the launch configuration the benchmark
+    times.  The oracle computes sampled outputs one by one: token rows of Y,
+    dX, T_lr and S (row t depends on row t of X or dY only), kept blocks of
+    dW (block (i, j) is dY[:, i]^T X[:, j] by the gradient lemma), and all
+    of S, dU and dV."""
+    inp = large_full_inputs
+    n_out, n_in, ms, r, T = LARGE["n_out"], LARGE["n_in"], LARGE["ms"], LARGE["r"], inp["T"]
+    from paper_2112_00029_amd import pixelfly as pf
+    plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
+    print(f"[plan b={b} T={T}] {plan}", flush=True)
+    assert plan["lowrank_t_kernel"] == 2 and plan["lowrank_s_kernel"] == 2, plan
+    M, (row_ptr, col_idx, *_x) = om.layout(n_out, n_in, b, ms)
+    nnzb = int(M.sum())
+    W, Wr = synth.draw((nnzb, b, b), 0.02, 0, 2, "bf16")
+    raw = dict(inp["raw"], W=Wr)
+    out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", raw, timing=True)
+    splits = sum(int(plan[k] > 1) for k in ("lowrank_t_split", "lowrank_s_split", "tn_split"))
+    assert _reductions(kt) == splits, (kt, plan)
+
+    rng = np.random.default_rng([b, 77])
+    edges = [0, 1, 127, 128, 255, 256, 511, 512, T // 2 - 1, T // 2, T - 512, T - 1]
+    rows = np.unique(np.concatenate([edges, rng.integers(0, T, 20)]))
+    Wd = ol.unpack(W, row_ptr, col_idx, n_out // b, n_in // b, b)
+    Mel = om.element_mask(M, b)
+    X, U, V, dY = inp["X"], inp["U"], inp["V"], inp["dY"]
+
+    Y_ref, Tl_ref = ol.forward(X[rows], Wd, U, V)
+    g_rows = ol.backward(X[rows], Wd, Mel, dY[rows], U, V)
+    sel = lambda t: to_host(t[torch_cuda().as_tensor(rows, device="cuda")])
+    check_close("Y[rows]", sel(out["Y"]), Y_ref, "bf16")
+    check_close("T_lr[rows]", sel(out["T_lr"]), Tl_ref, "bf16")
+    check_close("dX[rows]", sel(out["dX"]), g_rows["dX"], "bf16")
+
+    # Kept blocks of dW: first and last of the CSR order and random ones.
+    blks = np.unique(np.concatenate([[0, nnzb - 1], rng.integers(0, nnzb, 22)]))
+    dW_got = to_host(out["dW"][torch_cuda().as_tensor(blks, device="cuda")])
+    blk_row = np.searchsorted(row_ptr, blks, side="right") - 1
+    dW_ref = np.empty((len(blks), b, b))
+    for q, (p, i) in enumerate(zip(blks, blk_row)):
+        j = col_idx[p]
+        I, J = slice(i * b, (i + 1) * b), slice(j * b, (j + 1) * b)
+        dW_ref[q] = ol.backward(X[:, J], Wd[I, J], Mel[I, J], dY[:, I])["dW"]
+    check_close("dW[blocks]", dW_got, dW_ref, "bf16")
+
+    # All of S, dU and dV (the low-rank gradients need no dense weight).
+    lr = ol.lowrank_grads(X, dY, U, V)
+    for k in ("S", "dU", "dV"):
+        check_close(k, to_host(out[k]), lr[k], "bf16")

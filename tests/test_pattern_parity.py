@@ -10,7 +10,7 @@ import pytest
 import synth
 from oracle import linear as ol
 from oracle import mask as om
-from tests._gpu_util import TOL, empty, rel_fro, to_dev, to_host, torch_cuda
+from tests._gpu_util import TOL, check_close, empty, rel_fro, to_dev, to_host, torch_cuda
 
 pytestmark = pytest.mark.gpu
 
@@ -45,9 +45,8 @@ def test_cover_layout_parity(n, p, d, T):
            "dW": ol.pack((dY.T @ X) * C, row_ptr, col_idx, n // b, b)}
     got = {"Y": to_host(Y), "dX": to_host(dX), "dW": to_host(dW)}
     for k in ref:
-        e = rel_fro(got[k], ref[k])
-        print(f"  {k}: rel_fro={e:.3e}  cover density {C.mean():.4f}", flush=True)
-        assert e <= TOL["bf16"], (k, e)
+        print(f"  cover density {C.mean():.4f}", flush=True)
+        check_close(k, got[k], ref[k], "bf16")
 
 
 @pytest.mark.parametrize("b,T,r", [(32, 300, 32), (64, 520, 64)])
@@ -91,10 +90,7 @@ def test_empty_block_columns_with_lowrank(b, T, r):
     got = {"Y": to_host(Y), "T_lr": to_host(Tl), "S": to_host(S), "dX": to_host(dX),
            "dW": to_host(dW), "dU": to_host(dU), "dV": to_host(dV)}
     for k in ref:
-        e = rel_fro(got[k], ref[k])
-        print(f"  {k}: rel_fro={e:.3e}", flush=True)
-        assert e <= TOL["bf16"], (k, e)
+        check_close(k, got[k], ref[k], "bf16")
     # the empty columns of dX hold only the low-rank term
     cols = np.r_[0:b, (nb - 1) * b:n]
-    e = rel_fro(got["dX"][:, cols], (g["S"] @ V)[:, cols])
-    assert e <= TOL["bf16"], ("dX empty columns", e)
+    check_close("dX empty columns", got["dX"][:, cols], (g["S"] @ V)[:, cols], "bf16")
