@@ -374,6 +374,24 @@ pf_status pf_attn_bwd(const pf_layout *layout, int32_t B, int32_t H,
 size_t pf_attn_workspace_bytes(int32_t B, int32_t H, int32_t Sq);
 
 /*
+ * pf_attn_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops that
+ * forbid allocation).  Same arguments, results and errors as pf_attn_bwd
+ * minus the workspace; it allocates nothing.  The row terms delta live in a
+ * library-owned device array of 2^22 floats (16 MiB) per GPU, held until the
+ * process ends: calls with B*H*Sq above 2^22 fail with UNSUPPORTED.  Every
+ * call on a GPU uses that GPU's one array, so calls that may overlap on one
+ * GPU (other streams, other threads) race and must be serialised by the
+ * caller.  The array's device address is looked up on the first call on
+ * each device.
+ */
+pf_status pf_attn_bwd_noalloc(const pf_layout *layout, int32_t B, int32_t H,
+                              int32_t Sq, int32_t d, float scale, const void *Q,
+                              const void *K, const void *V, const void *O,
+                              const float *lse, const void *dO, void *dQ,
+                              void *dK, void *dV, void *stream);
+
+/*
  * Dense comparator GEMM built from the same MFMA tiles as the sparse
  * kernels (the speedup baseline: an equally shaped dense layer):
  *   PF_OP_NT: C[M][N] = A[M][K] . B[N][K]^T   (forward,  X W^T)

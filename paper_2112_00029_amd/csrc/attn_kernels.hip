@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "pf_launch.h"
 
 namespace pf {
@@ -604,6 +606,34 @@ hipError_t launch_attn_bwd_dq(const AttnArgs &a, int part, hipStream_t s) {
 
 hipError_t launch_attn_bwd_dkv(const AttnArgs &a, int part, hipStream_t s) {
   return attn_launch(attn_bwd_dkv_kernel<1>, attn_bwd_dkv_kernel<2>, 2, a, part, s);
+}
+
+// Scratch of the allocation-free attention backward: the row terms delta,
+// one float per query row of the call (kAttnScratchRows at most).  Each GPU
+// the library runs on holds its own copy until the process ends.  In host
+// code `scratch` names a host-side stand-in, not device memory: only the
+// address attn_scratch returns may reach a kernel.
+static __device__ __align__(256) float scratch[kAttnScratchRows];
+
+hipError_t attn_scratch(float **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    // Once per device, with that device current: its copy of the array.
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = (float *)addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace pf

@@ -1249,10 +1249,14 @@ size_t pf_attn_workspace_bytes(int32_t B, int32_t H, int32_t Sq) {
   return ((size_t)B * H * Sq * sizeof(float) + 255) / 256 * 256;
 }
 
-pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d, float scale,
-                      const void *Q, const void *K, const void *V, const void *O, const float *lse,
-                      const void *dO, void *dQ, void *dK, void *dV, void *workspace, size_t ws_bytes,
-                      void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of both attention backward calls (before any enqueue).
+pf_status attn_bwd_check(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d,
+                         const void *Q, const void *K, const void *V, const void *O,
+                         const float *lse, const void *dO, void *dQ, void *dK, void *dV) {
   pf_status st = attn_check(L, B, H, Sq, d);
   if (st != PF_OK) return st;
   if ((st = need_ptr(Q, "Q")) != PF_OK || (st = need_ptr(K, "K")) != PF_OK ||
@@ -1261,23 +1265,27 @@ pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
       (st = need_ptr(dQ, "dQ")) != PF_OK || (st = need_ptr(dK, "dK")) != PF_OK ||
       (st = need_ptr(dV, "dV")) != PF_OK)
     return st;
-  if (ws_bytes < pf_attn_workspace_bytes(B, H, Sq))
-    return fail(PF_ERR_WORKSPACE, "workspace too small");
-  if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
-  if ((st = check_state(L)) != PF_OK) return st;
+  return PF_OK;
+}
+
+// dQ (with delta = rowsum(dO o O) into `delta`, B*H*Sq floats), then dK, dV.
+pf_status attn_bwd_enqueue(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, float scale,
+                           const void *Q, const void *K, const void *V, const void *O,
+                           const float *lse, const void *dO, void *dQ, void *dK, void *dV,
+                           float *delta, hipStream_t s) {
   pf::AttnArgs a{};
   a.Q = Q; a.K = K; a.V = V; a.O = O; a.dO = dO;
   a.dQ = dQ; a.dK = dK; a.dV = dV;
-  a.lse_in = lse; a.delta = (float *)workspace;
+  a.lse_in = lse; a.delta = delta;
   a.BH = B * H; a.S = Sq; a.nbq = Sq / 64; a.scale = scale;
   a.nlong = L->global_blocks;
   a.row_ptr = L->d_row_ptr; a.col_idx = L->d_col_idx;
   a.col_ptr = L->d_col_ptr; a.row_idx = L->d_row_idx;
-  hipStream_t s = (hipStream_t)stream;
   // Parts: 0 (all rows) without global stripes, else 1 (the stripes'
   // long rows / columns, grouped kernels) then 2 (the rest).
   const int parts[2] = {a.nlong > 0 ? 1 : 0, 2};
   const int nparts = a.nlong > 0 && a.nlong < a.nbq ? 2 : 1;
+  pf_status st;
   for (int i = 0; i < nparts; ++i) {
     Timed t(PF_KERNEL_ATTN_BWD_DQ, s);
     if ((st = hip_status(pf::launch_attn_bwd_dq(a, parts[i], s), "attention dQ kernel")) != PF_OK)
@@ -1289,6 +1297,43 @@ pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int3
       return st;
   }
   return PF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pf_status pf_attn_bwd(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d, float scale,
+                      const void *Q, const void *K, const void *V, const void *O, const float *lse,
+                      const void *dO, void *dQ, void *dK, void *dV, void *workspace, size_t ws_bytes,
+                      void *stream) {
+  pf_status st = attn_bwd_check(L, B, H, Sq, d, Q, K, V, O, lse, dO, dQ, dK, dV);
+  if (st != PF_OK) return st;
+  if (ws_bytes < pf_attn_workspace_bytes(B, H, Sq))
+    return fail(PF_ERR_WORKSPACE, "workspace too small");
+  if ((st = need_ptr(workspace, "workspace")) != PF_OK) return st;
+  if ((st = check_state(L)) != PF_OK) return st;
+  return attn_bwd_enqueue(L, B, H, Sq, scale, Q, K, V, O, lse, dO, dQ, dK, dV,
+                          (float *)workspace, (hipStream_t)stream);
+}
+
+pf_status pf_attn_bwd_noalloc(const pf_layout *L, int32_t B, int32_t H, int32_t Sq, int32_t d,
+                              float scale, const void *Q, const void *K, const void *V,
+                              const void *O, const float *lse, const void *dO, void *dQ, void *dK,
+                              void *dV, void *stream) {
+  pf_status st = attn_bwd_check(L, B, H, Sq, d, Q, K, V, O, lse, dO, dQ, dK, dV);
+  if (st != PF_OK) return st;
+  const int64_t rows = (int64_t)B * H * Sq;
+  if (rows > pf::kAttnScratchRows)
+    return fail(PF_ERR_UNSUPPORTED, "B * H * Sq = " + std::to_string(rows) +
+                                        " query rows exceed the allocation-free scratch of " +
+                                        std::to_string(pf::kAttnScratchRows) +
+                                        " rows; use pf_attn_bwd with a workspace");
+  if ((st = check_state(L)) != PF_OK) return st;
+  float *delta = nullptr;
+  if ((st = hip_status(pf::attn_scratch(&delta), "attention scratch lookup")) != PF_OK) return st;
+  return attn_bwd_enqueue(L, B, H, Sq, scale, Q, K, V, O, lse, dO, dQ, dK, dV, delta,
+                          (hipStream_t)stream);
 }
 
 size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K) {

@@ -218,5 +218,11 @@ hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
 hipError_t launch_attn_fwd(const AttnArgs &a, int part, hipStream_t s);
 hipError_t launch_attn_bwd_dq(const AttnArgs &a, int part, hipStream_t s);
 hipError_t launch_attn_bwd_dkv(const AttnArgs &a, int part, hipStream_t s);
+// The allocation-free attention backward keeps its row terms in a
+// file-scope device array of kAttnScratchRows floats (16 MiB per GPU);
+// attn_scratch gives this device's address of it (looked up on the first
+// call on each device).
+constexpr int64_t kAttnScratchRows = (int64_t)1 << 22;
+hipError_t attn_scratch(float **ptr);
 
 }  // namespace pf

@@ -103,6 +103,8 @@ _SIGS = {
     "pf_attn_bwd": (_i32, [_p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p, _p,
                            _p, _p, _sz, _p]),
     "pf_attn_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "pf_attn_bwd_noalloc": (_i32, [_p, _i32, _i32, _i32, _i32, _f32, _p, _p, _p, _p, _p, _p, _p,
+                                   _p, _p, _p]),
     "pf_dense_gemm": (_i32, [_i32, _i32, _i64, _i64, _i64, _p, _p, _p, _p, _sz, _p]),
     "pf_dense_workspace_bytes": (_sz, [_i32, _i32, _i64, _i64, _i64]),
     "pf_timing_begin": (_i32, [_i32]),
@@ -333,6 +335,13 @@ def pf_attn_bwd(layout, B, H, S, d, scale, Q, K, V, O, lse, dO, dQ, dK, dV, work
     _check(_lib.pf_attn_bwd(layout.handle, B, H, S, d, scale, _ptr(Q), _ptr(K), _ptr(V),
                             _ptr(O), _ptr(lse), _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV),
                             _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def pf_attn_bwd_noalloc(layout, B, H, S, d, scale, Q, K, V, O, lse, dO, dQ, dK, dV,
+                        stream=None) -> None:
+    _check(_lib.pf_attn_bwd_noalloc(layout.handle, B, H, S, d, scale, _ptr(Q), _ptr(K), _ptr(V),
+                                    _ptr(O), _ptr(lse), _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV),
+                                    _stream(stream)))
 
 
 def pf_attn_workspace_bytes(B, H, S) -> int:

@@ -43,5 +43,6 @@ hipError_t launch_gelu_bwd(int, int64_t, const void *, const void *, void *, hip
 hipError_t launch_attn_fwd(const AttnArgs &, int, hipStream_t) { no_kernels("attn_fwd"); }
 hipError_t launch_attn_bwd_dq(const AttnArgs &, int, hipStream_t) { no_kernels("attn_dq"); }
 hipError_t launch_attn_bwd_dkv(const AttnArgs &, int, hipStream_t) { no_kernels("attn_dkv"); }
+hipError_t attn_scratch(float **) { no_kernels("attn_scratch"); }
 
 }  // namespace pf
