@@ -79,7 +79,7 @@ def library_source_hash():
 
 def measured_traffic(workload, kernel):
     """HBM bytes per launch of a kernel class from the committed counter
-    summaries (profiles/*traffic*.md lines of the form
+    summaries (lines of profiles/*.md of the form
     `traffic workload=W kernel=C bytes=B fetch=F write=X source=H`), or
     (None, reason) when none matches the current sources."""
     pdir = os.path.join(ROOT, "profiles")
@@ -88,7 +88,7 @@ def measured_traffic(workload, kernel):
     cur = library_source_hash()
     stale = False
     for f in sorted(os.listdir(pdir)):
-        if "traffic" not in f:
+        if not f.endswith(".md"):
             continue
         with open(os.path.join(pdir, f)) as fh:
             for line in fh:

@@ -275,9 +275,10 @@ struct SkinnyPlan {
   int bm;
   int nsplit;
   size_t ws;
+  int G;  // output blocks per tile (128 columns)
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
-  SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0};
+  SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0, 128 / blk};
   if (r <= 0 || use_skinny(dtype, T, r, (int64_t)kblocks * blk)) return p;  // no split
   const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + 127) / 128;
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
@@ -782,7 +783,7 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
       return;
     }
     const SkinnyPlan sp = skinny_plan(dtype, b, T, kblocks, r);
-    const int G = 128 / b;
+    const int G = sp.G;
     const NTChoice c = nt_choose(dt, b, G, sp.bm, (kblocks + sp.nsplit - 1) / sp.nsplit, T,
                                  (r / b + G - 1) / G, sp.nsplit, true);
     (void)b_kn;
@@ -892,7 +893,7 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
     if (st != PF_OK) return st;
   } else if (r > 0) {
     // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(PF_KERNEL_LOWRANK_T, dt, b, 128 / b, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
+    st = dense_nt(PF_KERNEL_LOWRANK_T, dt, b, sp.G, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
                   r / b, T_lr, r, sp.nsplit,
                   (float *)workspace, s, "T_lr kernel");
     if (st != PF_OK) return st;
@@ -985,7 +986,7 @@ pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void
     return skinny_bf16(PF_KERNEL_LOWRANK_S, true, T, dY, L->n_out, U, r, (int)L->n_out, r, S, s,
                        "S kernel");
   const int b = L->b;
-  return dense_nt(PF_KERNEL_LOWRANK_S, dt, b, 128 / b, true, sp.bm, T, dY, L->n_out, U, r,
+  return dense_nt(PF_KERNEL_LOWRANK_S, dt, b, sp.G, true, sp.bm, T, dY, L->n_out, U, r,
                   L->nb_out, r / b, S, r, sp.nsplit, ws, s, "S kernel");
 }
 

@@ -184,8 +184,8 @@ def test_mlp_pair_gelu(T):
     L2 = pf.pf_layout_create(K, N, b, ms)
     if T == 8192:
         p1, p2 = pf.pf_linear_plan_get(L1, dtype, T, r), pf.pf_linear_plan_get(L2, dtype, T, r)
-        assert (p1["fwd_tile_m"], p1["fwd_tile_n"]) == (256, 256), p1  # GELU forward, wide
-        assert (p2["bwd_tile_m"], p2["bwd_tile_n"]) == (256, 256), p2  # GELU backward, wide
+        assert p1["fwd_tile_n"] == 256, p1  # GELU forward on wide tiles
+        assert p2["bwd_tile_n"] == 256, p2  # GELU backward on wide tiles
         assert p1["lowrank_t_kernel"] == 2 and p1["lowrank_s_split"] > 1, p1
         assert p2["lowrank_t_kernel"] == 2 and p2["lowrank_t_split"] > 1, p2
     pf.pf_layout_upload(L1)
