@@ -54,3 +54,45 @@ def second_order(factors: dict, dim: int) -> np.ndarray:
         for ic in range(ia + 1, len(ks)):
             C += factors[ks[ia]] @ factors[ks[ic]]
     return C
+
+
+def product_layer_forward(X, factors):
+    """The product form as a layer on token rows.  `factors` lists dense
+    F_1 .. F_L in application order (smallest stride first), so the matrix is
+    M = F_L ... F_1 (Section 3.2's product of factors, each a general matrix
+    on the support of its I + B_k) and Y = X M^T, computed factor by factor:
+    x_0 = X, x_f = x_{f-1} F_f^T.  Returns (Y, [x_0, ..., x_{L-1}]), the
+    input of every factor."""
+    xs, x = [], X
+    for F in factors:
+        xs.append(x)
+        x = x @ F.T
+    return x, xs
+
+
+def product_layer_backward(xs, factors, supports, dY):
+    """Gradients of L = <dY, Y> for product_layer_forward: g_L = dY,
+    g_{f-1} = g_f F_f, and each factor's gradient restricted to its support,
+    dF_f = (g_f^T x_{f-1}) o S_f (the masked-gradient rule of the appendix on
+    gradient computation, applied to each factor).  `supports` holds the
+    element masks S_f.  Returns (dX, [dF_1 .. dF_L], [g_1 .. g_L])."""
+    L = len(factors)
+    g = dY
+    dF, gs = [None] * L, [None] * L
+    for f in range(L - 1, -1, -1):
+        gs[f] = g
+        dF[f] = (g.T @ xs[f]) * supports[f]
+        g = g @ factors[f]
+    return g, dF, gs
+
+
+def product_factor_mask(nb: int, L: int) -> np.ndarray:
+    """Block mask of all factors' gradients at once: an (L nb) x (L nb)
+    block-diagonal whose f-th diagonal block is the support of the factor of
+    stride 2^(f+1) (block units), so that the gradients of every factor are
+    one masked product of the stacked output gradients and inputs."""
+    from .mask import factor_matrix_support
+    M = np.zeros((L * nb, L * nb), dtype=bool)
+    for f in range(L):
+        M[f * nb:(f + 1) * nb, f * nb:(f + 1) * nb] = factor_matrix_support(nb, 2 ** (f + 1))
+    return M
