@@ -570,8 +570,19 @@ class Butterfly:
             nz = 2 * (n // b)
             self.fac[k] = dict(L=L, W=dr((nz, b, b), 1.0 / np.sqrt(2 * b), 20 + k), dW=e(nz, b, b),
                                act=e(T, n), g=e(T, n))
+        # The product form in one launch per pass: factors packed [L][nb][2][b][b]
+        # on the stacked layout, factor inputs / output gradients saved [T][L][n].
+        self.prod = {}
+        for ms in self.strides:
+            Lp = pf.pf_layout_create_butterfly(n, b, ms)
+            pf.pf_layout_upload(Lp)
+            nf = ms.bit_length() - 1
+            nz = pf.pf_layout_info_get(Lp)["nnzb"]
+            self.prod[ms] = dict(L=Lp, F=dr((nz, b, b), 1.0 / np.sqrt(2 * b), 40 + ms), dF=e(nz, b, b),
+                                 acts=e(T, nf * n), grads=e(T, nf * n))
         self.wsb = max(pf.pf_workspace_bytes(c["L"], T, 0, "bf16")
-                       for c in list(self.flat.values()) + list(self.fac.values()))
+                       for c in list(self.flat.values()) + list(self.fac.values())
+                       + list(self.prod.values()))
         self.ws = torch.empty(max(self.wsb, 256), dtype=torch.uint8, device="cuda")
         self.nnzb = self.flat[self.strides[-1]]["nnzb"]
 
@@ -601,6 +612,13 @@ class Butterfly:
             pf.pf_linear_bwd_data(c["L"], "bf16", T, 0, g, c["W"], None, None, None, c["g"], **kw)
             g = c["g"]
 
+    def _product_kernel(self, ms):
+        pf, T, c = self.pf, self.wl.T, self.prod[ms]
+        pf.pf_butterfly_fwd(c["L"], T, self.X, c["F"], self.Y, c["acts"])
+        pf.pf_butterfly_bwd_data(c["L"], T, self.dY, c["F"], self.dX, c["grads"])
+        pf.pf_linear_bwd_weight(c["L"], "bf16", T, 0, c["grads"], c["acts"], None, None, c["dF"],
+                                None, None, self.ws, self.wsb)
+
     def call(self, name):
         self._flat(self.strides[-1])
 
@@ -617,11 +635,15 @@ class Butterfly:
         rows = []
         for ms in self.strides:
             tf = timed(self.torch, lambda ms=ms: self._flat(ms), 20, 3)
-            tp = timed(self.torch, lambda ms=ms: self._product(ms), 20, 3)
-            rows.append({"max_stride": ms, "flat_ms": tf, "product_ms": tp,
-                         "product_over_flat": tp / tf,
+            tk = timed(self.torch, lambda ms=ms: self._product_kernel(ms), 20, 3)
+            tc = timed(self.torch, lambda ms=ms: self._product(ms), 20, 3)
+            rows.append({"max_stride": ms, "flat_ms": tf, "product_ms": tk,
+                         "product_over_flat": tk / tf, "product_chain_ms": tc,
                          "factors": len([k for k in self.strides if k <= ms])})
-        return {"flat_vs_product": rows}
+        return {"flat_vs_product": rows,
+                "product_form": "one launch applies every factor (activation tile in LDS) "
+                                "forward and backward-data, plus one launch for all factors' "
+                                "gradients; product_chain_ms runs each factor as its own layer"}
 
     def dense_setup(self):
         torch, wl = self.torch, self.wl

@@ -163,6 +163,47 @@ pf_status pf_layout_create_from_element_mask(int64_t n_out, int64_t n_in, int32_
 pf_status pf_layout_create_factor(int64_t n, int32_t b, int32_t k, pf_layout **out);
 
 /*
+ * Product form of an n x n block butterfly (Section 3.2: the product of
+ * factors F_L ... F_1, each a general matrix on the support of I + B_k,
+ * k = 2, 4, ..., max_stride; appendix on benchmarking the butterfly
+ * multiply), as a layer on token rows: Y = X (F_L ... F_1)^T, smallest
+ * stride applied first.  The layout returned here stacks the factors'
+ * supports on the diagonal of an (L nb) x (L nb) block grid (L = log2
+ * max_stride, nb = n / b): block row f nb + p keeps columns f nb + p and
+ * f nb + (p XOR 2^f).  Its block-CSR order is the packing of the factors:
+ * F (and dF) = [L][nb][2][b][b], factor f's block row p holding its two kept
+ * blocks in ascending column order, element (r, c) of block (p, q) being
+ * F_f[p b + r][q b + c].  Requires b >= 1 dividing n, max_stride a power of
+ * two >= 2 dividing n / b.  Host only.  Errors: INVALID_ARG, NOMEM.
+ */
+pf_status pf_layout_create_butterfly(int64_t n, int32_t b, int32_t max_stride,
+                                     pf_layout **out);
+
+/*
+ * One launch: the whole product on T token rows (bf16; b = 32 and
+ * max_stride <= 32 in this build, else UNSUPPORTED).  Each workgroup holds a
+ * 32-token x (max_stride * 32)-feature tile of the activation in LDS and
+ * applies every factor to it in place.
+ *   pf_butterfly_fwd:       Y = X (F_L ... F_1)^T; with acts non-NULL it also
+ *                           writes the input of every factor, acts[t][f][:] =
+ *                           x_f (x_0 = X, x_f = x_{f-1} F_{f+1}^T), T x (L n).
+ *   pf_butterfly_bwd_data:  dX = dY F_L ... F_1; with grads non-NULL it also
+ *                           writes the gradient at every factor's output,
+ *                           grads[t][f][:] = g_{f+1} (g_L = dY, g_f = g_{f+1} F_{f+1}).
+ * The factors' gradients, dF_f = (g_f^T x_{f-1}) on the support of F_f, are
+ * one masked product on the same layout:
+ *   pf_linear_bwd_weight(layout, PF_BF16, T, 0, grads, acts, NULL, NULL, dF,
+ *                        NULL, NULL, workspace, ws_bytes, stream)
+ * (that call needs pf_layout_upload; these two do not).  X, Y, dY, dX are
+ * T x n row-major; pointers 16-byte aligned.  Errors: INVALID_ARG (not a
+ * butterfly layout, bad sizes or pointers), UNSUPPORTED, HIP.
+ */
+pf_status pf_butterfly_fwd(const pf_layout *layout, int64_t T, const void *X,
+                           const void *F, void *Y, void *acts, void *stream);
+pf_status pf_butterfly_bwd_data(const pf_layout *layout, int64_t T, const void *dY,
+                                const void *F, void *dX, void *grads, void *stream);
+
+/*
  * Mask selection for one layer from a compute budget (Section 3.3, step 2):
  * a share lowrank_share of the budget (the paper's rule of thumb: one
  * quarter to one third) goes to the low-rank part, whose rank is the largest
@@ -436,7 +477,8 @@ typedef enum {
   PF_KERNEL_ATTN_BWD_DQ = 8,    /* dQ (and the row terms delta) */
   PF_KERNEL_ATTN_BWD_DKV = 9,   /* dK, dV */
   PF_KERNEL_DENSE = 10,         /* dense comparator GEMM */
-  PF_KERNEL_COUNT = 11
+  PF_KERNEL_BUTTERFLY = 11,     /* product-form butterfly (forward, backward-data) */
+  PF_KERNEL_COUNT = 12
 } pf_kernel_class;
 
 pf_status pf_timing_begin(int32_t max_launches_per_class);

@@ -591,6 +591,29 @@ pf_status pf_layout_create_factor(int64_t n, int32_t b, int32_t k, pf_layout **o
   return PF_OK;
 }
 
+pf_status pf_layout_create_butterfly(int64_t n, int32_t b, int32_t max_stride, pf_layout **out) {
+  if (!out) return fail(PF_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  pf_layout *L = new (std::nothrow) pf_layout();
+  if (!L) return fail(PF_ERR_NOMEM, "host allocation failed");
+  std::string e;
+  try {
+    e = pf::build_butterfly_layout(*L, n, b, max_stride);
+  } catch (const std::bad_alloc &) {
+    delete L;
+    return fail(PF_ERR_NOMEM, "host allocation failed");
+  } catch (...) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, "layout build failed");
+  }
+  if (!e.empty()) {
+    delete L;
+    return fail(PF_ERR_INVALID_ARG, e);
+  }
+  *out = L;
+  return PF_OK;
+}
+
 pf_status pf_select_mask(int64_t n_out, int64_t n_in, int32_t b, double budget,
                          double lowrank_share, int32_t *r_out, int32_t *max_stride_out,
                          int64_t *params_out) {
@@ -1335,6 +1358,56 @@ pf_status pf_attn_bwd_noalloc(const pf_layout *L, int32_t B, int32_t H, int32_t 
   if ((st = hip_status(pf::attn_scratch(&delta), "attention scratch lookup")) != PF_OK) return st;
   return attn_bwd_enqueue(L, B, H, Sq, scale, Q, K, V, O, lse, dO, dQ, dK, dV, delta,
                           (hipStream_t)stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The product-form butterfly calls: validation (before any enqueue) and
+// the one launch.
+pf_status butterfly_call(bool bwd, const pf_layout *L, int64_t T, const void *in, const void *F,
+                         void *out, void *save, void *stream) {
+  if (!L) return fail(PF_ERR_INVALID_ARG, "layout is NULL");
+  if (L->bfly_nfac < 1) return fail(PF_ERR_INVALID_ARG, "not a product-form butterfly layout");
+  const int64_t k = (int64_t)1 << L->bfly_nfac;
+  if (L->b != pf::kBflyBlock || k * L->b > pf::kBflyMaxGroupCols)
+    return fail(PF_ERR_UNSUPPORTED, "the product kernel supports b = 32, max_stride <= 32");
+  if (T < 1 || T > ((int64_t)1 << 30)) return fail(PF_ERR_INVALID_ARG, "T must be in [1, 2^30]");
+  if (L->bfly_n * L->bfly_nfac * 2 > kMaxRowBytes)
+    return fail(PF_ERR_UNSUPPORTED, "rows of the saved activations too wide");
+  pf_status st;
+  if ((st = need_ptr(in, bwd ? "dY" : "X")) != PF_OK || (st = need_ptr(F, "F")) != PF_OK ||
+      (st = need_ptr(out, bwd ? "dX" : "Y")) != PF_OK)
+    return st;
+  if (save && (st = need_ptr(save, bwd ? "grads" : "acts")) != PF_OK) return st;
+  pf::BflyArgs a{};
+  a.in = in;
+  a.F = F;
+  a.out = out;
+  a.save = save;
+  a.T = T;
+  a.n = L->bfly_n;
+  a.nb = (int)(L->bfly_n / L->b);
+  a.k = (int)k;
+  a.nfac = L->bfly_nfac;
+  hipStream_t s = (hipStream_t)stream;
+  Timed t(PF_KERNEL_BUTTERFLY, s);
+  return hip_status(pf::launch_bfly(bwd, a, s), "butterfly product kernel");
+}
+
+}  // namespace
+
+extern "C" {
+
+pf_status pf_butterfly_fwd(const pf_layout *L, int64_t T, const void *X, const void *F, void *Y,
+                           void *acts, void *stream) {
+  return butterfly_call(false, L, T, X, F, Y, acts, stream);
+}
+
+pf_status pf_butterfly_bwd_data(const pf_layout *L, int64_t T, const void *dY, const void *F,
+                                void *dX, void *grads, void *stream) {
+  return butterfly_call(true, L, T, dY, F, dX, grads, stream);
 }
 
 size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int64_t K) {

@@ -241,6 +241,43 @@ std::string build_factor_layout(pf_layout &L, int64_t n, int32_t b, int32_t k) {
   return e;
 }
 
+// Product form of the block butterfly (Section 3.2, a product of factors
+// each on the support of I + B_k, k = 2, 4, ..., max_stride): the layout
+// holding every factor's kept blocks, factor f (stride 2^(f+1)) on the f-th
+// diagonal block of an (L nb) x (L nb) grid.  Block row f nb + p keeps the
+// columns f nb + p and f nb + (p XOR 2^f), ascending, which is also the
+// order the factors are packed in.  The weight gradient of all factors is
+// one masked product on this layout.
+std::string build_butterfly_layout(pf_layout &L, int64_t n, int32_t b, int32_t max_stride) {
+  if (b < 1 || n < b || n % b) return "b must be >= 1 and divide n";
+  const int64_t nb = n / b;
+  if (max_stride < 2 || !is_pow2(max_stride)) return "max_stride must be a power of two >= 2";
+  if (nb % max_stride) return "max_stride must divide n / b";
+  int nfac = 0;
+  while ((1 << nfac) < max_stride) ++nfac;
+  if ((int64_t)nfac * nb > (1 << 20)) return "too many blocks";
+  const int32_t rows = (int32_t)(nfac * nb);
+  L.n_out = L.n_in = (int64_t)rows * b;
+  L.b = b;
+  L.max_stride = L.eff_stride = max_stride;
+  L.nb_out = L.nb_in = rows;
+  L.s = rows;
+  L.bfly_n = n;
+  L.bfly_nfac = nfac;
+  L.row_ptr.assign(1, 0);
+  L.col_idx.clear();
+  for (int f = 0; f < nfac; ++f) {
+    const int64_t h = (int64_t)1 << f;
+    for (int64_t p = 0; p < nb; ++p) {
+      const int64_t q = p ^ h;
+      L.col_idx.push_back((int32_t)(f * nb + std::min(p, q)));
+      L.col_idx.push_back((int32_t)(f * nb + std::max(p, q)));
+      L.row_ptr.push_back((int32_t)L.col_idx.size());
+    }
+  }
+  return finish_layout(L);
+}
+
 // Layout of the (b, b)-block cover of an element mask (appendix on the cost
 // model: the block-aligned mask with the fewest nonzeros containing it):
 // block (i, j) is kept iff any element of it is nonzero.

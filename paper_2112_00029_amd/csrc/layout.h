@@ -11,6 +11,10 @@ struct pf_layout {
   int64_t n_out = 0, n_in = 0;
   int32_t b = 0, max_stride = 0, eff_stride = 0, s = 0, nb_out = 0, nb_in = 0;
   int32_t global_blocks = 0;  // attention layouts: width of the global stripes (blocks)
+  // Product-form butterfly layouts: the n x n matrix and its number of
+  // factors (strides 2 .. 2^bfly_nfac); 0 for every other layout.
+  int64_t bfly_n = 0;
+  int32_t bfly_nfac = 0;
   int64_t nnzb = 0;
   std::vector<int32_t> row_ptr, col_idx, col_ptr, row_idx, tperm;
 
@@ -57,6 +61,11 @@ std::string build_factor_layout(pf_layout &L, int64_t n, int32_t b, int32_t k);
 // Layout of the (b, b)-block cover of an n_out x n_in element mask.
 std::string build_cover_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
                                const uint8_t *elem_mask);
+// Stacked factor supports of the product form of an n x n block butterfly
+// with strides 2 .. max_stride: an (L nb) x (L nb) block-diagonal layout
+// (L = log2 max_stride, nb = n / b) whose f-th diagonal block keeps (p, p)
+// and (p, p XOR 2^f).  Its block-CSR order is the packing of the factors.
+std::string build_butterfly_layout(pf_layout &L, int64_t n, int32_t b, int32_t max_stride);
 std::string finish_layout(pf_layout &L);
 // Re-verify the work lists against the block-CSR.  Returns "" or an error.
 std::string check_layout(const pf_layout &L);

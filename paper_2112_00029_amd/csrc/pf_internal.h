@@ -218,6 +218,20 @@ hipError_t launch_gelu_bwd(int dtype, int64_t n, const void *dH,
 hipError_t launch_attn_fwd(const AttnArgs &a, int part, hipStream_t s);
 hipError_t launch_attn_bwd_dq(const AttnArgs &a, int part, hipStream_t s);
 hipError_t launch_attn_bwd_dkv(const AttnArgs &a, int part, hipStream_t s);
+// Product form of the block butterfly (butterfly.hip): one launch applies
+// every factor to TM-token x (k * 32)-feature tiles held in LDS.
+constexpr int kBflyBlock = 32;
+constexpr int kBflyMaxGroupCols = 1024;  // k * 32: the features of one group
+struct BflyArgs {
+  const void *in;  // X (forward) or dY (backward), T x n
+  const void *F;   // factors, packed [nfac][nb][2][32][32] (block-CSR order)
+  void *out;       // Y or dX, T x n
+  void *save;      // [T][nfac][n]: factor inputs / output gradients, or null
+  int64_t T, n;
+  int nb, k, nfac;  // n / 32, 2^nfac (blocks per group), factors
+};
+hipError_t launch_bfly(bool bwd, const BflyArgs &a, hipStream_t s);
+
 // The allocation-free attention backward keeps its row terms in a
 // file-scope device array of kAttnScratchRows floats (16 MiB per GPU);
 // attn_scratch gives this device's address of it (looked up on the first

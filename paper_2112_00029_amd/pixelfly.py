@@ -27,7 +27,7 @@ PF_EPI_NONE, PF_EPI_GELU = 0, 1
 PF_OP_NT, PF_OP_NN, PF_OP_TN = 0, 1, 2
 # Kernel classes of the timing hook (pf_kernel_class).
 KERNEL_CLASSES = ["spmm_fwd", "spmm_bwd_data", "sddmm", "lowrank_t", "lowrank_s", "reduce",
-                  "gelu_bwd", "attn_fwd", "attn_bwd_dq", "attn_bwd_dkv", "dense"]
+                  "gelu_bwd", "attn_fwd", "attn_bwd_dq", "attn_bwd_dkv", "dense", "butterfly"]
 PF_KERNEL_COUNT = len(KERNEL_CLASSES)
 
 
@@ -79,6 +79,9 @@ _SIGS = {
     "pf_layout_create_attention": (_i32, [_i64, _i32, _i32, _i32, ctypes.POINTER(_p)]),
     "pf_layout_create_from_element_mask": (_i32, [_i64, _i64, _i32, _p, ctypes.POINTER(_p)]),
     "pf_layout_create_factor": (_i32, [_i64, _i32, _i32, ctypes.POINTER(_p)]),
+    "pf_layout_create_butterfly": (_i32, [_i64, _i32, _i32, ctypes.POINTER(_p)]),
+    "pf_butterfly_fwd": (_i32, [_p, _i64, _p, _p, _p, _p, _p]),
+    "pf_butterfly_bwd_data": (_i32, [_p, _i64, _p, _p, _p, _p, _p]),
     "pf_select_mask": (_i32, [_i64, _i64, _i32, ctypes.c_double, ctypes.c_double,
                               ctypes.POINTER(_i32), ctypes.POINTER(_i32), ctypes.POINTER(_i64)]),
     "pf_layout_info_get": (_i32, [_p, ctypes.POINTER(pf_layout_info)]),
@@ -218,6 +221,22 @@ def pf_layout_create_factor(n: int, b: int, k: int) -> Layout:
     h = _p()
     _check(_lib.pf_layout_create_factor(n, b, k, ctypes.byref(h)))
     return Layout(h.value)
+
+
+def pf_layout_create_butterfly(n: int, b: int, max_stride: int) -> Layout:
+    h = _p()
+    _check(_lib.pf_layout_create_butterfly(n, b, max_stride, ctypes.byref(h)))
+    return Layout(h.value)
+
+
+def pf_butterfly_fwd(layout, T, X, F, Y, acts=None, stream=None) -> None:
+    _check(_lib.pf_butterfly_fwd(layout.handle, T, _ptr(X), _ptr(F), _ptr(Y), _ptr(acts),
+                                 _stream(stream)))
+
+
+def pf_butterfly_bwd_data(layout, T, dY, F, dX, grads=None, stream=None) -> None:
+    _check(_lib.pf_butterfly_bwd_data(layout.handle, T, _ptr(dY), _ptr(F), _ptr(dX),
+                                      _ptr(grads), _stream(stream)))
 
 
 def pf_select_mask(n_out: int, n_in: int, b: int, budget: float, lowrank_share: float = 0.25) -> dict:

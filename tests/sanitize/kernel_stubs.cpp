@@ -44,5 +44,6 @@ hipError_t launch_attn_fwd(const AttnArgs &, int, hipStream_t) { no_kernels("att
 hipError_t launch_attn_bwd_dq(const AttnArgs &, int, hipStream_t) { no_kernels("attn_dq"); }
 hipError_t launch_attn_bwd_dkv(const AttnArgs &, int, hipStream_t) { no_kernels("attn_dkv"); }
 hipError_t attn_scratch(float **) { no_kernels("attn_scratch"); }
+hipError_t launch_bfly(bool, const BflyArgs &, hipStream_t) { no_kernels("bfly"); }
 
 }  // namespace pf

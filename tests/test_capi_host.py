@@ -186,7 +186,7 @@ def test_timing_hook_errors_before_any_hip_call():
     with pytest.raises(pf.PixelflyError) as e:
         pf.pf_timing_end()
     assert e.value.status == pf.PF_ERR_STATE
-    assert len(pf.KERNEL_CLASSES) == pf.PF_KERNEL_COUNT == 11
+    assert len(pf.KERNEL_CLASSES) == pf.PF_KERNEL_COUNT == 12
 
 
 @pytest.mark.parametrize("seq,b,ms,g", [(4096, 64, 64, 1), (4096, 64, 64, 2), (512, 64, 8, 1),
@@ -304,4 +304,44 @@ def test_mixed_call_errors_before_any_launch():
     with pytest.raises(pf.PixelflyError) as e:  # Wblk is required (the dgamma term)
         pf.pf_linear_bwd_weight_mixed(L, pf.PF_BF16, 128, 32, 0.5, A16, A16, None, A16, A16, A16,
                                       A16, A16, A16, A16, 1 << 30, stream=0)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("n,b,ms", [(1024, 32, 32), (1024, 32, 2), (2048, 32, 16), (512, 64, 8),
+                                    (96, 3, 4)])
+def test_butterfly_product_layout_bit_exact_vs_oracle(n, b, ms):
+    """Stacked factor supports of the product form: the C++ builder against
+    the oracle's block-diagonal factor mask, bit for bit."""
+    from oracle import butterfly as ob
+    L = pf.pf_layout_create_butterfly(n, b, ms)
+    info = pf.pf_layout_info_get(L)
+    nfac = ms.bit_length() - 1
+    M = ob.product_factor_mask(n // b, nfac)
+    row_ptr, col_idx, *_r = om.block_csr(M)
+    assert info["nb_out"] == info["nb_in"] == nfac * (n // b)
+    assert np.array_equal(info["row_ptr"], row_ptr) and np.array_equal(info["col_idx"], col_idx)
+    pf.pf_layout_check(L)
+
+
+def test_butterfly_product_errors():
+    for args in [(1024, 32, 3), (1024, 32, 1), (1000, 32, 4), (1024, 32, 64)]:
+        with pytest.raises(pf.PixelflyError) as e:
+            pf.pf_layout_create_butterfly(*args)
+        assert e.value.status == pf.PF_ERR_INVALID_ARG
+    fake = 1 << 40
+    flat = pf.pf_layout_create(1024, 1024, 32, 8)
+    with pytest.raises(pf.PixelflyError) as e:  # not a product layout
+        pf.pf_butterfly_fwd(flat, 64, fake, fake, fake)
+    assert e.value.status == pf.PF_ERR_INVALID_ARG
+    wide = pf.pf_layout_create_butterfly(4096, 32, 64)  # 64 x 32 features per group
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_butterfly_fwd(wide, 64, fake, fake, fake)
+    assert e.value.status == pf.PF_ERR_UNSUPPORTED
+    b64 = pf.pf_layout_create_butterfly(1024, 64, 4)
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_butterfly_bwd_data(b64, 64, fake, fake, fake)
+    assert e.value.status == pf.PF_ERR_UNSUPPORTED
+    L = pf.pf_layout_create_butterfly(1024, 32, 8)
+    with pytest.raises(pf.PixelflyError) as e:
+        pf.pf_butterfly_fwd(L, 64, fake + 2, fake, fake)  # misaligned X
     assert e.value.status == pf.PF_ERR_INVALID_ARG
