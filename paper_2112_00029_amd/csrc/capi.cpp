@@ -279,8 +279,13 @@ struct SkinnyPlan {
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0, 128 / blk};
+  if (dtype != 0 && r > 0 && r < 128) {
+    // fp32, r below one 128-column tile: one block per tile (no dead columns).
+    p.G = 1;
+    p.bm = blk == 32 ? 128 : 64;
+  }
   if (r <= 0 || use_skinny(dtype, T, r, (int64_t)kblocks * blk)) return p;  // no split
-  const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + 127) / 128;
+  const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + p.G * blk - 1) / (p.G * blk);
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
   int64_t ns;
   if (dtype == 0) {
@@ -291,7 +296,8 @@ SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
     if (ns == 2 && steps < 16) ns = 1;
   } else {
     const int64_t want = (PF_WG_TARGET + mtiles * ntiles - 1) / (mtiles * ntiles);
-    ns = std::min<int64_t>({want, PF_MAX_SPLIT, std::max<int64_t>(1, steps / 4)});
+    ns = std::min<int64_t>({want, p.G == 1 ? 2 * PF_MAX_SPLIT : PF_MAX_SPLIT,
+                            std::max<int64_t>(1, steps / 4)});
   }
   if (ns > 1) {
     p.nsplit = (int)ns;
@@ -302,7 +308,7 @@ SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
 
 // Split-token plan of the TN kernel.  Few work items (under one round of
 // kTNSlots resident workgroups): the split of at most PF_TN_MAX_SPLIT parts of
-// at least 512 tokens that minimises rounds x steps per workgroup.  Many
+// at least min_tokens tokens that minimises rounds x steps per workgroup.  Many
 // items: aim for about 4096 workgroups (token splits also shorten each
 // workgroup's serial chain and its L2 footprint) with power-of-two splits of
 // at least 512 tokens, at most PF_TN_MAX_SPLIT, keeping the fp32 partial
@@ -322,11 +328,15 @@ struct TNPlan {
 };
 
 // row_bytes: the largest operand row stride in bytes.
-TNPlan tn_plan(int items, int64_t T, int64_t row_bytes) {
+int64_t tn_min_tokens(int dtype) { return dtype == 0 ? 512 : 64; }
+
+// min_tokens: fewest tokens per split (512 for bf16, whose weight gradient
+// is bound by operand traffic; 64 for fp32, bound by its long MFMAs).
+TNPlan tn_plan(int items, int64_t T, int64_t row_bytes, int64_t min_tokens = 512) {
   TNPlan p{1, ((T + 63) / 64) * 64, 0};
   const int64_t min_split = (T * row_bytes + 0x7fffffffLL - 1) / 0x7fffffffLL;
   int64_t ns = 1;
-  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(PF_TN_MAX_SPLIT, T / 512));
+  const int64_t cap = std::max<int64_t>(1, std::min<int64_t>(PF_TN_MAX_SPLIT, T / min_tokens));
   if (items < PF_TN_ROUND_ITEMS) {
     // Few items: the split that finishes soonest when kTNSlots workgroups
     // run at a time, i.e. fewest (rounds x 64-token steps per workgroup);
@@ -780,7 +790,7 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
   fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
   const int64_t es = dtype == PF_BF16 ? 2 : 4;
   const int items = pf::tn_items_total(a, L->b);
-  const size_t tn = tn_plan(items, T, std::max(L->n_out, L->n_in) * es).ws;
+  const size_t tn = tn_plan(items, T, std::max(L->n_out, L->n_in) * es, tn_min_tokens(dtype)).ws;
   const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
   const size_t bwd = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
   return std::max({tn, fwd, bwd}) + mix_dgamma_bytes(items);
@@ -839,7 +849,8 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   a.n_items = (int)L->tn_items.size();
   fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
   const int items = pf::tn_items_total(a, b);
-  const TNPlan tp = tn_plan(items, T, std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
+  const TNPlan tp = tn_plan(items, T, std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4),
+                            tn_min_tokens(dtype));
   p.tn_items = items;
   p.tn_split = tp.nsplit;
   p.tn_chunk = tp.chunk;
@@ -1116,7 +1127,7 @@ pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, con
   a.T = T;
   a.scale_w = a.scale_lr = 1.f;
   *plan = tn_plan(pf::tn_items_total(a, L->b), T,
-                  std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4));
+                  std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4), tn_min_tokens(dtype));
   a.nsplit = plan->nsplit;
   a.chunk = plan->chunk;
   return a;
@@ -1414,7 +1425,7 @@ size_t pf_dense_workspace_bytes(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_
   if (dtype != PF_BF16 && dtype != PF_FP32) return 0;
   if (op != PF_OP_TN || M < 64 || N < 64 || K < 1 || M % 64 || N % 64) return 0;
   int items = (int)(((M / 64 + 1) / 2) * ((N / 64 + 1) / 2));
-  return tn_plan(items, K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4)).ws;
+  return tn_plan(items, K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4), tn_min_tokens(dtype)).ws;
 }
 
 // Blocks of 64 columns per dense comparator tile: 256-wide bf16 tiles when
@@ -1452,7 +1463,8 @@ pf_status pf_dense_gemm(pf_dtype dtype, pf_gemm_op op, int64_t M, int64_t N, int
       a.dr[0] = pf::TNDense{A, M, B, N, C, N, (int)(M / 64), (int)(N / 64)};
       a.n_dense = 1;
       a.T = K;
-      TNPlan p = tn_plan(pf::tn_items_total(a, 64), K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4));
+      TNPlan p = tn_plan(pf::tn_items_total(a, 64), K, std::max(M, N) * (dtype == PF_BF16 ? 2 : 4),
+                         tn_min_tokens(dtype));
       if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
       a.nsplit = p.nsplit;
       a.chunk = p.chunk;

@@ -804,9 +804,12 @@ __global__ __launch_bounds__(256, 2) void tn_kernel(TNArgs a_arg) {
         static_for<TN>([&](auto tn) __attribute__((always_inline)) {
           bfg[tn] = Bs[kq * LDS_S + wn * 64 + tn * 32 + (lane & 31)];
         });
+        // fp32 MFMAs are long (the kernel is MFMA-bound at these sizes):
+        // sub-tiles without a kept block are skipped (a wave-uniform branch).
         static_for<TM>([&](auto tm) __attribute__((always_inline)) {
           static_for<TN>([&](auto tn) __attribute__((always_inline)) {
-            acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
+            if (live[tm][tn])
+              acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x2f32(af[tm], bfg[tn], acc[tm][tn], 0, 0, 0);
           });
         });
       });
@@ -1021,6 +1024,14 @@ template <typename T, int BLK, bool BKN>
 static hipError_t nt_dispatch_g(int G, int bm, bool dense, const NTArgs &a, hipStream_t s) {
   constexpr int GMAX = 128 / BLK;
   if (dense) {
+    // fp32 rank-r products narrower than 128 columns run one block wide
+    // (32-column tiles need 128 token rows: one 32-row MFMA tile per wave).
+    if constexpr (std::is_same<T, float>::value && GMAX > 1) {
+      if (G == 1) {
+        if constexpr (BLK == 32) return nt_go<T, BLK, 1, BKN, 128, true>(a, s);
+        else return bm == 64 ? nt_go<T, BLK, 1, BKN, 64, true>(a, s) : nt_go<T, BLK, 1, BKN, 128, true>(a, s);
+      }
+    }
     if (G != GMAX) return hipErrorInvalidValue;
     return bm == 64 ? nt_go<T, BLK, GMAX, BKN, 64, true>(a, s) : nt_go<T, BLK, GMAX, BKN, 128, true>(a, s);
   }
