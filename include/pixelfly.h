@@ -253,8 +253,12 @@ pf_status pf_layout_plan_get(const pf_layout *layout, int32_t *stats,
  * products report their output tile and kernel family (1: operands copied
  * global -> LDS directly; 0: staged through registers).  The weight
  * gradient reports its work items (kept-block tiles plus the dU and dV
- * tiles), the token split and the tokens per split.  Errors as the compute
- * calls' argument checks: INVALID_ARG, UNSUPPORTED.
+ * tiles), the token split and the tokens per split, its tile side (128, or
+ * 256 for the bf16 kernel whose 256 workgroups first run whole items and
+ * then share the remaining items' tokens evenly) and, for the 256 tiles,
+ * how many items are shared by several workgroups (their fp32 partial sums
+ * added in token order by a second pass).  Errors as the compute calls'
+ * argument checks: INVALID_ARG, UNSUPPORTED.
  */
 typedef struct {
   int32_t lowrank_t_kernel, lowrank_t_split, lowrank_t_tile_m, lowrank_t_tile_n;
@@ -264,6 +268,7 @@ typedef struct {
   int32_t tn_items, tn_split;
   int64_t tn_chunk;
   uint64_t workspace_bytes; /* pf_workspace_bytes of the same arguments */
+  int32_t tn_tile, tn_shared;
 } pf_linear_plan;
 
 pf_status pf_linear_plan_get(const pf_layout *layout, pf_dtype dtype, int64_t T,

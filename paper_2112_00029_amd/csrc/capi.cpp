@@ -22,8 +22,8 @@ LaunchEvents &next_launch_events() {
   return e;
 }
 
-int tn_items_total(const TNArgs &a, int blk) {
-  const int GT = 128 / blk;
+int tn_items_total(const TNArgs &a, int blk, int tile) {
+  const int GT = tile / blk;
   int n = a.n_items;
   for (int r = 0; r < a.n_dense; ++r)
     n += ((a.dr[r].na_blk + GT - 1) / GT) * ((a.dr[r].nb_blk + GT - 1) / GT);
@@ -325,6 +325,10 @@ struct TNPlan {
   int nsplit;
   int64_t chunk;
   size_t ws;
+  // 256 x 256 kernel: items shared by several workgroups (summed from the
+  // partial slots by a second pass).
+  bool wide = false;
+  int shared = 0;
 };
 
 // row_bytes: the largest operand row stride in bytes.
@@ -372,6 +376,50 @@ TNPlan tn_plan(int items, int64_t T, int64_t row_bytes, int64_t min_tokens = 512
   }
   return p;
 }
+
+// The 256 x 256 weight-gradient kernel runs a call when: bf16, b of 64 or
+// 128, no mixing weight, at least PF_WIDE_MIN_T tokens, at least one full
+// round of work items (kTNWGrid), every operand's rows over the whole token
+// range addressable with 32-bit offsets, and the wide items waste at most a
+// fifth of their block slots (kept blocks over rows x kept columns of every
+// item; a wave whose columns keep nothing skips its MFMAs).  With fewer
+// items than workgroups every item is shared: workgroups then read
+// different token rows of the same columns at a time, L2 stops serving the
+// neighbours, and the 128 x 128 kernel measured faster (the 16384 x 4096
+// layer at b = 64: 208 items, 540 against 466 us).
+void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
+                     const void *X, const void *T_lr, const void *S, void *dU, void *dV);
+bool tn_wide(const pf_layout *L, int dtype, int64_t T, int32_t r, bool mixed) {
+  if (dtype != 0 || mixed || (L->b != 64 && L->b != 128) || L->tn_items_w.empty()) return false;
+  if (T < PF_WIDE_MIN_T) return false;
+  pf::TNArgs w{};
+  w.n_items = (int)L->tn_items_w.size();
+  fill_tn_regions(w, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+  if (pf::tn_items_total(w, L->b, pf::kTNWTile) < pf::kTNWGrid) return false;
+  const int64_t row_bytes = std::max<int64_t>({L->n_out, L->n_in, (int64_t)r}) * 2;
+  // Copies run up to seven 32-token steps past a segment (read as zeros).
+  if ((T + 512) * row_bytes > 0x7fffffffLL) return false;
+  const int GT = 256 / L->b;
+  int64_t slots = 0;
+  for (auto &it : L->tn_items_w) slots += (int64_t)GT * it.nb;
+  return L->nnzb * 5 >= slots * 4;
+}
+
+// Plan of the 256 x 256 kernel over `items` work items: kTNWGrid
+// workgroups; the items past the last full round are shared.  Workspace:
+// two fp32 partial slots of 256 x 256 per workgroup.
+TNPlan tn_plan_wide(int items, int64_t T) {
+  TNPlan p{1, ((T + 63) / 64) * 64, 0};
+  p.wide = true;
+  p.shared = items % pf::kTNWGrid;
+  if (p.shared > 0)
+    p.ws = (size_t)2 * pf::kTNWGrid * pf::kTNWTile * pf::kTNWTile * sizeof(float);
+  return p;
+}
+
+pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *dY,
+                   const void *X, const void *T_lr, const void *S, void *dWblk, void *dU,
+                   void *dV, TNPlan *plan, bool mixed = false);
 
 // Workspace the mixed weight-gradient call adds after the split partials:
 // the kept-block dot partials (one per item, or 16 per item after a split)
@@ -737,7 +785,8 @@ pf_status pf_layout_upload(pf_layout *L, void *stream) {
       vec(L->fwd_tiles_w, L->d_fwd_tiles_w), vec(L->bwd_tiles_w, L->d_bwd_tiles_w),
       vec(L->kcols_fwd_w, L->d_kcols_fwd_w), vec(L->blks_fwd_w, L->d_blks_fwd_w),
       vec(L->kcols_bwd_w, L->d_kcols_bwd_w), vec(L->blks_bwd_w, L->d_blks_bwd_w),
-      vec(L->tn_items, L->d_tn_items),       vec(L->row_ptr, L->d_row_ptr),
+      vec(L->tn_items, L->d_tn_items),       vec(L->tn_items_w, L->d_tn_items_w),
+      vec(L->row_ptr, L->d_row_ptr),
       vec(L->col_idx, L->d_col_idx),         vec(L->col_ptr, L->d_col_ptr),
       vec(L->row_idx, L->d_row_idx)};
   constexpr int NP = (int)(sizeof(pieces) / sizeof(pieces[0]));
@@ -790,10 +839,19 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
   fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
   const int64_t es = dtype == PF_BF16 ? 2 : 4;
   const int items = pf::tn_items_total(a, L->b);
+  // The 128 x 128 plan (mixed calls, and the rest when the wide kernel does
+  // not apply) and, where it applies, the 256 x 256 one.
   const size_t tn = tn_plan(items, T, std::max(L->n_out, L->n_in) * es, tn_min_tokens(dtype)).ws;
+  size_t tnw = 0;
+  if (tn_wide(L, (int)dtype, T, r, false)) {
+    pf::TNArgs w{};
+    w.n_items = (int)L->tn_items_w.size();
+    fill_tn_regions(w, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
+    tnw = tn_plan_wide(pf::tn_items_total(w, L->b, pf::kTNWTile), T).ws;
+  }
   const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
   const size_t bwd = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
-  return std::max({tn, fwd, bwd}) + mix_dgamma_bytes(items);
+  return std::max({tn, tnw, fwd, bwd}) + mix_dgamma_bytes(items);
 }
 
 pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -845,15 +903,14 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   p.bwd_tile_m = cg.bm;
   p.bwd_tile_n = cg.bn;
   p.bwd_direct_lds = cg.dma;
-  pf::TNArgs a{};
-  a.n_items = (int)L->tn_items.size();
-  fill_tn_regions(a, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
-  const int items = pf::tn_items_total(a, b);
-  const TNPlan tp = tn_plan(items, T, std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4),
-                            tn_min_tokens(dtype));
-  p.tn_items = items;
+  TNPlan tp;
+  const pf::TNArgs a =
+      tn_args(L, dtype, T, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, &tp);
+  p.tn_items = pf::tn_items_total(a, b, tp.wide ? pf::kTNWTile : 128);
   p.tn_split = tp.nsplit;
   p.tn_chunk = tp.chunk;
+  p.tn_tile = tp.wide ? pf::kTNWTile : 128;
+  p.tn_shared = tp.shared;
   p.workspace_bytes = pf_workspace_bytes(L, T, r, dtype);
   *o = p;
   return PF_OK;
@@ -1055,11 +1112,12 @@ pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const voi
 // (S and X only) go first, then, for each group of dY block columns linked
 // by a shared item (union-find over block rows of W), the group's kept-block
 // items followed by its dU items.  Without the low-rank regions, or with
-// more items than the order holds, the natural order stays.
-void set_tn_order(pf::TNArgs &a, const pf_layout *L) {
+// more items than the order holds, the natural order stays.  `items` is the
+// kept-block list of the launch, tiles of GT x GT blocks.
+void set_tn_order(pf::TNArgs &a, const pf_layout *L, const std::vector<pf::TNItem> &items,
+                  int GT) {
   a.n_order = 0;
   if (a.n_dense < 2) return;
-  const int GT = 128 / L->b;
   const pf::TNDense &d0 = a.dr[0], &d1 = a.dr[1];
   const int nsp = a.n_items;
   const int nbg0 = (d0.nb_blk + GT - 1) / GT, n0 = ((d0.na_blk + GT - 1) / GT) * nbg0;
@@ -1078,7 +1136,7 @@ void set_tn_order(pf::TNArgs &a, const pf_layout *L) {
     r1 = std::min(r0 + GT, d0.na_blk);
   };
   for (int i = 0; i < nsp; ++i) {
-    const pf::TNItem &it = L->tn_items[i];
+    const pf::TNItem &it = items[i];
     for (int g = 1; g < it.na; ++g) unite(it.a_col[g], it.a_col[0]);
   }
   for (int q = 0; q < n0; ++q) {
@@ -1093,7 +1151,7 @@ void set_tn_order(pf::TNArgs &a, const pf_layout *L) {
     if (sp_of[root].empty() && du_of[root].empty()) roots.push_back(root);
   };
   for (int i = 0; i < nsp; ++i) {
-    const int root = find(L->tn_items[i].a_col[0]);
+    const int root = find(items[i].a_col[0]);
     note(root);
     sp_of[root].push_back(i);
   }
@@ -1113,29 +1171,46 @@ void set_tn_order(pf::TNArgs &a, const pf_layout *L) {
   if (k == total) a.n_order = total;
 }
 
-// Weight-gradient work list and its token split.
+// Weight-gradient work list and its token split (the 256 x 256 kernel when
+// tn_wide allows; mixed calls always take the 128 x 128 one).
 pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, const void *dY,
                    const void *X, const void *T_lr, const void *S, void *dWblk, void *dU,
-                   void *dV, TNPlan *plan) {
+                   void *dV, TNPlan *plan, bool mixed) {
   pf::TNArgs a{};
   a.A = dY; a.lda = L->n_out;
   a.B = X; a.ldb = L->n_in;
   a.Wout = dWblk;
-  a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
-  fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
-  set_tn_order(a, L);
   a.T = T;
   a.scale_w = a.scale_lr = 1.f;
-  *plan = tn_plan(pf::tn_items_total(a, L->b), T,
-                  std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4), tn_min_tokens(dtype));
+  fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
+  if (tn_wide(L, (int)dtype, T, r, mixed)) {
+    a.items = L->d_tn_items_w; a.n_items = (int)L->tn_items_w.size();
+    set_tn_order(a, L, L->tn_items_w, pf::kTNWTile / L->b);
+    *plan = tn_plan_wide(pf::tn_items_total(a, L->b, pf::kTNWTile), T);
+  } else {
+    a.items = L->d_tn_items; a.n_items = (int)L->tn_items.size();
+    set_tn_order(a, L, L->tn_items, 128 / L->b);
+    *plan = tn_plan(pf::tn_items_total(a, L->b), T,
+                    std::max(L->n_out, L->n_in) * (dtype == PF_BF16 ? 2 : 4), tn_min_tokens(dtype));
+  }
   a.nsplit = plan->nsplit;
   a.chunk = plan->chunk;
   return a;
 }
 
 // dW on the mask, dU, dV (and the pass over split partials).
-pf_status enqueue_tn(const pf_layout *L, int dt, pf::TNArgs a, float *ws, hipStream_t s) {
+pf_status enqueue_tn(const pf_layout *L, int dt, pf::TNArgs a, const TNPlan &p, float *ws,
+                     hipStream_t s) {
   a.partials = ws;
+  if (p.wide) {
+    {
+      Timed t(PF_KERNEL_SDDMM, s);
+      pf_status st = hip_status(pf::launch_tnw(L->b, pf::kTNWGrid, a, s), "weight-gradient kernel");
+      if (st != PF_OK || p.shared <= 0) return st;
+    }
+    Timed t(PF_KERNEL_REDUCE, s);
+    return hip_status(pf::launch_tnw_reduce(L->b, p.shared, a, s), "weight-gradient reduction");
+  }
   {
     Timed t(PF_KERNEL_SDDMM, s);
     pf_status st = hip_status(pf::launch_tn(dt, L->b, a, s), "weight-gradient kernel");
@@ -1174,7 +1249,7 @@ pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, in
   TNPlan p;
   const pf::TNArgs a = tn_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, &p);
   if ((st = need_ws(p.ws, workspace, ws_bytes)) != PF_OK) return st;
-  return enqueue_tn(L, (int)dtype, a, (float *)workspace, (hipStream_t)stream);
+  return enqueue_tn(L, (int)dtype, a, p, (float *)workspace, (hipStream_t)stream);
 }
 
 pf_status pf_linear_bwd_data_mixed(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -1206,7 +1281,7 @@ pf_status pf_linear_bwd_weight_mixed(const pf_layout *L, pf_dtype dtype, int64_t
   if (!dgamma || ((uintptr_t)dgamma & 3)) return fail(PF_ERR_INVALID_ARG, "dgamma NULL or misaligned");
   if ((st = check_state(L)) != PF_OK) return st;
   TNPlan p;
-  pf::TNArgs a = tn_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, &p);
+  pf::TNArgs a = tn_args(L, dtype, T, r, dY, X, T_lr, S, dWblk, dU, dV, &p, true);
   const int items = pf::tn_items_total(a, L->b);
   const size_t off = align256(p.ws);
   const size_t need = off + mix_dgamma_bytes(items);
@@ -1218,7 +1293,7 @@ pf_status pf_linear_bwd_weight_mixed(const pf_layout *L, pf_dtype dtype, int64_t
   float *sparts = wparts + (size_t)items * 16;
   a.wdot_out = wparts;
   hipStream_t s = (hipStream_t)stream;
-  if ((st = enqueue_tn(L, (int)dtype, a, (float *)workspace, s)) != PF_OK) return st;
+  if ((st = enqueue_tn(L, (int)dtype, a, p, (float *)workspace, s)) != PF_OK) return st;
   Timed t(PF_KERNEL_REDUCE, s);
   return hip_status(pf::launch_mix_dgamma((int)dtype, S, T_lr, r > 0 ? T * r : 0, wparts,
                                           a.nsplit > 1 ? items * 16 : items, sparts, dgamma, s),

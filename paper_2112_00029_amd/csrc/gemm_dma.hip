@@ -31,6 +31,7 @@
 #include <algorithm>
 #include <type_traits>
 
+#include "pf_dma.h"
 #include "pf_launch.h"
 
 // Token rows per group of the workgroup order (a group covers the token
@@ -43,29 +44,6 @@
 namespace pf {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef short s16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef uint16_t bf16_t;
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-typedef __attribute__((address_space(3))) void lds_void;
-
-template <int I, int N, typename F>
-__device__ __forceinline__ void sfor_impl(F &&f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    sfor_impl<I + 1, N>(f);
-  }
-}
-template <int N, typename F>
-__device__ __forceinline__ void sfor(F &&f) {
-  sfor_impl<0, N>(f);
-}
-
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
          ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
@@ -76,108 +54,6 @@ __device__ __forceinline__ float gelu(float x) {
 __device__ __forceinline__ float gelu_grad(float x) {
   const float Phi = 0.5f * (1.0f + erff(x * 0.70710678118654752f));
   return Phi + x * 0.39894228040143268f * __expf(-0.5f * x * x);
-}
-
-// Workgroups are dispatched round-robin over the 8 XCDs; remap so that
-// consecutive logical ids run on the same XCD (and share its L2).
-__device__ __forceinline__ int xcd_remap(int bid, int n) {
-  constexpr int X = 8;
-  const int q = n / X, rem = n % X, x = bid % X, slot = bid / X;
-  return x * q + min(x, rem) + slot;
-}
-
-// Buffer resource over [p, p + bytes): loads outside the range return zero
-// (ragged token tiles, K padding).
-__device__ __forceinline__ rsrc_t make_rsrc(const void *p, int64_t bytes) {
-  const int64_t b = bytes < 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)b, 0x00020000);
-}
-
-// One 1 KiB window: lane i copies 16 bytes from rsrc + voff + soff to
-// lds + 16 i.
-__device__ __forceinline__ void dma16(rsrc_t r, uint8_t *lds, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, (int)voff, (int)soff, 0, 0);
-}
-
-// Load of work-list metadata (tile lists, column and block indices) through
-// the constant address space: these arrays do not change while a kernel
-// runs, and such loads always use the scalar unit.  A generic load of them
-// after an operand copy becomes a vector load (the copy counts as a
-// possible writer), and its vmcnt wait then also waits for every copy in
-// flight: the A copies of a step would land before its B copies issue.
-template <typename T>
-__device__ __forceinline__ T ld_meta(const T *p) {
-  return *(const __attribute__((address_space(4))) T *)p;
-}
-
-// Wait until at most VM vector-memory operations of this wave are in flight
-// and all of its LDS reads have returned.
-template <int VM>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(VM >= 0 && VM < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((VM & 15) | ((VM >> 4) << 14) | (7 << 4));
-}
-__device__ __forceinline__ void barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// XOR swizzle of the 16-byte chunk index in a [row][chunk] LDS region with
-// CPR chunks per row (row-major operand, read with 16-byte fragment reads:
-// 16 consecutive rows at a fixed chunk hit distinct banks).
-template <int CPR>
-__device__ __forceinline__ int swz_row(int r) {
-  if constexpr (CPR == 4) return (r >> 2) & 3;
-  else return (r >> 1) & 7;
-}
-// Same for a [k][n] region read with the transpose read (4 consecutive k
-// rows x 32 bytes hit distinct banks).
-template <int CPR>
-__device__ __forceinline__ int swz_k(int k) {
-  if constexpr (CPR == 4) return 0;
-  else if constexpr (CPR == 8) return ((k >> 1) & 1) << 2;
-  else return (k & 3) << 2;
-}
-
-// MFMA 32x32x16 operand (lane l: row l % 32, k = (l / 32) * 8 + 0..7 of
-// k-slice kq) from a swizzled [row][chunk] region with row stride RB bytes.
-template <int RB>
-__device__ __forceinline__ bf16x8 frag_rows(const uint8_t *region, int r0, int kq, int lane) {
-  constexpr int CPR = RB / 16;
-  const int r = r0 + (lane & 31);
-  const int c = kq * 2 + (lane >> 5);
-  return *(const bf16x8 *)(region + r * RB + ((c ^ swz_row<CPR>(r)) << 4));
-}
-
-__device__ __forceinline__ s16x4 tr16(const uint8_t *p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(p));
-}
-
-// Same operand from a swizzled [k][n] region (n contiguous, RB bytes per k
-// row): rows are n0 + l % 32, read with ds_read_b64_tr_b16 (within each
-// 16-lane group, lanes 4m..4m+3 address k row m and lane j receives the 4
-// k values of column j).
-template <int RB>
-__device__ __forceinline__ bf16x8 frag_kn(const uint8_t *region, int n0, int kq, int lane) {
-  constexpr int CPR = RB / 16;
-  const int g16 = lane >> 4, i = lane & 15;
-  const int n = n0 + (g16 & 1) * 16 + (i & 3) * 4;
-  const int k = kq * 16 + (g16 >> 1) * 8 + (i >> 2);
-  const int c = n >> 3, half = ((n >> 2) & 1) << 3;
-  const s16x4 lo = tr16(region + k * RB + ((c ^ swz_k<CPR>(k)) << 4) + half);
-  const s16x4 hi = tr16(region + (k + 4) * RB + ((c ^ swz_k<CPR>(k + 4)) << 4) + half);
-  const s16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(bf16x8, v);
-}
-
-// Pipeline stage I of BYTES bytes: a distinct LDS object per stage, so that
-// the compiler's LDS-DMA dependency tracking can tell the stages apart; only
-// the stages a kernel uses are allocated.
-template <int I, int BYTES>
-__device__ __forceinline__ uint8_t *stage_buf() {
-  __shared__ __attribute__((aligned(1024))) uint8_t buf[BYTES];
-  return buf;
 }
 
 template <int BLK, int G, bool BKN, int BM, int BK, int NS, int NW, bool DENSE, int EPI, int OCC>
@@ -194,7 +70,6 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   constexpr int RBA = KW * 2, RPWA = 1024 / RBA;
   constexpr int RBB = BKN ? BLK * 2 : KW * 2, RPWB = 1024 / RBB;
   constexpr int A_BYTES = BM * BK * 2, B_BYTES = BN * BK * 2;
-  constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int PIECE = BLK * KW * 2;
   constexpr int AWW = A_BYTES / (1024 * NW), BWW = B_BYTES / (1024 * NW);  // windows per wave
   constexpr int WPH = BM / RPWA;                             // A windows per sub-block
@@ -211,15 +86,25 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   static_assert(RBA != 128 || AWW % 2 == 0, "window parity (A)");
   static_assert(BKN || RBB != 128 || (BWW % 2 == 0 && WPP % 2 == 0), "window parity (B)");
 
-  uint8_t *const st0 = stage_buf<0, STAGE>(), *const st1 = stage_buf<1, STAGE>();
-  uint8_t *const st2 = NS > 2 ? stage_buf<2, STAGE>() : st0;
-  uint8_t *const st3 = NS > 3 ? stage_buf<3, STAGE>() : st1;
-  auto stage = [&](auto j) __attribute__((always_inline)) -> uint8_t * {
+  // Each stage holds its A and B operands in LDS arrays of their own: with
+  // the transposed B reads addressed off a small array (frag_kn), the
+  // compiler can tell them apart from the next stage's copies and keeps
+  // those in flight instead of waiting for them before the reads.
+  uint8_t *const sa0 = stage_buf<0, A_BYTES>(), *const sb0 = stage_buf<1, B_BYTES>();
+  uint8_t *const sa1 = stage_buf<2, A_BYTES>(), *const sb1 = stage_buf<3, B_BYTES>();
+  uint8_t *const sa2 = NS > 2 ? stage_buf<4, A_BYTES>() : sa0;
+  uint8_t *const sb2 = NS > 2 ? stage_buf<5, B_BYTES>() : sb0;
+  uint8_t *const sa3 = NS > 3 ? stage_buf<6, A_BYTES>() : sa1;
+  uint8_t *const sb3 = NS > 3 ? stage_buf<7, B_BYTES>() : sb1;
+  struct Stage {
+    uint8_t *a, *b;
+  };
+  auto stage = [&](auto j) __attribute__((always_inline)) -> Stage {
     constexpr int J = decltype(j)::value;
-    if constexpr (J == 0) return st0;
-    else if constexpr (J == 1) return st1;
-    else if constexpr (J == 2) return st2;
-    else return st3;
+    if constexpr (J == 0) return Stage{sa0, sb0};
+    else if constexpr (J == 1) return Stage{sa1, sb1};
+    else if constexpr (J == 2) return Stage{sa2, sb2};
+    else return Stage{sa3, sb3};
   };
 
   const bf16_t *__restrict__ A = (const bf16_t *)a.A;
@@ -271,8 +156,20 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
 
   // Sub-block h of step t: A base, byte range, row stride and column offset
   // (bytes).  Kept block, low-rank block or zero padding, chosen by selects.
+  // Dense mode: token tile mt starts its K range mt steps in (mod total)
+  // and wraps around.  In step with one another, every tile would read the
+  // same columns of rows one operand stride apart (a power of two such as
+  // 32 KiB), which concentrates the requests on few HBM channels; staggered
+  // starts spread them (the S product at 16384 tokens, 16384 x 256: 219 ->
+  // 194 us).  The order is fixed per tile, so results stay deterministic.
+  const int rot = (DENSE && total > 0) ? mt % total : 0;
+  auto rstep = [&](int t) __attribute__((always_inline)) -> int {
+    if constexpr (DENSE) { const int u = t + rot; return u >= total ? u - total : u; }
+    else return t;
+  };
   auto a_src = [&](int t, int h, const bf16_t *&base, int64_t &bytes, uint32_t &ldb,
                    uint32_t &colb) __attribute__((always_inline)) {
+    t = rstep(t);
     const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
     const bool sp = c < nsteps;
     const int kcol = DENSE ? c : ld_meta(&a.kcols[kcol_off + max(min(c, nsteps - 1), 0)]);
@@ -284,6 +181,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   // Piece (g, h) of step t: B base at the piece, byte range, row stride.
   auto b_src = [&](int t, int g, int h, const bf16_t *&base, int64_t &bytes,
                    uint32_t &ldb) __attribute__((always_inline)) {
+    t = rstep(t);
     const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
     const int64_t ob = out_blk(g);
     if constexpr (DENSE) {
@@ -327,8 +225,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     }
   }
 
-  // Issue this wave's copies of step t into stage buffer sb.
-  auto issue = [&](int t, uint8_t *sb) __attribute__((always_inline)) {
+  // Issue this wave's copies of step t into stage st.
+  auto issue = [&](int t, Stage st) __attribute__((always_inline)) {
     {
       const int wa0 = w * AWW;
       const int h = __builtin_amdgcn_readfirstlane(wa0 / WPH), wr0 = wa0 % WPH;
@@ -340,7 +238,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       const uint32_t vrow = a_row * ldb;
       sfor<AWW>([&](auto i) __attribute__((always_inline)) {
         const int wr = wr0 + i;
-        dma16(r, sb + (wa0 + i) * 1024, vrow + a_c16[i & 1],
+        dma16(r, st.a + (wa0 + i) * 1024, vrow + a_c16[i & 1],
               (uint32_t)(wr * RPWA) * ldb + colb);
       });
     }
@@ -357,7 +255,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       const rsrc_t r = make_rsrc(base, bytes);
       const uint32_t vrow = b_row * ldb;
       sfor<WIN>([&](auto i) __attribute__((always_inline)) {
-        dma16(r, sb + A_BYTES + (wb0 + i) * 1024, vrow + b_c16[i & 1],
+        dma16(r, st.b + (wb0 + i) * 1024, vrow + b_c16[i & 1],
               (uint32_t)((wi0 + i) * RPWB) * ldb);
       });
     });
@@ -376,7 +274,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   const int kswitch = nsteps * BLK;
   // The switch check is a branch per K slice; launches without the mixing
   // weight run an instantiation without it (see the loop below).
-  auto compute_m = [&](const uint8_t *sb, int t, auto mix) __attribute__((always_inline)) {
+  auto compute_m = [&](Stage st, int t, auto mix) __attribute__((always_inline)) {
     sfor<BK / 16>([&](auto ks) __attribute__((always_inline)) {
       constexpr int h = (ks * 16) / KW, kq = ks % (KW / 16);
       if (decltype(mix)::value && (s_begin + t) * BK + ks * 16 == kswitch) {
@@ -389,12 +287,12 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       }
       bf16x8 xf[TM], wf[TN];
       sfor<TM>([&](auto tm) __attribute__((always_inline)) {
-        xf[tm] = frag_rows<RBA>(sb + h * (BM * RBA), wm * WTM + tm * 32, kq, lane);
+        xf[tm] = frag_rows<RBA>(st.a + h * (BM * RBA), wm * WTM + tm * 32, kq, lane);
       });
       sfor<TN>([&](auto tn) __attribute__((always_inline)) {
         const int n0 = wn * WTN + tn * 32;
         const int g = n0 / BLK, nl = n0 % BLK;
-        const uint8_t *piece = sb + A_BYTES + (g * NH + h) * PIECE;
+        const uint8_t *piece = st.b + (g * NH + h) * PIECE;
         if constexpr (BKN) wf[tn] = frag_kn<RBB>(piece, nl, kq, lane);
         else wf[tn] = frag_rows<RBB>(piece, nl, kq, lane);
       });
@@ -412,8 +310,8 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     if (j < total) issue(j, stage(j));
   });
   auto run = [&](auto mix) __attribute__((always_inline)) {
-    auto compute = [&](const uint8_t *sb, int t) __attribute__((always_inline)) {
-      compute_m(sb, t, mix);
+    auto compute = [&](Stage st, int t) __attribute__((always_inline)) {
+      compute_m(st, t, mix);
     };
     for (int t0 = 0; t0 < total; t0 += NS) {
       bool done = false;
@@ -456,14 +354,17 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   constexpr int SROW = WTN * 4, SCH = SROW / 16;  // staged row bytes, chunks
   constexpr int SP = 32;                          // rows per pass
   constexpr int LPR = WTN / 8, RPI = 64 / LPR;    // lanes per row, rows per store step
-  // Waves per stage buffer; the buffers used are the ones after the stage
-  // read in the last step, so NW / WPS of them must not wrap around to it.
-  constexpr int WPS = STAGE / (SP * SROW) < NW ? STAGE / (SP * SROW) : NW;
+  // Staging slices per stage (in its A array, then its B array); the stages
+  // used are the ones after the stage read in the last step, so NW / WPS of
+  // them must not wrap around to it.
+  constexpr int SLICE = SP * SROW, SPA = A_BYTES / SLICE, SPB = B_BYTES / SLICE;
+  constexpr int WPS = SPA + SPB < NW ? SPA + SPB : NW;
   static_assert(WPS >= 1 && (NW + WPS - 1) / WPS <= NS - 1, "staging room");
   static_assert((SCH & (SCH - 1)) == 0 && SP % RPI == 0, "staging");
-  const int sidx = (total + w / WPS) % NS;
-  uint8_t *const stg =
-      (sidx == 0 ? st0 : sidx == 1 ? st1 : sidx == 2 ? st2 : st3) + (w % WPS) * (SP * SROW);
+  const int sidx = (total + w / WPS) % NS, slice = w % WPS;
+  uint8_t *const sta = sidx == 0 ? sa0 : sidx == 1 ? sa1 : sidx == 2 ? sa2 : sa3;
+  uint8_t *const stb = sidx == 0 ? sb0 : sidx == 1 ? sb1 : sidx == 2 ? sb2 : sb3;
+  uint8_t *const stg = slice < SPA ? sta + slice * SLICE : stb + (slice - SPA) * SLICE;
   int ob[G];
   sfor<G>([&](auto g) __attribute__((always_inline)) { ob[g] = out_blk(g); });
   bf16_t *C = (bf16_t *)a.C;

@@ -119,8 +119,11 @@ static int32_t csr_pos(const pf_layout &L, int i, int j) {
   return (it != e && *it == j) ? (int32_t)(it - L.col_idx.begin()) : -1;
 }
 
-static void build_tn_items(pf_layout &L) {
-  const int GA = tn_group(L.b), GB = GA;
+// Weight-gradient items of GA x GA blocks: block rows with identical column
+// lists bundled GA at a time (the rest bundled in row order), each bundle's
+// column union cut into runs of GA columns.
+static void build_tn_items(pf_layout &L, int GA, std::vector<TNItem> &out) {
+  const int GB = GA;
   auto groups = group_identical(L.row_ptr, L.col_idx);
   std::vector<std::vector<int32_t>> bundles;
   std::vector<int32_t> leftover;
@@ -134,7 +137,7 @@ static void build_tn_items(pf_layout &L) {
   for (size_t t = 0; t < leftover.size(); t += GA)
     bundles.emplace_back(leftover.begin() + t,
                          leftover.begin() + std::min(leftover.size(), t + GA));
-  L.tn_items.clear();
+  out.clear();
   for (auto &bun : bundles) {
     std::vector<int32_t> cols;
     for (int i : bun)
@@ -152,9 +155,15 @@ static void build_tn_items(pf_layout &L) {
         for (int b = 0; b < kTNMax; ++b)
           it.out_blk[a * kTNMax + b] =
               (a < it.na && b < it.nb) ? csr_pos(L, bun[a], cols[c0 + b]) : -1;
-      L.tn_items.push_back(it);
+      out.push_back(it);
     }
   }
+}
+
+static void build_tn_items(pf_layout &L) {
+  build_tn_items(L, tn_group(L.b), L.tn_items);
+  L.tn_items_w.clear();
+  if (L.b == 64 || L.b == 128) build_tn_items(L, 256 / L.b, L.tn_items_w);
 }
 
 std::string build_layout(pf_layout &L, int64_t n_out, int64_t n_in, int32_t b,
@@ -399,17 +408,28 @@ std::string check_layout(const pf_layout &L) {
   if (!e.empty()) return "backward-data: " + e;
   e = sweep(L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w, L.G_bwd_w, true);
   if (!e.empty()) return "backward-data (wide): " + e;
-  std::fill(seen.begin(), seen.end(), 0);
-  for (auto &it : L.tn_items)
-    for (int a = 0; a < it.na; ++a)
-      for (int b = 0; b < it.nb; ++b) {
-        int32_t p = it.out_blk[a * kTNMax + b];
-        if (p != csr_pos(L, it.a_col[a], it.b_col[b]))
-          return "weight-gradient item block index mismatch";
-        if (p >= 0) seen[p]++;
-      }
-  for (int v : seen)
-    if (v != 1) return "weight-gradient items do not cover each kept block once";
+  auto items = [&](const std::vector<TNItem> &list, const char *what) -> std::string {
+    std::fill(seen.begin(), seen.end(), 0);
+    for (auto &it : list) {
+      for (int a = 0; a < kTNMax; ++a)
+        for (int b = 0; b < kTNMax; ++b) {
+          const int32_t p = it.out_blk[a * kTNMax + b];
+          if (a < it.na && b < it.nb) {
+            if (p != csr_pos(L, it.a_col[a], it.b_col[b]))
+              return std::string(what) + " item block index mismatch";
+            if (p >= 0) seen[p]++;
+          } else if (p >= 0) {
+            return std::string(what) + " item keeps a block outside its extent";
+          }
+        }
+    }
+    for (int v : seen)
+      if (v != 1) return std::string(what) + " items do not cover each kept block once";
+    return "";
+  };
+  e = items(L.tn_items, "weight-gradient");
+  if (!e.empty()) return e;
+  if (!L.tn_items_w.empty()) return items(L.tn_items_w, "weight-gradient (wide)");
   return "";
 }
 

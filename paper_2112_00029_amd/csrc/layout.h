@@ -29,6 +29,9 @@ struct pf_layout {
   std::vector<int32_t> kcols_fwd, blks_fwd, kcols_bwd, blks_bwd;
   std::vector<int32_t> kcols_fwd_w, blks_fwd_w, kcols_bwd_w, blks_bwd_w;
   std::vector<pf::TNItem> tn_items;
+  // Weight-gradient items of the 256 x 256 bf16 kernel (b = 64 or 128):
+  // bundles of 256 / b block rows x 256 / b block columns; empty otherwise.
+  std::vector<pf::TNItem> tn_items_w;
 
   // Device copies (valid after pf_layout_upload).
   int device = -1;
@@ -39,7 +42,7 @@ struct pf_layout {
   const pf::NTTile *d_fwd_tiles_w = nullptr, *d_bwd_tiles_w = nullptr;
   const int32_t *d_kcols_fwd_w = nullptr, *d_blks_fwd_w = nullptr;
   const int32_t *d_kcols_bwd_w = nullptr, *d_blks_bwd_w = nullptr;
-  const pf::TNItem *d_tn_items = nullptr;
+  const pf::TNItem *d_tn_items = nullptr, *d_tn_items_w = nullptr;
   const int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
   const int32_t *d_col_ptr = nullptr, *d_row_idx = nullptr;
 };

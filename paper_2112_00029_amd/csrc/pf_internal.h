@@ -107,7 +107,8 @@ struct TNArgs {
   int64_t T;
   int nsplit;
   int64_t chunk;        // tokens per split (multiple of 64)
-  float *partials;      // [items_total][nsplit][128*128] when nsplit > 1
+  float *partials;      // [items_total][nsplit][128*128] when nsplit > 1;
+                        // the 256 x 256 kernel: two slots of 256*256 per workgroup
   // Mixing weight: stores scale the kept-block sums by scale_w and the dense
   // regions by scale_lr (1 and 1 otherwise).  With wdot set, every workgroup
   // that stores kept blocks also writes the sum over its stored elements of
@@ -184,6 +185,12 @@ hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, 
 // The TN kernel, and (a.nsplit > 1) the pass that sums its split partials.
 hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
 hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s);
+// bf16 weight gradient on 256 x 256 tiles (blk 64 or 128) on kTNWGrid
+// workgroups (gemm_tnw.hip), and the pass that sums its `shared` items.
+constexpr int kTNWGrid = 256;
+constexpr int kTNWTile = 256;
+hipError_t launch_tnw(int blk, int grid, const TNArgs &a, hipStream_t s);
+hipError_t launch_tnw_reduce(int blk, int shared, const TNArgs &a, hipStream_t s);
 // Per-element-type parts of the register-staged kernels (one object file
 // each): T is uint16_t (bf16 storage) or float.
 template <typename T, bool BKN>
@@ -200,7 +207,8 @@ extern template hipError_t launch_tn_t<uint16_t>(int, const TNArgs &, hipStream_
 extern template hipError_t launch_tn_t<float>(int, const TNArgs &, hipStream_t);
 extern template hipError_t launch_tn_reduce_t<uint16_t>(int, const TNArgs &, hipStream_t);
 extern template hipError_t launch_tn_reduce_t<float>(int, const TNArgs &, hipStream_t);
-int tn_items_total(const TNArgs &a, int blk);
+// Work items of a TN launch on tile x tile tiles (128 or 256).
+int tn_items_total(const TNArgs &a, int blk, int tile = 128);
 hipError_t launch_skinny(bool b_kn, const SkinnyArgs &a, hipStream_t s);
 // dgamma of the mixing weight: partial sums of <S, T_lr> (n elements,
 // kMixDotParts workgroups), then one workgroup adds the kernel-stored partial

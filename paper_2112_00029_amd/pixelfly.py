@@ -70,7 +70,8 @@ class pf_linear_plan(ctypes.Structure):
         "lowrank_s_kernel", "lowrank_s_split", "lowrank_s_tile_m", "lowrank_s_tile_n",
         "fwd_tile_m", "fwd_tile_n", "fwd_direct_lds", "bwd_tile_m", "bwd_tile_n",
         "bwd_direct_lds", "tn_items", "tn_split")] + [("tn_chunk", _i64),
-                                                       ("workspace_bytes", ctypes.c_uint64)]
+                                                       ("workspace_bytes", ctypes.c_uint64),
+                                                       ("tn_tile", _i32), ("tn_shared", _i32)]
 
 
 _SIGS = {
