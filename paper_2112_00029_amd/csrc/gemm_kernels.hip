@@ -605,8 +605,17 @@ __global__ __launch_bounds__(256) void reduce_rows_kernel(int nsplit, const floa
                                                           int64_t ldc) {
   const int64_t n4 = M * ncols / 4;  // ncols is a multiple of 32
   for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < n4; q += (int64_t)gridDim.x * 256) {
+    // Splits in batches of 4 (loads issued together, added in split order).
     f32x4 v = *(const f32x4 *)(P + q * 4);
-    for (int s = 1; s < nsplit; ++s) v += *(const f32x4 *)(P + (int64_t)s * M * ncols + q * 4);
+    for (int s0 = 1; s0 < nsplit; s0 += 4) {
+      f32x4 t[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (s0 + u < nsplit) t[u] = *(const f32x4 *)(P + (int64_t)(s0 + u) * M * ncols + q * 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (s0 + u < nsplit) v += t[u];
+    }
     const int64_t e = q * 4, row = e / ncols, col = e % ncols;
     T *o = C + row * ldc + col;
 #pragma unroll
@@ -907,9 +916,18 @@ __global__ __launch_bounds__(256) void tn_reduce_kernel(TNArgs a_arg) {
   const int blk = v.oblk(ga, gb);
   float wd = 0.f;
   if (blk >= 0) {
+    // Splits in batches of 4 (loads issued together, added in split order).
     const float *part_p = a.partials + (int64_t)item * a.nsplit * (128 * 128) + q;
     f32x4 acc = *(const f32x4 *)part_p;
-    for (int sp = 1; sp < a.nsplit; ++sp) acc += *(const f32x4 *)(part_p + (int64_t)sp * (128 * 128));
+    for (int s0 = 1; s0 < a.nsplit; s0 += 4) {
+      f32x4 t[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (s0 + u < a.nsplit) t[u] = *(const f32x4 *)(part_p + (int64_t)(s0 + u) * (128 * 128));
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (s0 + u < a.nsplit) acc += t[u];
+    }
     const int64_t po = (int64_t)blk * (BLK * BLK) + (rl % BLK) * BLK + (cl % BLK);
     if (a.wdot && v.sparse) {
       const T *wp = (const T *)a.wdot + po;

@@ -324,15 +324,28 @@ __global__ __launch_bounds__(256) void tnw_reduce_kernel(TNArgs a_arg) {
   const int w = th / 64, lane = th % 64, wm = w & 1, wn = w >> 1;
   const int g_first = share_of((int64_t)li * S, Lw, G);
   const int g_last = share_of((int64_t)(li + 1) * S - 1, Lw, G);
+  // Segments in batches of 8: the batch's loads are issued together, then
+  // added in token order.
   f32x4 tot = {0.f, 0.f, 0.f, 0.f};
   bool first = true;
-  for (int gk = g_first; gk <= g_last; ++gk) {
-    if ((Lw * (gk + 1)) / G <= (Lw * gk) / G) continue;  // empty share
-    // The item is gk's first segment when gk's share starts in it.
-    const int wk = (Lw * gk) / G >= (int64_t)li * S ? 0 : 1;
-    const f32x4 term = *(const f32x4 *)(a.partials + ((int64_t)gk * 2 + wk) * kWSlot + e);
-    tot = first ? term : tot + term;
-    first = false;
+  for (int g0 = g_first; g0 <= g_last; g0 += 8) {
+    f32x4 term[8];
+    bool have[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int gk = g0 + u;
+      // Empty shares (and positions past g_last) hold no segment; the item
+      // is gk's first segment when gk's share starts in it.
+      have[u] = gk <= g_last && (Lw * (gk + 1)) / G > (Lw * gk) / G;
+      const int wk = (Lw * gk) / G >= (int64_t)li * S ? 0 : 1;
+      if (have[u]) term[u] = *(const f32x4 *)(a.partials + ((int64_t)gk * 2 + wk) * kWSlot + e);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (!have[u]) continue;
+      tot = first ? term[u] : tot + term[u];
+      first = false;
+    }
   }
   store4(a, v, wm * 128 + tm * 32 + (lane & 31), wn * 64 + tn * 32 + q * 8 + (lane >> 5) * 4, tot);
 }
