@@ -305,6 +305,28 @@ def test_large_layer_T4096_all_outputs(b):
         check_close(k, got[k], ref[k], "bf16")
 
 
+@pytest.mark.parametrize("T", [2509, 2049])
+def test_large_layer_ragged_T_wide_weight_gradient(T):
+    """The 16384 x 4096 layer at b = 128 with a token count that is not a
+    multiple of the 32-token step: the 256 x 256 weight gradient's segments
+    end inside a step (rows past T read as zeros) and the shares of the 16
+    remaining items start mid-item.  Every output element against the
+    oracle."""
+    from paper_2112_00029_amd import pixelfly as pf
+    n_out, n_in, ms, r, b = LARGE["n_out"], LARGE["n_in"], LARGE["ms"], LARGE["r"], 128
+    plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
+    print(f"[plan b={b} T={T}] {plan}", flush=True)
+    assert plan["tn_tile"] == 256 and plan["tn_shared"] > 0, plan
+    inp = _inputs(n_out, n_in, b, ms, T, r, "bf16")
+    out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", inp["raw"], timing=True)
+    assert kt["sddmm"][0] == 1, kt
+    got = {k: to_host(v) for k, v in out.items()}
+    ref = _oracle(inp, r, b)
+    ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
+    for k in ["Y", "dX", "dW", "T_lr", "S", "dU", "dV"]:
+        check_close(k, got[k], ref[k], "bf16")
+
+
 @pytest.fixture(scope="module")
 def large_full_inputs():
     """Seeded inputs of the full 16384-token layer shared by every block size
