@@ -305,15 +305,17 @@ def test_large_layer_T4096_all_outputs(b):
         check_close(k, got[k], ref[k], "bf16")
 
 
-@pytest.mark.parametrize("T", [2509, 2049])
-def test_large_layer_ragged_T_wide_weight_gradient(T):
+@pytest.mark.parametrize("T,r", [(2509, 256), (2049, 256), (2509, 128)])
+def test_large_layer_ragged_T_wide_weight_gradient(T, r):
     """The 16384 x 4096 layer at b = 128 with a token count that is not a
     multiple of the 32-token step: the 256 x 256 weight gradient's segments
     end inside a step (rows past T read as zeros) and the shares of the 16
-    remaining items start mid-item.  Every output element against the
-    oracle."""
+    remaining items start mid-item.  At r = 128 the dU and dV tiles are half
+    empty (one 128-column or 128-row block of the 256 x 256 tile), so waves
+    whose quarter holds nothing skip their MFMAs and the stores drop the
+    empty half.  Every output element against the oracle."""
     from paper_2112_00029_amd import pixelfly as pf
-    n_out, n_in, ms, r, b = LARGE["n_out"], LARGE["n_in"], LARGE["ms"], LARGE["r"], 128
+    n_out, n_in, ms, b = LARGE["n_out"], LARGE["n_in"], LARGE["ms"], 128
     plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
     print(f"[plan b={b} T={T}] {plan}", flush=True)
     assert plan["tn_tile"] == 256 and plan["tn_shared"] > 0, plan
