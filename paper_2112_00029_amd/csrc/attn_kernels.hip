@@ -45,6 +45,13 @@ constexpr float kLn2 = 0.6931471805599453f;
 // range-reduction sequence the library exp2f adds for denormal outputs.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Wait for every global load of this wave (vmcnt 0; LDS counter too).
+// Placed before a block loop whose first MFMAs use operands loaded ahead of
+// it: otherwise the compiler's wait analysis, joining that path with the
+// loop's back edge, can wait for the next tile's loads just issued at the
+// top of the loop as well.
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x70); }
+
 __device__ __forceinline__ float bf2f_a(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 __device__ __forceinline__ bf16_t f2bf_a(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
@@ -167,6 +174,11 @@ __global__ __launch_bounds__(256 * NG) void attn_fwd_kernel(AttnArgs a) {
     tk.store(Ks[grp][0], LDK, tid);
     tv.store(Vs[grp][0], LDV, tid);
   }
+  // Block column of this group's next tile, loaded one iteration ahead so
+  // that the tile loads do not wait on it (clamped into the row, which is
+  // never empty; unused past its end).
+  int cn = a.col_idx[min(p0 + grp + NG, p1 - 1)];
+  wait_loads();
   __syncthreads();
 
   for (int it = 0; it < iters; ++it) {
@@ -174,9 +186,10 @@ __global__ __launch_bounds__(256 * NG) void attn_fwd_kernel(AttnArgs a) {
     const int p = p0 + it * NG + grp;
     const bool valid = p < p1, next = p + NG < p1;
     if (next) {
-      tk.load(K + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
-      tv.load(V + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
+      tk.load(K + (int64_t)cn * BQ * D, tid);
+      tv.load(V + (int64_t)cn * BQ * D, tid);
     }
+    cn = a.col_idx[min(p + 2 * NG, p1 - 1)];
     if (valid) {
       // S^T[key][query] for 64 keys x this wave's 16 queries.
       f32x4 s[4];
@@ -348,6 +361,8 @@ __global__ __launch_bounds__(256 * NG) void attn_bwd_dq_kernel(AttnArgs a) {
     tk.store(Ks[grp][0], LDK, tid);
     tv.store(Vs[grp][0], LDK, tid);
   }
+  // Next block column one iteration ahead, as in the forward.
+  int cn = a.col_idx[min(p0 + grp + NG, p1 - 1)];
   __syncthreads();
 
   for (int it = 0; it < iters; ++it) {
@@ -355,9 +370,10 @@ __global__ __launch_bounds__(256 * NG) void attn_bwd_dq_kernel(AttnArgs a) {
     const int p = p0 + it * NG + grp;
     const bool valid = p < p1, next = p + NG < p1;
     if (next) {
-      tk.load(K + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
-      tv.load(V + (int64_t)a.col_idx[p + NG] * BQ * D, tid);
+      tk.load(K + (int64_t)cn * BQ * D, tid);
+      tv.load(V + (int64_t)cn * BQ * D, tid);
     }
+    cn = a.col_idx[min(p + 2 * NG, p1 - 1)];
     if (valid) {
     f32x4 s[4], dp[4];
 #pragma unroll
@@ -469,12 +485,13 @@ __global__ __launch_bounds__(256 * NG) void attn_bwd_dkv_kernel(AttnArgs a) {
     const int64_t qrow = (int64_t)a.row_idx[p] * BQ;
     tq.load(Q + qrow * D, tid);
     td.load(dO + qrow * D, tid);
-    if (tid < BQ) { rl = lse[qrow + tid] * kLog2e; rd = dl[qrow + tid]; }
+    // Raw values: scaling here would make the wave wait for the load.
+    if (tid < BQ) { rl = lse[qrow + tid]; rd = dl[qrow + tid]; }
   };
   auto sstore = [&](int buf) {
     tq.store(Qs[grp][buf], LDK, tid);
     td.store(dOs[grp][buf], LDK, tid);
-    if (tid < BQ) { ls[grp][buf][tid] = rl; ds[grp][buf][tid] = rd; }
+    if (tid < BQ) { ls[grp][buf][tid] = rl * kLog2e; ds[grp][buf][tid] = rd; }
   };
   const int iters = (p1 - p0 + NG - 1) / NG;
   if (p0 + grp < p1) {

@@ -135,19 +135,20 @@ __global__ __launch_bounds__(512, 1) void tnw_kernel(TNArgs a_arg) {
   constexpr int TM = 4, TN = 2;  // wave tile: 128 dW rows x 64 dW columns
   constexpr int CPB = BLK / 8;   // 16-byte chunks per block row
   static_assert(GT <= kTNMax, "item width");
-  // One LDS array per operand and stage (see frag_kn: the copies into the
-  // next stage then stay in flight while this one is read).
-  uint8_t *const s0 = stage_buf<0, 2 * kWOp>(), *const s1 = stage_buf<1, 2 * kWOp>();
-  uint8_t *const s2 = stage_buf<2, 2 * kWOp>(), *const s3 = stage_buf<3, 2 * kWOp>();
+  // One LDS object per stage (A at 0, B at kWOp), each read at one integer
+  // offset from its object (see frag_kn), so the copies into the next stages
+  // stay in flight while this one is read.
+  uint8_t *const lds0 = stage_buf<0, 2 * kWOp>(), *const lds1 = stage_buf<1, 2 * kWOp>();
+  uint8_t *const lds2 = stage_buf<2, 2 * kWOp>(), *const lds3 = stage_buf<3, 2 * kWOp>();
   struct Stage {
     uint8_t *a, *b;
   };
   auto stage = [&](auto j) __attribute__((always_inline)) -> Stage {
     constexpr int J = decltype(j)::value % kWNS;
-    if constexpr (J == 0) return Stage{s0, s0 + kWOp};
-    else if constexpr (J == 1) return Stage{s1, s1 + kWOp};
-    else if constexpr (J == 2) return Stage{s2, s2 + kWOp};
-    else return Stage{s3, s3 + kWOp};
+    if constexpr (J == 0) return Stage{lds0, lds0 + kWOp};
+    else if constexpr (J == 1) return Stage{lds1, lds1 + kWOp};
+    else if constexpr (J == 2) return Stage{lds2, lds2 + kWOp};
+    else return Stage{lds3, lds3 + kWOp};
   };
 
   const int tid = threadIdx.x, lane = tid & 63;
