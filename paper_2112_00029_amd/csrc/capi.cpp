@@ -275,7 +275,7 @@ struct SkinnyPlan {
   int bm;
   int nsplit;
   size_t ws;
-  int G;  // output blocks per tile (128 columns)
+  int G;  // output blocks per tile (128 or 256 columns)
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0, 128 / blk};
@@ -285,6 +285,26 @@ SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
     p.bm = blk == 32 ? 128 : 64;
   }
   if (r <= 0 || use_skinny(dtype, T, r, (int64_t)kblocks * blk)) return p;  // no split
+  if (dtype == 0 && r % 256 == 0 && T >= 2048 && (int64_t)kblocks * blk >= 8192) {
+    // Deep products (S = dY U of a wide layer): 256 x 256 tiles, eight
+    // waves, one workgroup per CU, split until about 256 workgroups run, at
+    // least 8 steps of 64 per split.  They read half the operand bytes per
+    // flop of the 128 x 128 tiles (16384 x 16384 by 256: 181 -> 158 us
+    // with four splits, the reduction 5 us longer).
+    p.G = 256 / blk;
+    p.bm = 256;
+    const int64_t tiles = ((T + 255) / 256) * (r / 256);
+    const int64_t steps = ((int64_t)kblocks * blk) / 64;
+    const int64_t want = std::max<int64_t>(1, 256 / tiles);
+    const int64_t cap = std::max<int64_t>(1, steps / 8);
+    int64_t ns = 1;
+    while (ns * 2 <= std::min(want, cap)) ns *= 2;
+    if (ns > 1) {
+      p.nsplit = (int)ns;
+      p.ws = (size_t)ns * T * r * sizeof(float);
+    }
+    return p;
+  }
   const int64_t mtiles = (T + p.bm - 1) / p.bm, ntiles = (r + p.G * blk - 1) / (p.G * blk);
   const int64_t steps = ((int64_t)kblocks * blk) / (dtype == 0 ? 64 : 32);
   int64_t ns;

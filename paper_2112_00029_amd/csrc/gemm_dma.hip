@@ -179,11 +179,11 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     colb = (uint32_t)(((sp ? kcol : c - nsteps) * BLK + kk) * 2);
   };
   // Piece (g, h) of step t: B base at the piece, byte range, row stride.
-  auto b_src = [&](int t, int g, int h, const bf16_t *&base, int64_t &bytes,
-                   uint32_t &ldb) __attribute__((always_inline)) {
+  // ob: output block of piece g (the tile's out_blk[g]).
+  auto b_src = [&](int t, int g, int h, int64_t ob, const bf16_t *&base,
+                   int64_t &bytes, uint32_t &ldb) __attribute__((always_inline)) {
     t = rstep(t);
     const int k0 = (s_begin + t) * BK + h * KW, c = k0 / BLK, kk = k0 % BLK;
-    const int64_t ob = out_blk(g);
     if constexpr (DENSE) {
       ldb = (uint32_t)(a.ldb * 2);
       base = BKN ? B + ((int64_t)c * BLK + kk) * a.ldb + ob * BLK
@@ -225,6 +225,15 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
     }
   }
 
+  constexpr int PPW = BWW > WPP ? BWW / WPP : 1;  // pieces per wave
+  constexpr int WIN = BWW > WPP ? WPP : BWW;      // windows per piece and wave
+  // Output block of each of this wave's B pieces (fixed for the tile).
+  int64_t ob_w[PPW];
+  sfor<PPW>([&](auto pi) __attribute__((always_inline)) {
+    const int piece = __builtin_amdgcn_readfirstlane((w * BWW + pi * WIN) / WPP);
+    ob_w[pi] = out_blk(piece / NH);
+  });
+
   // Issue this wave's copies of step t into stage st.
   auto issue = [&](int t, Stage st) __attribute__((always_inline)) {
     {
@@ -242,8 +251,6 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
               (uint32_t)(wr * RPWA) * ldb + colb);
       });
     }
-    constexpr int PPW = BWW > WPP ? BWW / WPP : 1;  // pieces per wave
-    constexpr int WIN = BWW > WPP ? WPP : BWW;      // windows per piece and wave
     sfor<PPW>([&](auto pi) __attribute__((always_inline)) {
       const int wb0 = w * BWW + pi * WIN;
       // Uniform; readfirstlane lets the block lookups stay scalar loads.
@@ -251,7 +258,7 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       const bf16_t *base;
       int64_t bytes;
       uint32_t ldb;
-      b_src(t, piece / NH, piece % NH, base, bytes, ldb);
+      b_src(t, piece / NH, piece % NH, ob_w[pi], base, bytes, ldb);
       const rsrc_t r = make_rsrc(base, bytes);
       const uint32_t vrow = b_row * ldb;
       sfor<WIN>([&](auto i) __attribute__((always_inline)) {

@@ -287,6 +287,9 @@ def test_large_layer_T4096_all_outputs(b):
     print(f"[plan b={b} T={T}] {plan}", flush=True)
     assert plan["lowrank_t_kernel"] == 2 and plan["lowrank_t_split"] > 1, plan
     assert plan["lowrank_s_kernel"] == 2 and plan["lowrank_s_split"] > 1, plan
+    # S = dY U is 16384 deep: 256 x 256 tiles (T_lr, 4096 deep, 128 x 128).
+    assert (plan["lowrank_s_tile_m"], plan["lowrank_s_tile_n"]) == (256, 256), plan
+    assert (plan["lowrank_t_tile_m"], plan["lowrank_t_tile_n"]) == (128, 128), plan
     if b == 128:
         # 256 x 256 weight-gradient tiles: whole items, then items shared by
         # several workgroups, summed from their partial slots by a second pass.
@@ -355,6 +358,7 @@ def test_large_layer_full_size_sampled(large_full_inputs, b):
     print(f"[plan b={b} T={T}] {plan}", flush=True)
     assert plan["lowrank_t_kernel"] == 2 and plan["lowrank_s_kernel"] == 2, plan
     assert plan["tn_tile"] == (256 if b == 128 else 128), plan
+    assert (plan["lowrank_s_tile_n"], plan["lowrank_s_split"]) == (256, 4), plan
     M, (row_ptr, col_idx, *_x) = om.layout(n_out, n_in, b, ms)
     nnzb = int(M.sum())
     W, Wr = synth.draw((nnzb, b, b), 0.02, 0, 2, "bf16")
