@@ -382,6 +382,46 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   sfor<G>([&](auto gg) __attribute__((always_inline)) { if (gcol == gg) obg = ob[gg]; });
   const int64_t col = (int64_t)obg * BLK + cn % BLK;
   const bool col_ok = gcol < g_valid;
+  // Plain bf16 outputs of the block-sparse products (no GELU, no split
+  // partials): round to bf16 first and stage half the bytes.  A staged row
+  // is 64 columns = 16 units of 4 columns (8 bytes); lane l writes unit
+  // u = tn*8 + q*2 + l/32 of row l%32 at unit position u ^ (row & 15), so
+  // the 16 rows of a half-wave fill 16 different bank pairs.  A reader of
+  // 8 columns (units 2j, 2j + 1) finds them in one 16-byte chunk, in order
+  // when row & 1 is 0 and swapped when it is 1.  Same rounding as the fp32
+  // path: each value is rounded once, after the mixing-weight scale.
+  constexpr bool BF16_STAGE = !DENSE && EPI == 0;
+  if constexpr (BF16_STAGE) {
+    constexpr int SROW2 = WTN * 2;
+    static_assert(SROW2 == 128 && 32 * SROW2 <= SLICE, "bf16 staging");
+    sfor<TM>([&](auto tm) __attribute__((always_inline)) {
+      const int r = lane & 31;
+      sfor<TN>([&](auto tn) __attribute__((always_inline)) {
+        sfor<4>([&](auto q) __attribute__((always_inline)) {
+          float v0 = acc[tn][tm][q * 4 + 0], v1 = acc[tn][tm][q * 4 + 1];
+          float v2 = acc[tn][tm][q * 4 + 2], v3 = acc[tn][tm][q * 4 + 3];
+          if (a.mix) {
+            v0 *= a.mix_out;
+            v1 *= a.mix_out;
+            v2 *= a.mix_out;
+            v3 *= a.mix_out;
+          }
+          const int u = tn * 8 + q * 2 + (lane >> 5);
+          *(u32x2 *)(stg + r * SROW2 + ((u ^ (r & 15)) << 3)) =
+              u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+        });
+      });
+      sfor<32 / RPI>([&](auto it) __attribute__((always_inline)) {
+        const int rr = it * RPI + rl, sw = rr & 15;
+        u32x4 v = *(const u32x4 *)(stg + rr * SROW2 + ((((2 * jl) ^ sw) >> 1) << 4));
+        if (sw & 1) v = u32x4{v[2], v[3], v[0], v[1]};
+        const int64_t gm = m0 + wm * WTM + tm * 32 + rr;
+        if (gm >= a.M || !col_ok) return;
+        *(u32x4 *)(C + gm * a.ldc + col) = v;
+      });
+    });
+    return;
+  }
   sfor<TM * (32 / SP)>([&](auto pass) __attribute__((always_inline)) {
     constexpr int tm = pass / (32 / SP), half = pass % (32 / SP);
     if ((lane & 31) / SP == half) {
