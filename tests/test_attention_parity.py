@@ -100,3 +100,9 @@ def test_attention_global_rows_shorter_than_groups():
     """Two key blocks per row: two of the four groups of the forward / dQ
     kernels own no block and must contribute nothing."""
     _run(1, 2, 128, 2, heads=[(0, 0), (0, 1)], g=1)
+
+
+def test_attention_single_block_sequence():
+    """Sequence of one 64-row block (every row keeps exactly one block, the
+    prefetched next-block index clamps onto it), five heads."""
+    _run(1, 5, 64, 1, heads=[(0, 0), (0, 4)])
