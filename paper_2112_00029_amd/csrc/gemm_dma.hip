@@ -22,9 +22,11 @@
 //    epilogue transposes each wave's tile through LDS so that every store
 //    covers whole 128-byte row segments.
 //
-// Tile: BM tokens x BN = G * BLK output columns, 4 waves as 2 x 2.  The
-// virtual K range of a tile is its kept blocks, then the r / BLK low-rank
-// blocks, then zero padding to a multiple of BK.
+// Tile: BM tokens x BN = G * BLK output columns, NW = 4 or 8 waves of 64
+// output columns each by BM / (NW / (BN / 64)) tokens (the configurations
+// are listed above ntd_cfg).  The virtual K range of a tile is its kept
+// blocks, then the r / BLK low-rank blocks, then zero padding to a multiple
+// of BK.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -354,8 +356,9 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
   // and, for q = 0..3, output columns tn*32 + q*8 + (l/32)*4 + 0..3.  Full
   // 128-byte row segments store far faster than 8-byte pieces scattered
   // over 32 rows, so each wave transposes its tile through LDS, 32 rows at a
-  // time (fp32, 16-byte chunks XOR-swizzled by row), and every lane then
-  // writes 8 consecutive columns of one row.  The staging area is the stage
+  // time (fp32 values in 16-byte chunks XOR-swizzled by row; plain bf16
+  // outputs are rounded first and staged as bf16, see below), and every
+  // lane then writes 8 consecutive columns of one row.  The staging area is the stage
   // buffer no wave reads in the last step; it needs no barrier because each
   // wave only touches its own slice and a wave's LDS accesses are ordered.
   constexpr int SROW = WTN * 4, SCH = SROW / 16;  // staged row bytes, chunks
