@@ -116,6 +116,9 @@ CASES = [
     # 512-token tiles (128-column outputs with 512+ workgroups)
     pytest.param(4096, 4096, 128, 32, 8000, 128, "bf16", id="b128_4096sq_T8000_tall"),
     pytest.param(16384, 4096, 128, 32, 200, 256, "bf16", id="large_b128_T200"),
+    # S = dY U 8256 deep with r = 512: two 256-wide columns of the split
+    # 256 x 256 rank-r tiles, ragged last token tile
+    pytest.param(8256, 1024, 64, 16, 2100, 512, "bf16", id="deep_S_r512_T2100"),
     pytest.param(16384, 4096, 64, 32, 200, 256, "bf16", id="large_b64_T200"),
     pytest.param(16384, 4096, 32, 32, 200, 256, "bf16", id="large_b32_T200"),
     # rank-r kernel edges: r = 32 (half of a 64-column tile past r), K and N
