@@ -420,7 +420,11 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
         if (sw & 1) v = u32x4{v[2], v[3], v[0], v[1]};
         const int64_t gm = m0 + wm * WTM + tm * 32 + rr;
         if (gm >= a.M || !col_ok) return;
-        *(u32x4 *)(C + gm * a.ldc + col) = v;
+        // Streaming store: the output is not read again by this launch, and
+        // keeping it out of the caches leaves them to the operands (16384 x
+        // 4096 step at b = 128: 1.754 -> 1.730 ms; S = dY U, which follows,
+        // 158 -> 146 us).
+        __builtin_nontemporal_store(v, (u32x4 *)(C + gm * a.ldc + col));
       });
     });
     return;
