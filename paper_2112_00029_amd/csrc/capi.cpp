@@ -349,6 +349,7 @@ struct TNPlan {
   // partial slots by a second pass).
   bool wide = false;
   int shared = 0;
+  int grid = 0;  // 256 x 256 kernel: workgroups
 };
 
 // row_bytes: the largest operand row stride in bytes.
@@ -415,7 +416,11 @@ bool tn_wide(const pf_layout *L, int dtype, int64_t T, int32_t r, bool mixed) {
   pf::TNArgs w{};
   w.n_items = (int)L->tn_items_w.size();
   fill_tn_regions(w, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
-  if (pf::tn_items_total(w, L->b, pf::kTNWTile) < pf::kTNWGrid) return false;
+  // Fewer items than workgroups run one workgroup per item (no shared
+  // items, no second pass) while they still fill three quarters of the CUs:
+  // at 16384 x 4096, b = 64 (208 items) that took the weight gradient from
+  // 475 us on the 128 x 128 kernel (4 token splits + reduction) to 402 us.
+  if (pf::tn_items_total(w, L->b, pf::kTNWTile) < pf::kTNWMinItems) return false;
   const int64_t row_bytes = std::max<int64_t>({L->n_out, L->n_in, (int64_t)r}) * 2;
   // Copies run up to seven 32-token steps past a segment (read as zeros).
   if ((T + 512) * row_bytes > 0x7fffffffLL) return false;
@@ -426,12 +431,14 @@ bool tn_wide(const pf_layout *L, int dtype, int64_t T, int32_t r, bool mixed) {
 }
 
 // Plan of the 256 x 256 kernel over `items` work items: kTNWGrid
-// workgroups; the items past the last full round are shared.  Workspace:
-// two fp32 partial slots of 256 x 256 per workgroup.
+// workgroups (one per item when there are fewer items); the items past the
+// last full round are shared.  Workspace: two fp32 partial slots of
+// 256 x 256 per workgroup.
 TNPlan tn_plan_wide(int items, int64_t T) {
   TNPlan p{1, ((T + 63) / 64) * 64, 0};
   p.wide = true;
-  p.shared = items % pf::kTNWGrid;
+  p.grid = std::min(items, pf::kTNWGrid);
+  p.shared = items % p.grid;
   if (p.shared > 0)
     p.ws = (size_t)2 * pf::kTNWGrid * pf::kTNWTile * pf::kTNWTile * sizeof(float);
   return p;
@@ -1225,7 +1232,7 @@ pf_status enqueue_tn(const pf_layout *L, int dt, pf::TNArgs a, const TNPlan &p, 
   if (p.wide) {
     {
       Timed t(PF_KERNEL_SDDMM, s);
-      pf_status st = hip_status(pf::launch_tnw(L->b, pf::kTNWGrid, a, s), "weight-gradient kernel");
+      pf_status st = hip_status(pf::launch_tnw(L->b, p.grid, a, s), "weight-gradient kernel");
       if (st != PF_OK || p.shared <= 0) return st;
     }
     Timed t(PF_KERNEL_REDUCE, s);

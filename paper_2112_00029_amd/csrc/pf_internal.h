@@ -186,8 +186,10 @@ hipError_t launch_reduce_rows(int dtype, int nsplit, const float *P, int64_t M, 
 hipError_t launch_tn(int dtype, int blk, const TNArgs &a, hipStream_t s);
 hipError_t launch_tn_reduce(int dtype, int blk, const TNArgs &a, hipStream_t s);
 // bf16 weight gradient on 256 x 256 tiles (blk 64 or 128) on kTNWGrid
-// workgroups (gemm_tnw.hip), and the pass that sums its `shared` items.
+// workgroups, or one per item when fewer (gemm_tnw.hip), and the pass that
+// sums its `shared` items.
 constexpr int kTNWGrid = 256;
+constexpr int kTNWMinItems = 192;  // fewest items the 256 x 256 kernel takes
 constexpr int kTNWTile = 256;
 hipError_t launch_tnw(int blk, int grid, const TNArgs &a, hipStream_t s);
 hipError_t launch_tnw_reduce(int blk, int shared, const TNArgs &a, hipStream_t s);

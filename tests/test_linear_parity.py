@@ -297,13 +297,18 @@ def test_large_layer_T4096_all_outputs(b):
         # 256 x 256 weight-gradient tiles: whole items, then items shared by
         # several workgroups, summed from their partial slots by a second pass.
         assert plan["tn_tile"] == 256 and plan["tn_split"] == 1 and plan["tn_shared"] > 0, plan
+    elif b == 64:
+        # 208 items of 256 x 256, fewer than the 256 workgroups: one
+        # workgroup per item, nothing shared, no second pass.
+        assert plan["tn_tile"] == 256 and plan["tn_items"] == 208 and plan["tn_shared"] == 0, plan
     else:
         assert plan["tn_tile"] == 128 and plan["tn_items"] >= 512 and plan["tn_split"] > 1, plan
     inp = _inputs(n_out, n_in, b, ms, T, r, "bf16")
     out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", inp["raw"], timing=True)
     # T_lr and S split their K range; the weight gradient splits its tokens
-    # (128 x 128) or shares items between workgroups (256 x 256).
-    assert _reductions(kt) == 3, kt
+    # (128 x 128) or shares items between workgroups (256 x 256), except
+    # with one workgroup per item (b = 64: no second pass).
+    assert _reductions(kt) == (2 if b == 64 else 3), kt
     got = {k: to_host(v) for k, v in out.items()}
     ref = _oracle(inp, r, b)
     ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
@@ -311,20 +316,23 @@ def test_large_layer_T4096_all_outputs(b):
         check_close(k, got[k], ref[k], "bf16")
 
 
-@pytest.mark.parametrize("T,r", [(2509, 256), (2049, 256), (2509, 128)])
-def test_large_layer_ragged_T_wide_weight_gradient(T, r):
+@pytest.mark.parametrize("T,r,b", [(2509, 256, 128), (2049, 256, 128), (2509, 128, 128),
+                                   (2509, 256, 64), (2049, 128, 64)])
+def test_large_layer_ragged_T_wide_weight_gradient(T, r, b):
     """The 16384 x 4096 layer at b = 128 with a token count that is not a
     multiple of the 32-token step: the 256 x 256 weight gradient's segments
     end inside a step (rows past T read as zeros) and the shares of the 16
     remaining items start mid-item.  At r = 128 the dU and dV tiles are half
     empty (one 128-column or 128-row block of the 256 x 256 tile), so waves
     whose quarter holds nothing skip their MFMAs and the stores drop the
-    empty half.  Every output element against the oracle."""
+    empty half.  At b = 64 (208 items, one workgroup per item) every item
+    runs whole over the ragged token range.  Every output element against
+    the oracle."""
     from paper_2112_00029_amd import pixelfly as pf
-    n_out, n_in, ms, b = LARGE["n_out"], LARGE["n_in"], LARGE["ms"], 128
+    n_out, n_in, ms = LARGE["n_out"], LARGE["n_in"], LARGE["ms"]
     plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
     print(f"[plan b={b} T={T}] {plan}", flush=True)
-    assert plan["tn_tile"] == 256 and plan["tn_shared"] > 0, plan
+    assert plan["tn_tile"] == 256 and (plan["tn_shared"] > 0) == (b == 128), plan
     inp = _inputs(n_out, n_in, b, ms, T, r, "bf16")
     out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", inp["raw"], timing=True)
     assert kt["sddmm"][0] == 1, kt
@@ -360,7 +368,7 @@ def test_large_layer_full_size_sampled(large_full_inputs, b):
     plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
     print(f"[plan b={b} T={T}] {plan}", flush=True)
     assert plan["lowrank_t_kernel"] == 2 and plan["lowrank_s_kernel"] == 2, plan
-    assert plan["tn_tile"] == (256 if b == 128 else 128), plan
+    assert plan["tn_tile"] == (256 if b in (128, 64) else 128), plan
     assert (plan["lowrank_s_tile_n"], plan["lowrank_s_split"]) == (256, 4), plan
     M, (row_ptr, col_idx, *_x) = om.layout(n_out, n_in, b, ms)
     nnzb = int(M.sum())

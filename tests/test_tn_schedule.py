@@ -41,7 +41,8 @@ def segments(I, S, G):
     return out
 
 
-CASES = [(272, 256, 256), (272, 64, 256), (208, 256, 256), (208, 64, 256), (1, 1, 256),
+CASES = [(272, 256, 256), (272, 64, 256), (208, 256, 256), (208, 64, 256), (208, 512, 208),
+         (192, 33, 192), (1, 1, 256),
          (3, 2, 256), (255, 7, 256), (256, 5, 256), (257, 5, 256), (513, 33, 256),
          (1000, 129, 256), (17, 1000, 256), (64, 128, 256), (5, 3, 8)]
 
