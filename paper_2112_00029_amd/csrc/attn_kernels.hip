@@ -52,6 +52,28 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // top of the loop as well.
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x70); }
 
+// x combined with the value of lane l ^ 16 (l ^ 32) by max or +: the two
+// swaps exchange rows of 16 (halves of 32) lanes inside the VALU, where a
+// lane shuffle would make a round trip through the LDS.  Each lane gets its
+// own and its partner's value in some order, so max and + give the same bits
+// in both lanes and as the shuffle form.
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float add_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ float bf2f_a(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 __device__ __forceinline__ bf16_t f2bf_a(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
@@ -204,8 +226,7 @@ __global__ __launch_bounds__(256 * NG) void attn_fwd_kernel(AttnArgs a) {
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
         for (int j = 0; j < 4; ++j) bmax = fmaxf(bmax, s[mt][j]);
-      bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
-      bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+      bmax = max_xor32(max_xor16(bmax));
       // The softmax reference m_run moves only when some row's maximum grew
       // by more than 8 (log2 units): until then the probabilities stay below
       // 2^8 and the rescale of O and l, a wave-uniform branch, is skipped.
@@ -228,8 +249,7 @@ __global__ __launch_bounds__(256 * NG) void attn_fwd_kernel(AttnArgs a) {
           s[mt][j] = e;
           rs += e;
         }
-      rs += __shfl_xor(rs, 16);
-      rs += __shfl_xor(rs, 32);
+      rs = add_xor32(add_xor16(rs));
       l_run += rs;
       // O^T[dim][query] += V^T[dim][key] P^T[key][query]
       const bf16x8 pb0 = pack_perm(s[0], s[1]), pb1 = pack_perm(s[2], s[3]);
