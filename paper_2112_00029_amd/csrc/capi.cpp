@@ -186,9 +186,17 @@ NTChoice nt_choose(int dtype, int blk, int G, int bm, int kmax, int64_t M, int n
   return NTChoice{true, pf::NTD_DEFAULT, 256, w};  // 256 x 256 and 256 x 64 tiles
 }
 
+// Output tiles per band of the forward's workgroup order: one band per XCD
+// once there are 64 or more output tiles (fewer: the token-tile groups).
+int nt_band(bool dense, bool b_kn, int ntiles) {
+  return !dense && !b_kn && ntiles >= 64 ? (ntiles + 7) / 8 : 0;
+}
+
 hipError_t nt_launch(pf_kernel_class kc, int dtype, int blk, int G, bool b_kn, int bm, int kmax,
-                     const pf::NTArgs &a, hipStream_t s) {
+                     const pf::NTArgs &a_in, hipStream_t s) {
   Timed t(kc, s);
+  pf::NTArgs a = a_in;
+  a.band = nt_band(a.dense != 0, b_kn, a.ntiles);
   const NTChoice c = nt_choose(dtype, blk, G, bm, kmax, a.M, a.ntiles, a.nsplit, a.dense != 0);
   if (c.dma) return pf::launch_ntd(blk, G, b_kn, c.variant, a, s);
   return pf::launch_nt(dtype, blk, G, b_kn, bm, a, s);

@@ -80,6 +80,11 @@ struct NTArgs {
   // mix_out = beta (or mix_out = alpha with no low-rank blocks).
   int mix;
   float mix_ratio, mix_out;
+  // Workgroup order of a block-sparse launch with B read [n][k] (forward):
+  // 0 walks groups of token tiles over all output tiles; band > 0 walks
+  // bands of `band` output tiles, each over all token tiles in groups of
+  // four, so that the workgroups of one XCD share one band's weight blocks.
+  int band;
 };
 
 // A dense region of the TN kernel: out[a][b] = sum_t A[t][a] B[t][b] over

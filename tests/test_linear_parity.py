@@ -120,6 +120,9 @@ CASES = [
     # 256 x 256 rank-r tiles, ragged last token tile
     pytest.param(8256, 1024, 64, 16, 2100, 512, "bf16", id="deep_S_r512_T2100"),
     pytest.param(16384, 4096, 64, 32, 200, 256, "bf16", id="large_b64_T200"),
+    # forward in bands of output tiles (64+ tiles): 68 tiles of 128 columns
+    # in bands of 9 (the last of 5), 5 token tiles (a last group of one)
+    pytest.param(8320, 512, 32, 16, 600, 64, "bf16", id="band_ragged_N8320_T600"),
     pytest.param(16384, 4096, 32, 32, 200, 256, "bf16", id="large_b32_T200"),
     # rank-r kernel edges: r = 32 (half of a 64-column tile past r), K and N
     # = 32 mod 64 (the last 64-wide step half outside), 3 steps for 4 waves
