@@ -476,7 +476,8 @@ typedef enum {
   PF_KERNEL_SDDMM = 2,          /* weight gradient on the mask, dU, dV */
   PF_KERNEL_LOWRANK_T = 3,      /* rank-r product T_lr = X V^T */
   PF_KERNEL_LOWRANK_S = 4,      /* rank-r product S = dY U */
-  PF_KERNEL_REDUCE = 5,         /* sums of split partial results */
+  PF_KERNEL_REDUCE = 5,         /* sums of split partial results; the b = 32
+                                   backward-data pair-block gather */
   PF_KERNEL_GELU_BWD = 6,       /* standalone GELU backward */
   PF_KERNEL_ATTN_FWD = 7,
   PF_KERNEL_ATTN_BWD_DQ = 8,    /* dQ (and the row terms delta) */

@@ -26,7 +26,8 @@ ARCH = "gfx950"
 SOURCES = (
     [("layout.cpp", "layout", ()), ("capi.cpp", "capi", ()),
      ("skinny.hip", "skinny", ()), ("attn_kernels.hip", "attn_kernels", ()),
-     ("butterfly.hip", "butterfly", ()), ("gemm_tnw.hip", "gemm_tnw", ())]
+     ("butterfly.hip", "butterfly", ()), ("gemm_tnw.hip", "gemm_tnw", ()),
+     ("pairs.hip", "pairs", ())]
     + [("gemm_kernels.hip", f"gemm_kernels_p{p}", (f"PF_GK_PART={p}",)) for p in range(7)]
     + [("gemm_dma.hip", f"gemm_dma_b{b}_{k}", (f"PF_PART_BLK={b}", f"PF_PART_BKN={k}"))
        for b in (32, 64, 128) for k in (0, 1)]

@@ -489,6 +489,20 @@ NTList bwd_list(const pf_layout *L, int dt, int64_t T) {
                 L->d_kcols_bwd, L->d_blks_bwd};
 }
 
+// b = 32 backward-data on 64-wide pair tiles (bf16, no two block columns
+// sharing their kept rows, rank a multiple of 64, T x K of 4M or more): the
+// 32-wide tiles read dY in half 128-byte row segments; the pair tiles read
+// whole ones and multiply the dropped blocks of each pair block as zeros
+// (16384 x 4096: 468 -> 276 us plus a 5 us gather).  Small products do not
+// repay the gather launch (2048 tokens x 1024: 7.0 -> 8.7 + 4.4 us).
+bool use_bwd_pairs(const pf_layout *L, int dt, int64_t T, int32_t r) {
+  return dt == PF_BF16 && !L->bwd_tiles_p.empty() && L->G_bwd == 1 && L->G_bwd_w == 1 &&
+         r % 64 == 0 && T * L->n_in >= ((int64_t)1 << 22);
+}
+size_t pair_ws_bytes(const pf_layout *L, int dt, int64_t T, int32_t r) {
+  return use_bwd_pairs(L, dt, T, r) ? (L->pair_src.size() / 4) * 64 * 64 * 2 : 0;
+}
+
 void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
                      const void *X, const void *T_lr, const void *S, void *dU, void *dV) {
   a.n_dense = 0;
@@ -821,6 +835,8 @@ pf_status pf_layout_upload(pf_layout *L, void *stream) {
       vec(L->kcols_fwd_w, L->d_kcols_fwd_w), vec(L->blks_fwd_w, L->d_blks_fwd_w),
       vec(L->kcols_bwd_w, L->d_kcols_bwd_w), vec(L->blks_bwd_w, L->d_blks_bwd_w),
       vec(L->tn_items, L->d_tn_items),       vec(L->tn_items_w, L->d_tn_items_w),
+      vec(L->bwd_tiles_p, L->d_bwd_tiles_p), vec(L->kcols_bwd_p, L->d_kcols_bwd_p),
+      vec(L->blks_bwd_p, L->d_blks_bwd_p),   vec(L->pair_src, L->d_pair_src),
       vec(L->row_ptr, L->d_row_ptr),
       vec(L->col_idx, L->d_col_idx),         vec(L->col_ptr, L->d_col_ptr),
       vec(L->row_idx, L->d_row_idx)};
@@ -885,7 +901,9 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
     tnw = tn_plan_wide(pf::tn_items_total(w, L->b, pf::kTNWTile), T).ws;
   }
   const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
-  const size_t bwd = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
+  const size_t sws = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
+  const size_t pws = pair_ws_bytes(L, (int)dtype, T, r);
+  const size_t bwd = pws ? align256(sws) + pws : sws;
   return std::max({tn, tnw, fwd, bwd}) + mix_dgamma_bytes(items);
 }
 
@@ -931,7 +949,10 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   p.lowrank_s_tile_n = sv[3];
   const NTList f = fwd_list(L, dt, T), g = bwd_list(L, dt, T);
   const NTChoice cf = nt_choose(dt, b, f.G, 128, f.kmax + r / b, T, f.ntiles, 1, false);
-  const NTChoice cg = nt_choose(dt, b, g.G, 128, g.kmax + r / b, T, g.ntiles, 1, false);
+  const NTChoice cg =
+      use_bwd_pairs(L, dt, T, r)
+          ? nt_choose(dt, 64, 1, 128, L->kmax_bwd_p + r / 64, T, (int)L->bwd_tiles_p.size(), 1, false)
+          : nt_choose(dt, b, g.G, 128, g.kmax + r / b, T, g.ntiles, 1, false);
   p.fwd_tile_m = cf.bm;
   p.fwd_tile_n = cf.bn;
   p.fwd_direct_lds = cf.dma;
@@ -1116,10 +1137,11 @@ pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void
                   L->nb_out, r / b, S, r, sp.nsplit, ws, s, "S kernel");
 }
 
-// dX = dY (M o W) + S V (optionally times gelu'(aux)).
+// dX = dY (M o W) + S V (optionally times gelu'(aux)).  pair_ws: room for
+// the pair blocks when use_bwd_pairs holds (pair_ws_bytes).
 pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const void *dY,
                      const void *Wblk, const void *S, const void *V, void *dX, pf_epilogue epi,
-                     const void *aux, hipStream_t s, const Mix &mix = kNoMix) {
+                     const void *aux, void *pair_ws, hipStream_t s, const Mix &mix = kNoMix) {
   const int b = L->b;
   pf::NTArgs a{};
   a.A = dY; a.lda = L->n_out;
@@ -1129,6 +1151,26 @@ pf_status enqueue_dx(const pf_layout *L, int dt, int64_t T, int32_t r, const voi
   a.aux = aux;
   a.epi = (int)epi;
   a.M = T;
+  if (use_bwd_pairs(L, dt, T, r)) {
+    const int npair = (int)(L->pair_src.size() / 4);
+    {
+      Timed t(PF_KERNEL_REDUCE, s);
+      pf_status st = hip_status(pf::launch_pair_gather(Wblk, L->d_pair_src, npair, pair_ws, s),
+                                "pair gather kernel");
+      if (st != PF_OK) return st;
+    }
+    a.B = pair_ws;
+    a.nlr = r / 64;
+    a.tiles = L->d_bwd_tiles_p;
+    a.ntiles = (int)L->bwd_tiles_p.size();
+    a.kcols = L->d_kcols_bwd_p;
+    a.blks = L->d_blks_bwd_p;
+    a.nsplit = 1;
+    set_mix(a, mix);
+    return hip_status(nt_launch(PF_KERNEL_SPMM_BWD_DATA, dt, 64, 1, true, 128,
+                                L->kmax_bwd_p + a.nlr, a, s),
+                      "backward-data kernel");
+  }
   const NTList tl = bwd_list(L, dt, T);
   a.tiles = tl.tiles;
   a.ntiles = tl.ntiles;
@@ -1267,11 +1309,13 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   pf_status st = check_bwd_data_args(L, dtype, T, r, dY, Wblk, U, V, S, dX, epi, aux);
   if (st != PF_OK) return st;
   const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
-  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
+  const size_t pws = pair_ws_bytes(L, (int)dtype, T, r);
+  if ((st = need_ws(pws ? align256(sp.ws) + pws : sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   if ((st = enqueue_s(L, (int)dtype, T, r, dY, U, S, sp, (float *)workspace, s)) != PF_OK) return st;
-  return enqueue_dx(L, (int)dtype, T, r, dY, Wblk, S, V, dX, epi, aux, s);
+  return enqueue_dx(L, (int)dtype, T, r, dY, Wblk, S, V, dX, epi, aux,
+                    (char *)workspace + align256(sp.ws), s);
 }
 
 pf_status pf_linear_bwd_weight(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,
@@ -1296,12 +1340,13 @@ pf_status pf_linear_bwd_data_mixed(const pf_layout *L, pf_dtype dtype, int64_t T
   if (st != PF_OK) return st;
   if ((st = check_bwd_data_args(L, dtype, T, r, dY, Wblk, U, V, S, dX, epi, aux)) != PF_OK) return st;
   const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
-  if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
+  const size_t pws = pair_ws_bytes(L, (int)dtype, T, r);
+  if ((st = need_ws(pws ? align256(sp.ws) + pws : sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   if ((st = enqueue_s(L, (int)dtype, T, r, dY, U, S, sp, (float *)workspace, s)) != PF_OK) return st;
-  return enqueue_dx(L, (int)dtype, T, r, dY, Wblk, S, V, dX, epi, aux, s,
-                    Mix{true, gamma, 1.f - gamma});
+  return enqueue_dx(L, (int)dtype, T, r, dY, Wblk, S, V, dX, epi, aux,
+                    (char *)workspace + align256(sp.ws), s, Mix{true, gamma, 1.f - gamma});
 }
 
 pf_status pf_linear_bwd_weight_mixed(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r,

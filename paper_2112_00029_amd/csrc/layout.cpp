@@ -335,6 +335,39 @@ std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, 
   return finish_layout(L);
 }
 
+// Backward-data pair lists (see pf_layout): b = 32 and even block counts
+// only.  Pair rows of a pair column ascending.
+static void build_bwd_pairs(pf_layout &L) {
+  L.bwd_tiles_p.clear();
+  L.kcols_bwd_p.clear();
+  L.blks_bwd_p.clear();
+  L.pair_src.clear();
+  L.kmax_bwd_p = 0;
+  if (L.b != 32 || L.nb_out % 2 || L.nb_in % 2) return;
+  std::vector<int32_t> prs;
+  for (int32_t q = 0; q < L.nb_in / 2; ++q) {
+    prs.clear();
+    for (int32_t j = 2 * q; j < 2 * q + 2; ++j)
+      for (int32_t p = L.col_ptr[j]; p < L.col_ptr[j + 1]; ++p) prs.push_back(L.row_idx[p] / 2);
+    std::sort(prs.begin(), prs.end());
+    prs.erase(std::unique(prs.begin(), prs.end()), prs.end());
+    NTTile t{};
+    t.g = 1;
+    t.nsteps = (int32_t)prs.size();
+    t.kcol_off = (int32_t)L.kcols_bwd_p.size();
+    t.blk_off = (int32_t)L.blks_bwd_p.size();
+    for (int g = 0; g < kMaxG; ++g) t.out_blk[g] = g == 0 ? q : -1;
+    for (int32_t r : prs) {
+      L.kcols_bwd_p.push_back(r);
+      L.blks_bwd_p.push_back((int32_t)(L.pair_src.size() / 4));
+      for (int a = 0; a < 2; ++a)
+        for (int c = 0; c < 2; ++c) L.pair_src.push_back(csr_pos(L, 2 * r + a, 2 * q + c));
+    }
+    L.kmax_bwd_p = std::max(L.kmax_bwd_p, t.nsteps);
+    L.bwd_tiles_p.push_back(t);
+  }
+}
+
 // CSC, work lists and their self-check, from row_ptr / col_idx.
 std::string finish_layout(pf_layout &L) {
   L.nnzb = (int64_t)L.col_idx.size();
@@ -372,6 +405,7 @@ std::string finish_layout(pf_layout &L) {
       [&](int col, int c) { return L.tperm[L.col_ptr[col] + c]; }, L.G_bwd_w,
       L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w);
   build_tn_items(L);
+  build_bwd_pairs(L);
   L.kmax_fwd = L.kmax_bwd = 0;
   for (auto &t : L.fwd_tiles) L.kmax_fwd = std::max(L.kmax_fwd, (int)t.nsteps);
   for (auto &t : L.bwd_tiles) L.kmax_bwd = std::max(L.kmax_bwd, (int)t.nsteps);
@@ -408,6 +442,35 @@ std::string check_layout(const pf_layout &L) {
   if (!e.empty()) return "backward-data: " + e;
   e = sweep(L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w, L.G_bwd_w, true);
   if (!e.empty()) return "backward-data (wide): " + e;
+  if (!L.bwd_tiles_p.empty()) {
+    // Pair lists: each pair block's sources are the CSR positions of its
+    // four blocks, and every kept block is one pair block's source once.
+    std::fill(seen.begin(), seen.end(), 0);
+    if (L.bwd_tiles_p.size() != (size_t)(L.nb_in / 2)) return "backward-data pairs: tile count";
+    for (size_t q = 0; q < L.bwd_tiles_p.size(); ++q) {
+      const NTTile &t = L.bwd_tiles_p[q];
+      if (t.g != 1 || t.out_blk[0] != (int32_t)q) return "backward-data pairs: tile column";
+      for (int c = 0; c < t.nsteps; ++c) {
+        const int32_t r = L.kcols_bwd_p[t.kcol_off + c], pb = L.blks_bwd_p[t.blk_off + c];
+        if (r < 0 || 2 * r + 1 >= L.nb_out || pb < 0 || 4 * (size_t)pb + 3 >= L.pair_src.size())
+          return "backward-data pairs: index out of range";
+        int any = 0;
+        for (int a = 0; a < 2; ++a)
+          for (int h = 0; h < 2; ++h) {
+            const int32_t src = L.pair_src[4 * pb + 2 * a + h];
+            if (src != csr_pos(L, 2 * r + a, 2 * (int32_t)q + h))
+              return "backward-data pairs: block source mismatch";
+            if (src >= 0) {
+              seen[src]++;
+              any = 1;
+            }
+          }
+        if (!any) return "backward-data pairs: empty pair block";
+      }
+    }
+    for (int v : seen)
+      if (v != 1) return "backward-data pairs do not cover each kept block exactly once";
+  }
   auto items = [&](const std::vector<TNItem> &list, const char *what) -> std::string {
     std::fill(seen.begin(), seen.end(), 0);
     for (auto &it : list) {

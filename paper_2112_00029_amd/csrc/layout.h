@@ -32,6 +32,15 @@ struct pf_layout {
   // Weight-gradient items of the 256 x 256 bf16 kernel (b = 64 or 128):
   // bundles of 256 / b block rows x 256 / b block columns; empty otherwise.
   std::vector<pf::TNItem> tn_items_w;
+  // Backward-data in 64-wide pairs (b = 32 with even block counts): block
+  // rows and columns taken in aligned pairs (2i, 2i + 1), a 64 x 64 pair
+  // block kept when any of its four b x b blocks is.  One tile per pair
+  // column (kcols: its pair rows, blks: pair block indices); pair_src holds
+  // for each pair block the CSR positions of its blocks (row half * 2 +
+  // column half; -1 for a dropped block, read as zeros).  Empty otherwise.
+  std::vector<pf::NTTile> bwd_tiles_p;
+  std::vector<int32_t> kcols_bwd_p, blks_bwd_p, pair_src;
+  int kmax_bwd_p = 0;
 
   // Device copies (valid after pf_layout_upload).
   int device = -1;
@@ -43,6 +52,8 @@ struct pf_layout {
   const int32_t *d_kcols_fwd_w = nullptr, *d_blks_fwd_w = nullptr;
   const int32_t *d_kcols_bwd_w = nullptr, *d_blks_bwd_w = nullptr;
   const pf::TNItem *d_tn_items = nullptr, *d_tn_items_w = nullptr;
+  const pf::NTTile *d_bwd_tiles_p = nullptr;
+  const int32_t *d_kcols_bwd_p = nullptr, *d_blks_bwd_p = nullptr, *d_pair_src = nullptr;
   const int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
   const int32_t *d_col_ptr = nullptr, *d_row_idx = nullptr;
 };

@@ -159,6 +159,10 @@ struct AttnArgs {
 // M-tile (tokens per workgroup): 128, or 64 for the skinny rank-r products.
 hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs &a,
                      hipStream_t s);
+// b = 32 backward-data pairs: Wp[p] (64 x 64 bf16) from the blocks of W that
+// src[4p .. 4p + 3] name (-1: zeros).
+hipError_t launch_pair_gather(const void *W, const int32_t *src, int npair, void *Wp,
+                              hipStream_t s);
 // bf16 NT family with direct global -> LDS operand copies (gemm_dma.hip).
 // The output tile is G * blk = 64, 128 or 256 columns wide (the token tile
 // follows: 256, 128, 256).  For 128-column tiles `variant` picks 512-token

@@ -120,6 +120,9 @@ CASES = [
     # 256 x 256 rank-r tiles, ragged last token tile
     pytest.param(8256, 1024, 64, 16, 2100, 512, "bf16", id="deep_S_r512_T2100"),
     pytest.param(16384, 4096, 64, 32, 200, 256, "bf16", id="large_b64_T200"),
+    # b = 32 backward-data on 64-wide pair tiles (T x K >= 4M), ragged
+    # last token tile
+    pytest.param(2048, 1024, 32, 16, 4100, 64, "bf16", id="b32_pairs_T4100"),
     # forward in bands of output tiles (64+ tiles): 68 tiles of 128 columns
     # in bands of 9 (the last of 5), 5 token tiles (a last group of one)
     pytest.param(8320, 512, 32, 16, 600, 64, "bf16", id="band_ragged_N8320_T600"),
@@ -306,12 +309,16 @@ def test_large_layer_T4096_all_outputs(b):
         assert plan["tn_tile"] == 256 and plan["tn_items"] == 208 and plan["tn_shared"] == 0, plan
     else:
         assert plan["tn_tile"] == 128 and plan["tn_items"] >= 512 and plan["tn_split"] > 1, plan
+        # Backward-data on 64-wide pair tiles (no two 32-wide block columns
+        # share their kept rows), after the pair-block gather.
+        assert (plan["bwd_tile_n"], plan["bwd_direct_lds"]) == (64, 1), plan
     inp = _inputs(n_out, n_in, b, ms, T, r, "bf16")
     out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", inp["raw"], timing=True)
     # T_lr and S split their K range; the weight gradient splits its tokens
     # (128 x 128) or shares items between workgroups (256 x 256), except
-    # with one workgroup per item (b = 64: no second pass).
-    assert _reductions(kt) == (2 if b == 64 else 3), kt
+    # with one workgroup per item (b = 64: no second pass); b = 32 adds the
+    # pair-block gather.
+    assert _reductions(kt) == {128: 3, 64: 2, 32: 4}[b], kt
     got = {k: to_host(v) for k, v in out.items()}
     ref = _oracle(inp, r, b)
     ref["dW"] = _pack_ref(ref, n_out, n_in, b, ms)
@@ -379,7 +386,10 @@ def test_large_layer_full_size_sampled(large_full_inputs, b):
     raw = dict(inp["raw"], W=Wr)
     out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", raw, timing=True)
     splits = sum(int(plan[k] > 1) for k in ("lowrank_t_split", "lowrank_s_split", "tn_split"))
-    assert _reductions(kt) == splits + int(plan["tn_shared"] > 0), (kt, plan)
+    gather = int(b == 32)  # b = 32: backward-data on 64-wide pair tiles
+    if b == 32:
+        assert (plan["bwd_tile_n"], plan["bwd_direct_lds"]) == (64, 1), plan
+    assert _reductions(kt) == splits + int(plan["tn_shared"] > 0) + gather, (kt, plan)
 
     rng = np.random.default_rng([b, 77])
     edges = [0, 1, 127, 128, 255, 256, 511, 512, T // 2 - 1, T // 2, T - 512, T - 1]

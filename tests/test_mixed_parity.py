@@ -25,6 +25,8 @@ CASES = [
     pytest.param(1024, 4096, 64, 16, 520, 128, "bf16", 0.45, 0, id="b64_fc2_g0.45"),
     pytest.param(4096, 4096, 128, 32, 2048, 128, "bf16", 0.8, 0, id="b128_tall_g0.8"),
     pytest.param(1024, 1024, 32, 32, 256, 32, "fp32", 0.25, 0, id="fp32_g0.25"),
+    # b = 32 backward-data on 64-wide pair tiles, GELU epilogues
+    pytest.param(2048, 1024, 32, 16, 4100, 64, "bf16", 0.4, 1, id="b32_pairs_gelu_g0.4"),
 ]
 
 
@@ -80,14 +82,20 @@ def test_mixed_parity(n_out, n_in, b, ms, T, r, dtype, gamma, epi):
     assert eg <= tol
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
-def test_mixed_bwd_data_gelu_epilogue(dtype):
+@pytest.mark.parametrize("dtype,shape", [
+    ("bf16", (768, 3072, 32, 16, 700, 96)),
+    ("fp32", (768, 3072, 32, 16, 700, 96)),
+    # 64-wide pair tiles of b = 32 (T x K >= 4M), ragged last token tile
+    ("bf16", (2048, 1024, 32, 16, 4100, 64)),
+], ids=["bf16", "fp32", "bf16_pairs"])
+def test_mixed_bwd_data_gelu_epilogue(dtype, shape):
     """Backward-data of the mixed layer with the GELU-derivative epilogue:
     dX = (dY (gamma B) + (1 - gamma) (dY U) V) * gelu'(aux), the form the
     second layer of an MLP hands back through the activation."""
     torch = torch_cuda()
     from paper_2112_00029_amd import pixelfly as pf
-    n_out, n_in, b, ms, T, r, gamma = 768, 3072, 32, 16, 700, 96, 0.35
+    n_out, n_in, b, ms, T, r = shape
+    gamma = 0.35
     print(f"[mixed-gelu] {n_out}x{n_in} b={b} T={T} r={r} {dtype} gamma={gamma}", flush=True)
     std = (1.0, 1.0 / np.sqrt(6 * 32), 1.0 / 32, 1.0) if dtype == "fp32" else (0.02,) * 4
     inp = _inputs(n_out, n_in, b, ms, T, r, dtype, std=std)
