@@ -358,6 +358,10 @@ struct TNPlan {
   bool wide = false;
   int shared = 0;
   int grid = 0;  // 256 x 256 kernel: workgroups
+  // b = 32 on pair blocks (256 x 256 kernel as b = 64): the pair-block
+  // gradients go to the workspace at pair_off, then scatter into dW.
+  bool pairs = false;
+  size_t pair_off = 0;
 };
 
 // row_bytes: the largest operand row stride in bytes.
@@ -417,7 +421,8 @@ TNPlan tn_plan(int items, int64_t T, int64_t row_bytes, int64_t min_tokens = 512
 // neighbours, and the 128 x 128 kernel measured faster (the 16384 x 4096
 // layer at b = 64: 208 items, 540 against 466 us).
 void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
-                     const void *X, const void *T_lr, const void *S, void *dU, void *dV);
+                     const void *X, const void *T_lr, const void *S, void *dU, void *dV,
+                     int blk = 0);
 bool tn_wide(const pf_layout *L, int dtype, int64_t T, int32_t r, bool mixed) {
   if (dtype != 0 || mixed || (L->b != 64 && L->b != 128) || L->tn_items_w.empty()) return false;
   if (T < PF_WIDE_MIN_T) return false;
@@ -436,6 +441,21 @@ bool tn_wide(const pf_layout *L, int dtype, int64_t T, int32_t r, bool mixed) {
   int64_t slots = 0;
   for (auto &it : L->tn_items_w) slots += (int64_t)GT * it.nb;
   return L->nnzb * 5 >= slots * 4;
+}
+
+// b = 32 weight gradient on the pair blocks (T x K of 4M or more, rank a
+// multiple of 64, the 256 x 256 item count of b = 64): the 32-token steps of
+// the 128 x 128 kernel read 64-byte row halves of both operands; the pair
+// items read whole 128-byte segments and compute the dropped quarters too.
+bool tn_pairs(const pf_layout *L, int dtype, int64_t T, int32_t r, bool mixed) {
+  if (dtype != 0 || mixed || L->b != 32 || L->tn_items_p.empty() || r % 64) return false;
+  if (T < PF_WIDE_MIN_T || T * L->n_in < ((int64_t)1 << 22)) return false;
+  pf::TNArgs w{};
+  w.n_items = (int)L->tn_items_p.size();
+  fill_tn_regions(w, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 64);
+  if (pf::tn_items_total(w, 64, pf::kTNWTile) < pf::kTNWMinItems) return false;
+  const int64_t row_bytes = std::max<int64_t>({L->n_out, L->n_in, (int64_t)r}) * 2;
+  return (T + 512) * row_bytes <= 0x7fffffffLL;
 }
 
 // Plan of the 256 x 256 kernel over `items` work items: kTNWGrid
@@ -503,12 +523,15 @@ size_t pair_ws_bytes(const pf_layout *L, int dt, int64_t T, int32_t r) {
   return use_bwd_pairs(L, dt, T, r) ? (L->pair_src.size() / 4) * 64 * 64 * 2 : 0;
 }
 
+// blk: block size of the regions' tiling (0: the layout's).
 void fill_tn_regions(pf::TNArgs &a, const pf_layout *L, int32_t r, const void *dY,
-                     const void *X, const void *T_lr, const void *S, void *dU, void *dV) {
+                     const void *X, const void *T_lr, const void *S, void *dU, void *dV,
+                     int blk) {
+  const int b = blk ? blk : L->b;
   a.n_dense = 0;
   if (r > 0) {
-    a.dr[0] = pf::TNDense{dY, L->n_out, T_lr, r, dU, r, L->nb_out, r / L->b};
-    a.dr[1] = pf::TNDense{S, r, X, L->n_in, dV, L->n_in, r / L->b, L->nb_in};
+    a.dr[0] = pf::TNDense{dY, L->n_out, T_lr, r, dU, r, (int)(L->n_out / b), r / b};
+    a.dr[1] = pf::TNDense{S, r, X, L->n_in, dV, L->n_in, r / b, (int)(L->n_in / b)};
     a.n_dense = 2;
   }
 }
@@ -837,6 +860,7 @@ pf_status pf_layout_upload(pf_layout *L, void *stream) {
       vec(L->tn_items, L->d_tn_items),       vec(L->tn_items_w, L->d_tn_items_w),
       vec(L->bwd_tiles_p, L->d_bwd_tiles_p), vec(L->kcols_bwd_p, L->d_kcols_bwd_p),
       vec(L->blks_bwd_p, L->d_blks_bwd_p),   vec(L->pair_src, L->d_pair_src),
+      vec(L->tn_items_p, L->d_tn_items_p),
       vec(L->row_ptr, L->d_row_ptr),
       vec(L->col_idx, L->d_col_idx),         vec(L->col_ptr, L->d_col_ptr),
       vec(L->row_idx, L->d_row_idx)};
@@ -894,11 +918,11 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
   // not apply) and, where it applies, the 256 x 256 one.
   const size_t tn = tn_plan(items, T, std::max(L->n_out, L->n_in) * es, tn_min_tokens(dtype)).ws;
   size_t tnw = 0;
-  if (tn_wide(L, (int)dtype, T, r, false)) {
-    pf::TNArgs w{};
-    w.n_items = (int)L->tn_items_w.size();
-    fill_tn_regions(w, L, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr);
-    tnw = tn_plan_wide(pf::tn_items_total(w, L->b, pf::kTNWTile), T).ws;
+  if (tn_wide(L, (int)dtype, T, r, false) || tn_pairs(L, (int)dtype, T, r, false)) {
+    TNPlan wp;
+    (void)tn_args(L, dtype, T, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                  &wp);
+    tnw = wp.ws;
   }
   const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
   const size_t sws = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
@@ -962,7 +986,7 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   TNPlan tp;
   const pf::TNArgs a =
       tn_args(L, dtype, T, r, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, &tp);
-  p.tn_items = pf::tn_items_total(a, b, tp.wide ? pf::kTNWTile : 128);
+  p.tn_items = pf::tn_items_total(a, tp.pairs ? 64 : b, tp.wide ? pf::kTNWTile : 128);
   p.tn_split = tp.nsplit;
   p.tn_chunk = tp.chunk;
   p.tn_tile = tp.wide ? pf::kTNWTile : 128;
@@ -1259,6 +1283,18 @@ pf::TNArgs tn_args(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, con
   a.Wout = dWblk;
   a.T = T;
   a.scale_w = a.scale_lr = 1.f;
+  if (tn_pairs(L, (int)dtype, T, r, mixed)) {
+    fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV, 64);
+    a.items = L->d_tn_items_p; a.n_items = (int)L->tn_items_p.size();
+    a.n_order = 0;
+    *plan = tn_plan_wide(pf::tn_items_total(a, 64, pf::kTNWTile), T);
+    plan->pairs = true;
+    plan->pair_off = align256(plan->ws);
+    plan->ws = plan->pair_off + (L->pair_src.size() / 4) * 64 * 64 * 2;
+    a.nsplit = plan->nsplit;
+    a.chunk = plan->chunk;
+    return a;
+  }
   fill_tn_regions(a, L, r, dY, X, T_lr, S, dU, dV);
   if (tn_wide(L, (int)dtype, T, r, mixed)) {
     a.items = L->d_tn_items_w; a.n_items = (int)L->tn_items_w.size();
@@ -1280,13 +1316,25 @@ pf_status enqueue_tn(const pf_layout *L, int dt, pf::TNArgs a, const TNPlan &p, 
                      hipStream_t s) {
   a.partials = ws;
   if (p.wide) {
+    const int blk = p.pairs ? 64 : L->b;
+    void *const dW = a.Wout;
+    if (p.pairs) a.Wout = (char *)ws + p.pair_off;
     {
       Timed t(PF_KERNEL_SDDMM, s);
-      pf_status st = hip_status(pf::launch_tnw(L->b, p.grid, a, s), "weight-gradient kernel");
-      if (st != PF_OK || p.shared <= 0) return st;
+      pf_status st = hip_status(pf::launch_tnw(blk, p.grid, a, s), "weight-gradient kernel");
+      if (st != PF_OK) return st;
     }
+    if (p.shared > 0) {
+      Timed t(PF_KERNEL_REDUCE, s);
+      pf_status st =
+          hip_status(pf::launch_tnw_reduce(blk, p.shared, a, s), "weight-gradient reduction");
+      if (st != PF_OK) return st;
+    }
+    if (!p.pairs) return PF_OK;
     Timed t(PF_KERNEL_REDUCE, s);
-    return hip_status(pf::launch_tnw_reduce(L->b, p.shared, a, s), "weight-gradient reduction");
+    return hip_status(pf::launch_pair_scatter(a.Wout, L->d_pair_src, (int)(L->pair_src.size() / 4),
+                                              dW, s),
+                      "pair scatter kernel");
   }
   {
     Timed t(PF_KERNEL_SDDMM, s);

@@ -335,37 +335,62 @@ std::string build_layout_from_mask(pf_layout &L, int32_t nb_out, int32_t nb_in, 
   return finish_layout(L);
 }
 
-// Backward-data pair lists (see pf_layout): b = 32 and even block counts
-// only.  Pair rows of a pair column ascending.
-static void build_bwd_pairs(pf_layout &L) {
+// Pair lists of b = 32 layouts with even block counts (see pf_layout): the
+// pair block-CSR, each pair block's sources, one backward-data tile per pair
+// column (pair rows ascending) and the weight-gradient items.
+static void build_pairs(pf_layout &L) {
   L.bwd_tiles_p.clear();
   L.kcols_bwd_p.clear();
   L.blks_bwd_p.clear();
   L.pair_src.clear();
+  L.pr_ptr.clear();
+  L.pr_col.clear();
+  L.tn_items_p.clear();
   L.kmax_bwd_p = 0;
   if (L.b != 32 || L.nb_out % 2 || L.nb_in % 2) return;
-  std::vector<int32_t> prs;
-  for (int32_t q = 0; q < L.nb_in / 2; ++q) {
-    prs.clear();
-    for (int32_t j = 2 * q; j < 2 * q + 2; ++j)
-      for (int32_t p = L.col_ptr[j]; p < L.col_ptr[j + 1]; ++p) prs.push_back(L.row_idx[p] / 2);
-    std::sort(prs.begin(), prs.end());
-    prs.erase(std::unique(prs.begin(), prs.end()), prs.end());
+  const int32_t npr = L.nb_out / 2, npc = L.nb_in / 2;
+  L.pr_ptr.assign(1, 0);
+  std::vector<int32_t> cols;
+  for (int32_t R = 0; R < npr; ++R) {
+    cols.clear();
+    for (int32_t i = 2 * R; i < 2 * R + 2; ++i)
+      for (int32_t p = L.row_ptr[i]; p < L.row_ptr[i + 1]; ++p) cols.push_back(L.col_idx[p] / 2);
+    std::sort(cols.begin(), cols.end());
+    cols.erase(std::unique(cols.begin(), cols.end()), cols.end());
+    for (int32_t Q : cols) {
+      L.pr_col.push_back(Q);
+      for (int a = 0; a < 2; ++a)
+        for (int c = 0; c < 2; ++c) L.pair_src.push_back(csr_pos(L, 2 * R + a, 2 * Q + c));
+    }
+    L.pr_ptr.push_back((int32_t)L.pr_col.size());
+  }
+  // Backward-data: per pair column, its pair rows (ascending) and their ids.
+  std::vector<std::vector<int32_t>> rows_of(npc), ids_of(npc);
+  for (int32_t R = 0; R < npr; ++R)
+    for (int32_t id = L.pr_ptr[R]; id < L.pr_ptr[R + 1]; ++id) {
+      rows_of[L.pr_col[id]].push_back(R);
+      ids_of[L.pr_col[id]].push_back(id);
+    }
+  for (int32_t q = 0; q < npc; ++q) {
     NTTile t{};
     t.g = 1;
-    t.nsteps = (int32_t)prs.size();
+    t.nsteps = (int32_t)rows_of[q].size();
     t.kcol_off = (int32_t)L.kcols_bwd_p.size();
     t.blk_off = (int32_t)L.blks_bwd_p.size();
     for (int g = 0; g < kMaxG; ++g) t.out_blk[g] = g == 0 ? q : -1;
-    for (int32_t r : prs) {
-      L.kcols_bwd_p.push_back(r);
-      L.blks_bwd_p.push_back((int32_t)(L.pair_src.size() / 4));
-      for (int a = 0; a < 2; ++a)
-        for (int c = 0; c < 2; ++c) L.pair_src.push_back(csr_pos(L, 2 * r + a, 2 * q + c));
-    }
+    L.kcols_bwd_p.insert(L.kcols_bwd_p.end(), rows_of[q].begin(), rows_of[q].end());
+    L.blks_bwd_p.insert(L.blks_bwd_p.end(), ids_of[q].begin(), ids_of[q].end());
     L.kmax_bwd_p = std::max(L.kmax_bwd_p, t.nsteps);
     L.bwd_tiles_p.push_back(t);
   }
+  // Weight-gradient items over the pair block-CSR, as for b = 64.
+  pf_layout P;
+  P.b = 64;
+  P.nb_out = npr;
+  P.nb_in = npc;
+  P.row_ptr = L.pr_ptr;
+  P.col_idx = L.pr_col;
+  build_tn_items(P, 4, L.tn_items_p);
 }
 
 // CSC, work lists and their self-check, from row_ptr / col_idx.
@@ -405,7 +430,7 @@ std::string finish_layout(pf_layout &L) {
       [&](int col, int c) { return L.tperm[L.col_ptr[col] + c]; }, L.G_bwd_w,
       L.bwd_tiles_w, L.kcols_bwd_w, L.blks_bwd_w);
   build_tn_items(L);
-  build_bwd_pairs(L);
+  build_pairs(L);
   L.kmax_fwd = L.kmax_bwd = 0;
   for (auto &t : L.fwd_tiles) L.kmax_fwd = std::max(L.kmax_fwd, (int)t.nsteps);
   for (auto &t : L.bwd_tiles) L.kmax_bwd = std::max(L.kmax_bwd, (int)t.nsteps);
@@ -470,6 +495,29 @@ std::string check_layout(const pf_layout &L) {
     }
     for (int v : seen)
       if (v != 1) return "backward-data pairs do not cover each kept block exactly once";
+    // Weight-gradient items over the pair blocks: each pair block once, at
+    // its pair block-CSR position.
+    const size_t npair = L.pair_src.size() / 4;
+    std::vector<int> pseen(npair, 0);
+    auto pair_pos = [&](int R, int Q) -> int32_t {
+      auto b = L.pr_col.begin() + L.pr_ptr[R], e = L.pr_col.begin() + L.pr_ptr[R + 1];
+      auto it = std::lower_bound(b, e, Q);
+      return (it != e && *it == Q) ? (int32_t)(it - L.pr_col.begin()) : -1;
+    };
+    for (auto &it : L.tn_items_p)
+      for (int a = 0; a < kTNMax; ++a)
+        for (int b = 0; b < kTNMax; ++b) {
+          const int32_t p = it.out_blk[a * kTNMax + b];
+          if (a < it.na && b < it.nb) {
+            if (it.a_col[a] < 0 || it.a_col[a] >= L.nb_out / 2 || p != pair_pos(it.a_col[a], it.b_col[b]))
+              return "weight-gradient pair item block index mismatch";
+            if (p >= 0) pseen[p]++;
+          } else if (p != -1) {
+            return "weight-gradient pair item padding not empty";
+          }
+        }
+    for (int v : pseen)
+      if (v != 1) return "weight-gradient pair items do not cover each pair block exactly once";
   }
   auto items = [&](const std::vector<TNItem> &list, const char *what) -> std::string {
     std::fill(seen.begin(), seen.end(), 0);

@@ -41,6 +41,12 @@ struct pf_layout {
   std::vector<pf::NTTile> bwd_tiles_p;
   std::vector<int32_t> kcols_bwd_p, blks_bwd_p, pair_src;
   int kmax_bwd_p = 0;
+  // The pair blocks as a block-CSR of their own (pair rows x pair columns,
+  // pair block ids in this order, pair_src indexed by them) and the
+  // weight-gradient items of the 256 x 256 kernel over it (bundles of four
+  // pair rows x runs of four pair columns).
+  std::vector<int32_t> pr_ptr, pr_col;
+  std::vector<pf::TNItem> tn_items_p;
 
   // Device copies (valid after pf_layout_upload).
   int device = -1;
@@ -53,6 +59,7 @@ struct pf_layout {
   const int32_t *d_kcols_bwd_w = nullptr, *d_blks_bwd_w = nullptr;
   const pf::TNItem *d_tn_items = nullptr, *d_tn_items_w = nullptr;
   const pf::NTTile *d_bwd_tiles_p = nullptr;
+  const pf::TNItem *d_tn_items_p = nullptr;
   const int32_t *d_kcols_bwd_p = nullptr, *d_blks_bwd_p = nullptr, *d_pair_src = nullptr;
   const int32_t *d_row_ptr = nullptr, *d_col_idx = nullptr;
   const int32_t *d_col_ptr = nullptr, *d_row_idx = nullptr;

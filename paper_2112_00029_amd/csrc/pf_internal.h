@@ -163,6 +163,10 @@ hipError_t launch_nt(int dtype, int blk, int G, bool b_kn, int bm, const NTArgs 
 // src[4p .. 4p + 3] name (-1: zeros).
 hipError_t launch_pair_gather(const void *W, const int32_t *src, int npair, void *Wp,
                               hipStream_t s);
+// The weight gradient's way back: the blocks of pair blocks Wp[p] that
+// src names (>= 0) copied to their places in W.
+hipError_t launch_pair_scatter(const void *Wp, const int32_t *src, int npair, void *W,
+                               hipStream_t s);
 // bf16 NT family with direct global -> LDS operand copies (gemm_dma.hip).
 // The output tile is G * blk = 64, 128 or 256 columns wide (the token tile
 // follows: 256, 128, 256).  For 128-column tiles `variant` picks 512-token

@@ -36,6 +36,9 @@ hipError_t launch_tnw_reduce(int, int, const TNArgs &, hipStream_t) { no_kernels
 hipError_t launch_pair_gather(const void *, const int32_t *, int, void *, hipStream_t) {
   no_kernels("pair_gather");
 }
+hipError_t launch_pair_scatter(const void *, const int32_t *, int, void *, hipStream_t) {
+  no_kernels("pair_scatter");
+}
 hipError_t launch_tn_reduce(int, int, const TNArgs &, hipStream_t) { no_kernels("tn_reduce"); }
 hipError_t launch_skinny(bool, const SkinnyArgs &, hipStream_t) { no_kernels("skinny"); }
 hipError_t launch_mix_dgamma(int, const void *, const void *, int64_t, const float *, int,

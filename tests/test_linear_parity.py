@@ -308,16 +308,17 @@ def test_large_layer_T4096_all_outputs(b):
         # workgroup per item, nothing shared, no second pass.
         assert plan["tn_tile"] == 256 and plan["tn_items"] == 208 and plan["tn_shared"] == 0, plan
     else:
-        assert plan["tn_tile"] == 128 and plan["tn_items"] >= 512 and plan["tn_split"] > 1, plan
-        # Backward-data on 64-wide pair tiles (no two 32-wide block columns
-        # share their kept rows), after the pair-block gather.
+        # Pair blocks (64 x 64): the weight gradient on 208 items of 256 x 256
+        # as at b = 64, then the scatter of the kept quarters; backward-data
+        # on 64-wide pair tiles after the pair-block gather.
+        assert plan["tn_tile"] == 256 and plan["tn_items"] == 208 and plan["tn_shared"] == 0, plan
         assert (plan["bwd_tile_n"], plan["bwd_direct_lds"]) == (64, 1), plan
     inp = _inputs(n_out, n_in, b, ms, T, r, "bf16")
     out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", inp["raw"], timing=True)
     # T_lr and S split their K range; the weight gradient splits its tokens
     # (128 x 128) or shares items between workgroups (256 x 256), except
-    # with one workgroup per item (b = 64: no second pass); b = 32 adds the
-    # pair-block gather.
+    # with one workgroup per item (b = 64 and b = 32: no second pass); b = 32
+    # adds the pair-block gather and scatter.
     assert _reductions(kt) == {128: 3, 64: 2, 32: 4}[b], kt
     got = {k: to_host(v) for k, v in out.items()}
     ref = _oracle(inp, r, b)
@@ -327,7 +328,8 @@ def test_large_layer_T4096_all_outputs(b):
 
 
 @pytest.mark.parametrize("T,r,b", [(2509, 256, 128), (2049, 256, 128), (2509, 128, 128),
-                                   (2509, 256, 64), (2049, 128, 64)])
+                                   (2509, 256, 64), (2049, 128, 64), (2509, 256, 32),
+                                   (2049, 128, 32)])
 def test_large_layer_ragged_T_wide_weight_gradient(T, r, b):
     """The 16384 x 4096 layer at b = 128 with a token count that is not a
     multiple of the 32-token step: the 256 x 256 weight gradient's segments
@@ -336,8 +338,9 @@ def test_large_layer_ragged_T_wide_weight_gradient(T, r, b):
     empty (one 128-column or 128-row block of the 256 x 256 tile), so waves
     whose quarter holds nothing skip their MFMAs and the stores drop the
     empty half.  At b = 64 (208 items, one workgroup per item) every item
-    runs whole over the ragged token range.  Every output element against
-    the oracle."""
+    runs whole over the ragged token range; b = 32 runs the same way on its
+    pair blocks (64 x 64, dropped quarters computed and not stored) and
+    scatters them.  Every output element against the oracle."""
     from paper_2112_00029_amd import pixelfly as pf
     n_out, n_in, ms = LARGE["n_out"], LARGE["n_in"], LARGE["ms"]
     plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
@@ -378,7 +381,7 @@ def test_large_layer_full_size_sampled(large_full_inputs, b):
     plan = pf.pf_linear_plan_get(pf.pf_layout_create(n_out, n_in, b, ms), "bf16", T, r)
     print(f"[plan b={b} T={T}] {plan}", flush=True)
     assert plan["lowrank_t_kernel"] == 2 and plan["lowrank_s_kernel"] == 2, plan
-    assert plan["tn_tile"] == (256 if b in (128, 64) else 128), plan
+    assert plan["tn_tile"] == 256, plan
     assert (plan["lowrank_s_tile_n"], plan["lowrank_s_split"]) == (256, 4), plan
     M, (row_ptr, col_idx, *_x) = om.layout(n_out, n_in, b, ms)
     nnzb = int(M.sum())
@@ -386,7 +389,7 @@ def test_large_layer_full_size_sampled(large_full_inputs, b):
     raw = dict(inp["raw"], W=Wr)
     out, _L, kt = _run_gpu_dev(n_out, n_in, b, ms, T, r, "bf16", raw, timing=True)
     splits = sum(int(plan[k] > 1) for k in ("lowrank_t_split", "lowrank_s_split", "tn_split"))
-    gather = int(b == 32)  # b = 32: backward-data on 64-wide pair tiles
+    gather = 2 * int(b == 32)  # b = 32: pair-block gather and scatter
     if b == 32:
         assert (plan["bwd_tile_n"], plan["bwd_direct_lds"]) == (64, 1), plan
     assert _reductions(kt) == splits + int(plan["tn_shared"] > 0) + gather, (kt, plan)
