@@ -76,6 +76,25 @@ def test_tiled_layouts_group_rows():
     assert st["G_bwd_wide"] == 4 and st["bwd_tiles_wide"] == 16
 
 
+def test_pair_block_plans():
+    """b = 32 layers with T x K >= 4M and a rank that is a multiple of 64 run
+    backward-data on 64-wide pair tiles and the weight gradient on pair items
+    of 256 x 256; smaller products, odd ranks and fp32 keep the 32-wide
+    tiles (host planning only, no kernel runs)."""
+    L = pf.pf_layout_create(16384, 4096, 32, 32)
+    p = pf.pf_linear_plan_get(L, "bf16", 16384, 256)
+    assert (p["bwd_tile_n"], p["bwd_direct_lds"]) == (64, 1), p
+    assert (p["tn_tile"], p["tn_items"], p["tn_shared"], p["tn_split"]) == (256, 208, 0, 1), p
+    # room for the pair blocks (1280 of 64 x 64 bf16) on top of the rest
+    assert p["workspace_bytes"] >= 1280 * 64 * 64 * 2
+    for T, r, dt in [(512, 256, "bf16"), (16384, 96, "bf16"), (16384, 256, "fp32")]:
+        q = pf.pf_linear_plan_get(L, dt, T, r)
+        assert q["bwd_tile_n"] == 32 and q["tn_tile"] == 128, (T, r, dt, q)
+    # 2048 tokens x 1024: below 4M, the gather would not pay
+    q = pf.pf_linear_plan_get(pf.pf_layout_create(1024, 1024, 32, 32), "bf16", 2048, 64)
+    assert q["bwd_tile_n"] == 32, q
+
+
 def test_layout_create_errors():
     for args in [(100, 64, 32, 2), (64, 64, 0, 2), (64, 64, 32, 3), (64, 64, 32, 0), (0, 64, 32, 1)]:
         with pytest.raises(pf.PixelflyError) as e:
