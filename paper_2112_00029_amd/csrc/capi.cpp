@@ -284,6 +284,7 @@ struct SkinnyPlan {
   int nsplit;
   size_t ws;
   int G;  // output blocks per tile (128 or 256 columns)
+  int blk = 0;  // block width of the product's K-steps and output blocks
 };
 SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
   SkinnyPlan p{dtype == 0 ? 128 : 64, 1, 0, 128 / blk};
@@ -331,6 +332,25 @@ SkinnyPlan skinny_plan(int dtype, int blk, int64_t T, int kblocks, int r) {
     p.nsplit = (int)ns;
     p.ws = (size_t)ns * T * r * sizeof(float);
   }
+  return p;
+}
+
+// Block width of a rank-r product: the products are dense, so bf16 takes
+// 128 (else 64) when r and K allow it, whatever the layout's b: b = 32
+// blocks would give K-steps of 32-column (64-byte) row halves (S = dY U at
+// 16384 x 4096 b = 32: 157 -> 132 us).  fp32 keeps b.
+int rank_blk(const pf_layout *L, int dtype, int32_t r, int64_t K) {
+  if (dtype == PF_BF16)
+    for (int cb : {128, 64})
+      if (r % cb == 0 && K % cb == 0) return cb;
+  return L->b;
+}
+// Plan of T_lr = X V^T (s_side false, K = n_in) or S = dY U (K = n_out).
+SkinnyPlan rank_plan(const pf_layout *L, int dtype, int64_t T, int32_t r, bool s_side) {
+  const int64_t K = s_side ? L->n_out : L->n_in;
+  const int rb = rank_blk(L, dtype, r, K);
+  SkinnyPlan p = skinny_plan(dtype, rb, T, (int)(K / rb), r);
+  p.blk = rb;
   return p;
 }
 
@@ -924,8 +944,8 @@ size_t pf_workspace_bytes(const pf_layout *L, int64_t T, int32_t r, pf_dtype dty
                   &wp);
     tnw = wp.ws;
   }
-  const size_t fwd = skinny_plan(dtype, L->b, T, L->nb_in, r).ws;
-  const size_t sws = skinny_plan(dtype, L->b, T, L->nb_out, r).ws;
+  const size_t fwd = rank_plan(L, (int)dtype, T, r, false).ws;
+  const size_t sws = rank_plan(L, (int)dtype, T, r, true).ws;
   const size_t pws = pair_ws_bytes(L, (int)dtype, T, r);
   const size_t bwd = pws ? align256(sws) + pws : sws;
   return std::max({tn, tnw, fwd, bwd}) + mix_dgamma_bytes(items);
@@ -942,6 +962,7 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
   pf_linear_plan p{};
   // Rank-r products: the same decisions as enqueue of T_lr and S.
   auto rank = [&](int64_t K, int kblocks, bool b_kn, int32_t *v) {
+    (void)kblocks;
     if (r <= 0) return;
     if (use_skinny(dt, T, r, K)) {
       v[0] = 1;
@@ -950,11 +971,11 @@ pf_status pf_linear_plan_get(const pf_layout *L, pf_dtype dtype, int64_t T, int3
       v[3] = 64;
       return;
     }
-    const SkinnyPlan sp = skinny_plan(dtype, b, T, kblocks, r);
-    const int G = sp.G;
-    const NTChoice c = nt_choose(dt, b, G, sp.bm, (kblocks + sp.nsplit - 1) / sp.nsplit, T,
-                                 (r / b + G - 1) / G, sp.nsplit, true);
-    (void)b_kn;
+    const SkinnyPlan sp = rank_plan(L, dt, T, r, b_kn);
+    const int G = sp.G, rb = sp.blk;
+    const int ksteps = (int)(K / rb);
+    const NTChoice c = nt_choose(dt, rb, G, sp.bm, (ksteps + sp.nsplit - 1) / sp.nsplit, T,
+                                 (r / rb + G - 1) / G, sp.nsplit, true);
     v[0] = 2;
     v[1] = sp.nsplit;
     v[2] = c.bm;
@@ -1053,7 +1074,7 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
   if (epi != PF_EPI_NONE && epi != PF_EPI_GELU) return fail(PF_ERR_INVALID_ARG, "bad epilogue");
   if (epi == PF_EPI_GELU && (st = need_ptr(Y_pre, "Y_pre")) != PF_OK) return st;
   if (epi == PF_EPI_NONE && Y_pre) return fail(PF_ERR_INVALID_ARG, "Y_pre given without GELU epilogue");
-  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_in, r);
+  const SkinnyPlan sp = rank_plan(L, (int)dtype, T, r, false);
   if ((st = need_ws(sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;
   hipStream_t s = (hipStream_t)stream;
@@ -1063,10 +1084,11 @@ pf_status linear_fwd(const pf_layout *L, pf_dtype dtype, int64_t T, int32_t r, c
                      s, "T_lr kernel");
     if (st != PF_OK) return st;
   } else if (r > 0) {
-    // T_lr = X V^T: dense NT over K, r/b output blocks.
-    st = dense_nt(PF_KERNEL_LOWRANK_T, dt, b, sp.G, false, sp.bm, T, X, L->n_in, V, L->n_in, L->nb_in,
-                  r / b, T_lr, r, sp.nsplit,
-                  (float *)workspace, s, "T_lr kernel");
+    // T_lr = X V^T: dense NT over K, r / blk output blocks.
+    const int rb = sp.blk;
+    st = dense_nt(PF_KERNEL_LOWRANK_T, dt, rb, sp.G, false, sp.bm, T, X, L->n_in, V, L->n_in,
+                  (int)(L->n_in / rb), r / rb, T_lr, r, sp.nsplit, (float *)workspace, s,
+                  "T_lr kernel");
     if (st != PF_OK) return st;
   }
   pf::NTArgs a{};
@@ -1156,9 +1178,9 @@ pf_status enqueue_s(const pf_layout *L, int dt, int64_t T, int32_t r, const void
   if (use_skinny(dt, T, r, L->n_out))
     return skinny_bf16(PF_KERNEL_LOWRANK_S, true, T, dY, L->n_out, U, r, (int)L->n_out, r, S, s,
                        "S kernel");
-  const int b = L->b;
-  return dense_nt(PF_KERNEL_LOWRANK_S, dt, b, sp.G, true, sp.bm, T, dY, L->n_out, U, r,
-                  L->nb_out, r / b, S, r, sp.nsplit, ws, s, "S kernel");
+  const int rb = sp.blk;
+  return dense_nt(PF_KERNEL_LOWRANK_S, dt, rb, sp.G, true, sp.bm, T, dY, L->n_out, U, r,
+                  (int)(L->n_out / rb), r / rb, S, r, sp.nsplit, ws, s, "S kernel");
 }
 
 // dX = dY (M o W) + S V (optionally times gelu'(aux)).  pair_ws: room for
@@ -1356,7 +1378,7 @@ pf_status pf_linear_bwd_data(const pf_layout *L, pf_dtype dtype, int64_t T, int3
                              void *workspace, size_t ws_bytes, void *stream) {
   pf_status st = check_bwd_data_args(L, dtype, T, r, dY, Wblk, U, V, S, dX, epi, aux);
   if (st != PF_OK) return st;
-  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
+  const SkinnyPlan sp = rank_plan(L, (int)dtype, T, r, true);
   const size_t pws = pair_ws_bytes(L, (int)dtype, T, r);
   if ((st = need_ws(pws ? align256(sp.ws) + pws : sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;
@@ -1387,7 +1409,7 @@ pf_status pf_linear_bwd_data_mixed(const pf_layout *L, pf_dtype dtype, int64_t T
   pf_status st = check_gamma(gamma);
   if (st != PF_OK) return st;
   if ((st = check_bwd_data_args(L, dtype, T, r, dY, Wblk, U, V, S, dX, epi, aux)) != PF_OK) return st;
-  const SkinnyPlan sp = skinny_plan(dtype, L->b, T, L->nb_out, r);
+  const SkinnyPlan sp = rank_plan(L, (int)dtype, T, r, true);
   const size_t pws = pair_ws_bytes(L, (int)dtype, T, r);
   if ((st = need_ws(pws ? align256(sp.ws) + pws : sp.ws, workspace, ws_bytes)) != PF_OK) return st;
   if ((st = check_state(L)) != PF_OK) return st;

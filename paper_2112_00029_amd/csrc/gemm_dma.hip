@@ -266,10 +266,18 @@ __global__ __launch_bounds__(64 * NW, OCC) void ntd_kernel(NTArgs a_arg) {
       a_src(t, h, base, bytes, ldb, colb);
       const rsrc_t r = make_rsrc(base, bytes);
       const uint32_t vrow = a_row * ldb;
+      // Dense mode with B read [k][n] on 256-wide tiles is S = dY U of a
+      // wide layer: it streams the whole of dY once, and non-temporal copies
+      // keep those lines from displacing the rest of the cache (16384 x
+      // 4096: S 144 -> 132 us; backward-data, which reads dY next, 2 us
+      // slower).  Not on the 128-wide tiles of narrower products (the MLP
+      // pair's S: its GELU backward-data then lost 6 us), nor for X in
+      // T_lr = X V^T (the forward re-reads X right after).
+      constexpr int AAUX = (DENSE && BKN && BN == 256) ? 2 : 0;
       sfor<AWW>([&](auto i) __attribute__((always_inline)) {
         const int wr = wr0 + i;
-        dma16(r, st.a + (wa0 + i) * 1024, vrow + a_c16[i & 1],
-              (uint32_t)(wr * RPWA) * ldb + colb);
+        dma16<AAUX>(r, st.a + (wa0 + i) * 1024, vrow + a_c16[i & 1],
+                    (uint32_t)(wr * RPWA) * ldb + colb);
       });
     }
     sfor<PPW>([&](auto pi) __attribute__((always_inline)) {

@@ -51,8 +51,11 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *p, int64_t bytes) {
 
 // One 1 KiB window: lane i copies 16 bytes from rsrc + voff + soff to
 // lds + 16 i.
+// AUX: the copy's cache policy bits (0: default; 2: non-temporal, for an
+// operand that one launch streams through once).
+template <int AUX = 0>
 __device__ __forceinline__ void dma16(rsrc_t r, uint8_t *lds, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, (int)voff, (int)soff, 0, 0);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, (int)voff, (int)soff, 0, AUX);
 }
 
 // Load of work-list metadata (tile lists, column and block indices) through
