@@ -106,3 +106,32 @@ def test_attention_single_block_sequence():
     """Sequence of one 64-row block (every row keeps exactly one block, the
     prefetched next-block index clamps onto it), five heads."""
     _run(1, 5, 64, 1, heads=[(0, 0), (0, 4)])
+
+
+def test_attention_repeat_calls_bitwise():
+    """Forward and backward of the 8 x 12 x 4096 global-stripe workload (the
+    grouped and the plain kernels, many workgroups per CU) three times on the
+    same inputs: every output identical to the bit.  Each output element is
+    summed in a fixed order, so any difference would be a race."""
+    torch = torch_cuda()
+    from paper_2112_00029_amd import pixelfly as pf
+    B, H, S, d, b, ms, g = 8, 12, 4096, 64, 64, 64, 1
+    print(f"[attn-repeat] B={B} H={H} S={S} global_blocks={g}", flush=True)
+    draw = lambda sid: to_dev(synth.draw((B, H, S, d), 1.0, 5, sid, "bf16")[1])
+    q, k, v, do = draw(11), draw(12), draw(13), draw(14)
+    L = pf.pf_layout_create_attention(S, b, ms, g)
+    pf.pf_layout_upload(L)
+    wsb = pf.pf_attn_workspace_bytes(B, H, S)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    runs = []
+    for _ in range(3):
+        O = empty((B, H, S, d), "bf16")
+        lse = torch.empty((B, H, S), dtype=torch.float32, device="cuda")
+        pf.pf_attn_fwd(L, B, H, S, d, 1.0 / np.sqrt(d), q, k, v, O, lse)
+        dQ, dK, dV = (empty((B, H, S, d), "bf16") for _ in range(3))
+        pf.pf_attn_bwd(L, B, H, S, d, 1.0 / np.sqrt(d), q, k, v, O, lse, do, dQ, dK, dV, ws, wsb)
+        torch.cuda.synchronize()
+        runs.append({"O": O, "lse": lse, "dQ": dQ, "dK": dK, "dV": dV})
+    for r in runs[1:]:
+        for name in runs[0]:
+            assert torch.equal(r[name], runs[0][name]), name

@@ -242,10 +242,14 @@ def test_mlp_pair_gelu(T):
         check_close(k, to_host(g), rf, dtype)
 
 
-def test_repeat_calls_are_deterministic():
-    """Split-token weight gradients combine partials in a fixed order: two
-    runs give identical bits (and the completion counters reset)."""
-    n_out, n_in, b, ms, T, r = 3072, 768, 32, 16, 4096, 96
+@pytest.mark.parametrize("n_out,n_in,b,ms,T,r", [
+    (3072, 768, 32, 16, 4096, 96),   # split-token weight gradient
+    (2048, 1024, 32, 16, 4100, 64),  # b = 32 backward-data on pair blocks
+    (8320, 512, 32, 16, 600, 64),    # forward in bands of output tiles
+])
+def test_repeat_calls_are_deterministic(n_out, n_in, b, ms, T, r):
+    """Split-token weight gradients combine partials in a fixed order, and no
+    output is summed by racing workgroups: two runs give identical bits."""
     inp = _inputs(n_out, n_in, b, ms, T, r, "bf16", seed=3)
     a, _ = _run_gpu(n_out, n_in, b, ms, T, r, "bf16", inp)
     c, _ = _run_gpu(n_out, n_in, b, ms, T, r, "bf16", inp)
