@@ -49,8 +49,14 @@ def test_cover_layout_parity(n, p, d, T):
         check_close(k, got[k], ref[k], "bf16")
 
 
-@pytest.mark.parametrize("b,T,r", [(32, 300, 32), (64, 520, 64)])
-def test_empty_block_columns_with_lowrank(b, T, r):
+@pytest.mark.parametrize("b,T,r,empty_cols", [
+    (32, 300, 32, (0, 9, 23)),
+    (64, 520, 64, (0, 9, 23)),
+    # b = 32 on pair blocks (T x K >= 4M): pair column 11 = block columns
+    # 22, 23 keeps nothing, pair columns 0 and 4 keep one of their two
+    (32, 5500, 64, (0, 9, 22, 23)),
+])
+def test_empty_block_columns_with_lowrank(b, T, r, empty_cols):
     """Block masks whose first, an inner and the last block column keep no
     block: the backward-data tiles of those columns have no kept step and
     carry only the low-rank term (dX columns = (dY U) V there)."""
@@ -61,9 +67,9 @@ def test_empty_block_columns_with_lowrank(b, T, r):
     print(f"[empty-cols] n={n} b={b} T={T} r={r}", flush=True)
     rng = np.random.default_rng([2112, b])
     Mb = rng.random((nb, nb)) < 0.2
-    Mb[:, [0, 9, nb - 1]] = False
-    Mb[np.arange(nb), rng.choice([j for j in range(nb) if j not in (0, 9, nb - 1)], nb)] = True
-    assert not Mb[:, 0].any() and not Mb[:, nb - 1].any() and Mb.any(axis=1).all()
+    Mb[:, list(empty_cols)] = False
+    Mb[np.arange(nb), rng.choice([j for j in range(nb) if j not in empty_cols], nb)] = True
+    assert not Mb[:, list(empty_cols)].any() and Mb.any(axis=1).all()
     row_ptr, col_idx, *_r = om.block_csr(Mb)
     nnzb = int(Mb.sum())
     X, Xr = synth.draw((T, n), 0.02, 3, 1, "bf16")
@@ -74,6 +80,8 @@ def test_empty_block_columns_with_lowrank(b, T, r):
     Wd = ol.unpack(W, row_ptr, col_idx, nb, nb, b)
     L = pf.pf_layout_create_from_mask(nb, nb, b, Mb.astype(np.uint8))
     pf.pf_layout_upload(L)
+    plan = pf.pf_linear_plan_get(L, "bf16", T, r)
+    assert (plan["bwd_tile_n"] == 64) == (b == 64 or T * n >= (1 << 22)), plan
     x, w, u, v, dy = (to_dev(a) for a in (Xr, Wr, Ur, Vr, dYr))
     Y, Tl, S, dX = empty((T, n), "bf16"), empty((T, r), "bf16"), empty((T, r), "bf16"), empty((T, n), "bf16")
     dW, dU, dV = empty((nnzb, b, b), "bf16"), empty((n, r), "bf16"), empty((r, n), "bf16")
@@ -92,5 +100,5 @@ def test_empty_block_columns_with_lowrank(b, T, r):
     for k in ref:
         check_close(k, got[k], ref[k], "bf16")
     # the empty columns of dX hold only the low-rank term
-    cols = np.r_[0:b, (nb - 1) * b:n]
+    cols = np.concatenate([np.arange(j * b, (j + 1) * b) for j in empty_cols])
     check_close("dX empty columns", got["dX"][:, cols], (g["S"] @ V)[:, cols], "bf16")
